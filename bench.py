@@ -1,0 +1,288 @@
+#!/usr/bin/env python3
+"""Throughput of the generalized Allreduce on one MI355X.
+
+Kolmakov & Zhang, "A Generalization of the Allreduce Operation"
+(arXiv:2004.09362).  P virtual ranks live on one GPU; one bench step runs
+the workload's Allreduce(s) once through the C-ABI library (libar.so).
+
+Metric: effective Allreduce bandwidth = P * n * element bytes / time (summed
+over the workload's instances), and the achieved algorithmic HBM bandwidth
+of the dominant kernel against the MI355X peak of 8 TB/s.
+
+Workloads (seeded synthetic rank buffers, resident in HBM before timing):
+  small_batch (default)  P in {5, 6, 7, 12}, n = 106 fp32 N(0,1) (about the
+                         425-byte average message the paper quotes), 65536
+                         instances per launch, latency-optimal k = ceil(log2 P)
+  gradsync               P = 24, n = 2^24 fp32 N(0,1e-3), k = 10
+  prime_sweep            P = 37, n = 2^22 fp32 U(-1,1), --k in 6..12 (default 12)
+  large                  P = 127, n = 2^26 fp32 N(0,1e-2), --k 14 (default) or 10
+  prime3                 P = 3, n = 1024 int32 U[-1000,1000], --k 2..4 (default 4)
+
+Each step uses one of several input sets in turn, so that the sets together
+exceed the 256 MB Infinity Cache and every step reads HBM.
+
+Prints ONE JSON line.  Only one GPU is used: --gpus above 1 exits with an error.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "effective allreduce GB/s (P*n*bytes/s) and achieved HBM GB/s vs peak, 1 GPU"
+HBM_PEAK_GBPS = 8000.0
+POOL_BYTES = 1 << 30  # rotate input sets until they span at least this much
+
+
+def log(msg):
+    print("[bench] " + msg, file=sys.stderr, flush=True)
+
+
+def ceil_log2(P):
+    return max(0, (P - 1).bit_length())
+
+
+def jobs_for(name, k_arg):
+    from paper_2004_09362_amd import synth
+    import numpy as np
+
+    w = synth.WORKLOADS[name]
+    jobs = []
+    for P in w["P"]:
+        if w["ks"] == "lo":
+            k = ceil_log2(P)
+        else:
+            k = k_arg if k_arg is not None else DEFAULT_K[name]
+            if k not in w["ks"]:
+                raise SystemExit("k=%d is not one of the %s workload's k values %s" % (k, name, w["ks"]))
+        jobs.append(dict(P=P, n=w["n"], batch=w["batch"], k=k, op=w["ops"][0],
+                         dtype=np.dtype(w["dtype"]), dist=w["dist"], seed=w["seed"]))
+    return w, jobs
+
+
+DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4}
+
+DESCRIPTIONS = {
+    "small_batch": "small_batch: P in {5,6,7,12}, n=106 fp32 N(0,1), 65536 instances per launch, k=ceil(log2 P), sum",
+    "gradsync": "gradsync: P=24, n=16777216 fp32 N(0,1e-3), k=10 (bandwidth-optimal), sum",
+    "prime_sweep": "prime_sweep: P=37, n=4194304 fp32 U(-1,1), k=%d, sum",
+    "large": "large: P=127, n=67108864 fp32 N(0,1e-2), k=%d, sum",
+    "prime3": "prime3: P=3, n=1024 int32 U[-1000,1000], k=%d, sum",
+}
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in ("kernels.hip", "capi.cpp", "plan.cpp", "ar_internal.hpp"):
+        with open(os.path.join(ROOT, "paper_2004_09362_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def traffic_from_profiles(workload, kernel, src_hash):
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel sources; else None."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        with open(path) as fh:
+            data = json.load(fh)
+        ent = data.get(workload, {}).get(kernel)
+        if not ent or ent.get("source_hash") != src_hash:
+            return None
+        return ent.get("bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def cpu_baseline(jobs, host_sets, budget_s=12.0):
+    """The CPU oracle (single thread, as it stands) on a bounded sample."""
+    import numpy as np
+
+    import oracle
+
+    oracle.lib()
+    total_bytes, total_t, parts = 0, 0.0, []
+    per_job_budget = budget_s / len(jobs)
+    for job, x in zip(jobs, host_sets):
+        P, n, B, k = job["P"], job["n"], job["batch"], job["k"]
+        if B > 1:
+            b = 64
+            while True:
+                t0 = time.perf_counter()
+                oracle.allreduce_batched(np.ascontiguousarray(x[:, :b]), k, job["op"])
+                dt = time.perf_counter() - t0
+                if dt >= per_job_budget or b >= x.shape[1]:
+                    break
+                b = min(x.shape[1], max(b * 2, int(b * per_job_budget / max(dt, 1e-3))))
+            total_bytes += P * n * b * job["dtype"].itemsize
+            parts.append("P=%d: %d of %d instances" % (P, b, B))
+        else:
+            # sampled columns: `c` per block, the same replay as a full run at those columns
+            q = n // P
+            c = 256
+            while True:
+                cols = np.unique(np.concatenate([np.arange(bb * q, bb * q + min(c, q)) for bb in range(P)]))
+                xs = np.ascontiguousarray(x[:, cols])
+                t0 = time.perf_counter()
+                oracle.allreduce(xs, k, job["op"], n=n, cols=cols)
+                dt = time.perf_counter() - t0
+                if dt >= per_job_budget or c >= q:
+                    break
+                c = min(q, max(c * 2, int(c * per_job_budget / max(dt, 1e-3))))
+            b = len(cols)
+            total_bytes += P * b * job["dtype"].itemsize
+            parts.append("P=%d: %d of %d columns" % (P, b, n))
+        total_t += dt
+    return {"value": round(total_bytes / total_t / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "; ".join(parts) + " (single-threaded C replay, %.1f s)" % total_t}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--workload", default="small_batch",
+                    choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3"])
+    ap.add_argument("--k", type=int, default=None)
+    ap.add_argument("--path", choices=["auto", "stepwise", "fused"], default="auto")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the P ranks are virtual ranks held on a single MI355X, and "
+              "runs across several GPUs are not part of this library (asked for --gpus %d)" % args.gpus,
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2004_09362_amd import ar, synth
+
+    steps = args.steps if args.steps is not None else (10 if args.workload == "large" else 20)
+    warmup = args.warmup if args.warmup is not None else (2 if args.workload == "large" else 5)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w, jobs = jobs_for(args.workload, args.k)
+    path = {"auto": ar.AR_PATH_AUTO, "stepwise": ar.AR_PATH_STEPWISE, "fused": ar.AR_PATH_FUSED}[args.path]
+
+    # ---- plans and resident inputs ----
+    set_bytes = sum(j["P"] * j["n"] * j["batch"] * j["dtype"].itemsize for j in jobs)
+    n_sets = int(max(1, min(steps + warmup, -(-POOL_BYTES // set_bytes))))
+    plans, sets = [], []
+    for j in jobs:
+        p = ar.Plan(j["P"], j["n"], j["dtype"].name, j["op"], j["k"], path=path)
+        plans.append(p)
+    log("workload %s: %d job(s), %d input set(s) of %.1f MB" % (args.workload, len(jobs), n_sets, set_bytes / 1e6))
+    for s in range(n_sets):
+        per = []
+        for j in jobs:
+            X = synth.device_ranks(j["seed"] + 7919 * s, j["P"], j["n"] * j["batch"], j["dtype"], j["dist"], dev)
+            per.append(X)
+        sets.append(per)
+    host_sets = None
+    if not args.no_cpu_baseline:
+        host_sets = []
+        for j, X in zip(jobs, sets[0]):
+            if j["batch"] > 1:
+                nb = min(j["batch"], 8192)
+                host_sets.append(X.view(j["P"], j["batch"], j["n"])[:, :nb].cpu().numpy())
+            else:
+                host_sets.append(X.cpu().numpy())
+    ptr_tables = [[[X[i] for i in range(j["P"])] for j, X in zip(jobs, per)] for per in sets]
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+
+    def run_step(s, events=None):
+        for jj, (j, p) in enumerate(zip(jobs, plans)):
+            if events is not None:
+                events[jj].record(stream)
+            p.batched(ptr_tables[s % n_sets][jj], j["batch"], j["n"], stream)
+        if events is not None:
+            events[len(jobs)].record(stream)
+
+    for s in range(warmup):
+        run_step(s)
+    torch.cuda.synchronize()
+
+    # ---- timed region: exactly `steps` steps ----
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(jobs) + 1)] for _ in range(steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start.record(stream)
+    for s in range(steps):
+        run_step(warmup + s, ev[s])
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = start.elapsed_time(stop)
+
+    per_job_ms = [0.0] * len(jobs)
+    for s in range(steps):
+        for jj in range(len(jobs)):
+            per_job_ms[jj] += ev[s][jj].elapsed_time(ev[s][jj + 1])
+    per_job_ms = [m / steps for m in per_job_ms]
+
+    eff_bytes = sum(j["P"] * j["n"] * j["batch"] * j["dtype"].itemsize for j in jobs)
+    ms_per_step = total_ms / steps
+    value = eff_bytes / (ms_per_step * 1e-3) / 1e9
+
+    # ---- roofline of the dominant kernel ----
+    dom = max(range(len(jobs)), key=lambda jj: per_job_ms[jj])
+    dj, dp = jobs[dom], plans[dom]
+    st = dp.stats()
+    fused = (path == ar.AR_PATH_FUSED) or (path == ar.AR_PATH_AUTO and st.fused_ok)
+    alg_bytes = (st.hbm_bytes_fused if fused else st.hbm_bytes_stepwise) * dj["batch"]
+    launches = 1 if fused else st.launches
+    bytes_per_launch = alg_bytes / launches
+    launch_ms = per_job_ms[dom] / launches
+    achieved = bytes_per_launch / (launch_ms * 1e-3) / 1e9
+    kname = ("fused_lo_kernel<P=%d>" % dj["P"]) if fused else "step_kernel"
+    src_hash = kernel_source_hash()
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_from_profiles(args.workload, kname, src_hash),
+            "kernel": kname, "bytes_per_launch": int(bytes_per_launch), "launch_ms": round(launch_ms, 5),
+            "launches_per_step": launches}
+    step_alg = 0
+    for j, p in zip(jobs, plans):
+        s2 = p.stats()
+        f2 = (path == ar.AR_PATH_FUSED) or (path == ar.AR_PATH_AUTO and s2.fused_ok)
+        step_alg += (s2.hbm_bytes_fused if f2 else s2.hbm_bytes_stepwise) * j["batch"]
+
+    desc = DESCRIPTIONS[args.workload]
+    if "%d" in desc:
+        desc = desc % jobs[0]["k"]
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int32" if jobs[0]["dtype"] == np.int32 else "f32",
+        "data": "synthetic (seeded; %d rotating input sets resident in HBM)" % n_sets,
+        "config": {"workload": desc, "P": [j["P"] for j in jobs], "n": jobs[0]["n"], "batch": jobs[0]["batch"],
+                   "k": [j["k"] for j in jobs], "op": jobs[0]["op"],
+                   "path": "fused" if fused else "stepwise", "parallelism": "1 GPU, P virtual ranks"},
+        "hbm_algorithmic_GBps_step": round(step_alg / (ms_per_step * 1e-3) / 1e9, 1),
+        "per_job_ms": {str(j["P"]): round(m, 5) for j, m in zip(jobs, per_job_ms)},
+        "wall_s_timed": round(wall, 4),
+        "roofline": roof,
+        "source_hash": src_hash,
+    }
+    if host_sets is not None:
+        log("timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(jobs, host_sets)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,161 @@
+/*
+ * ar.h -- C ABI of the MI355X generalized Allreduce library (libar.so).
+ *
+ * The operation is Allreduce as defined in Kolmakov & Zhang, "A
+ * Generalization of the Allreduce Operation" (arXiv:2004.09362), Sec. 1: P
+ * ranks each own a vector of n elements; afterwards every rank holds the
+ * elementwise combination of all P vectors.  Here the P ranks are virtual:
+ * P device buffers on one GPU.  The schedule is the paper's permutation-group
+ * algorithm over the cyclic group T_P with generator x -> x+1 (Sec. 5):
+ *   - reduction phase of the bandwidth-optimal algorithm (Sec. 7), run once
+ *     or, for fewer steps, shifted by s = 0 .. min(2^r, P)-1 (Sec. 8);
+ *   - distribution phase: the reduction steps reversed without combination
+ *     (Sec. 7), of which the first r are omitted (Sec. 8; r = ceil(log2 P)
+ *     is the latency-optimal version of Sec. 9).
+ * k_steps = 2*ceil(log2 P) - r, anywhere in [ceil(log2 P), 2*ceil(log2 P)].
+ *
+ * Conventions shared by all entry points:
+ *   - Every function returns an ar_status; AR_OK is 0.  On failure nothing
+ *     has been enqueued and ar_last_error() (per thread) describes it.
+ *   - Device pointers are plain HIP device addresses on the current device.
+ *     Host arrays (the table of rank pointers) are read during the call only.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream)
+ *     and the call returns without waiting.  Faults inside a kernel surface
+ *     at the caller's next synchronisation.
+ *   - The library never reads or writes host memory asynchronously and never
+ *     falls back to a CPU path: without a usable GPU, execute calls return
+ *     AR_ERR_NO_DEVICE.
+ */
+#ifndef AR_H_
+#define AR_H_
+
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  AR_OK = 0,
+  AR_ERR_INVALID_ARG = 1,   /* bad P, n, k, pointer, batch or stride      */
+  AR_ERR_UNSUPPORTED = 2,   /* dtype/op/path combination not provided     */
+  AR_ERR_ALIAS = 3,         /* two rank buffers overlap                   */
+  AR_ERR_OUT_OF_MEMORY = 4, /* workspace allocation failed                */
+  AR_ERR_HIP = 5,           /* a HIP runtime call failed                  */
+  AR_ERR_NO_DEVICE = 6,     /* no usable GPU                              */
+  AR_ERR_INTERNAL = 7       /* the plan failed its own consistency check  */
+} ar_status;
+
+typedef enum { AR_INT32 = 0, AR_FLOAT32 = 1 } ar_dtype;
+
+/* Combination function of Sec. 5.4.  AR_SUM on int32 wraps modulo 2^32.
+ * AR_MAX keeps the received value only when it is strictly greater than the
+ * kept one (so of -0.0 and +0.0 the kept value stays). */
+typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
+
+/* How ar_execute runs a plan.
+ *   STEPWISE: one kernel launch per communication step of the schedule
+ *             (2*ceil(log2 P) - r launches, plus one local copy when P = 2,
+ *             k = 1), each pulling the peer's blocks out of HBM.
+ *   FUSED:    one launch that keeps every step of the latency-optimal
+ *             schedule in registers, column by column, for many
+ *             independent instances (small messages, Sec. 1's 425-byte
+ *             average); only latency-optimal plans with P <= 16.
+ *   AUTO:     FUSED where it applies, STEPWISE otherwise.
+ * Both paths combine exactly the same operand pairs in the same order, so
+ * their results are bit-identical. */
+typedef enum { AR_PATH_AUTO = 0, AR_PATH_STEPWISE = 1, AR_PATH_FUSED = 2 } ar_path;
+
+typedef struct ar_plan ar_plan; /* opaque; owned by the caller between create and destroy */
+
+/* Sizes of a plan (per Allreduce instance).  Block counts follow the paper's
+ * cost equations (Secs. 7-9): a rank receives 2(P-1) blocks in the
+ * bandwidth-optimal schedule, P*ceil(log2 P) in the latency-optimal one. */
+typedef struct {
+  int32_t P, L, k, r, w;             /* L = ceil(log2 P), r = 2L - k, w = min(2^r, P)   */
+  int32_t rs_steps, ag_steps;        /* reduction / distribution steps; sum is k         */
+  int32_t launches;                  /* kernel launches of the STEPWISE path              */
+  int32_t fused_ok;                  /* 1 if the FUSED path can run this plan             */
+  int64_t n, elem_bytes;
+  int64_t blocks_pulled_per_rank;    /* same for every rank (translation invariance)     */
+  int64_t bytes_pulled_per_rank_min; /* blocks differ by at most one element in length   */
+  int64_t bytes_pulled_per_rank_max;
+  int64_t bytes_pulled_total;        /* over all ranks = blocks_pulled_per_rank * n * e  */
+  int64_t combines_per_rank;         /* block combinations                               */
+  int64_t hbm_bytes_stepwise;        /* algorithmic HBM bytes of the STEPWISE path       */
+  int64_t hbm_bytes_fused;           /* 2 * P * n * e: read every input, write every output */
+  int64_t workspace_bytes;           /* device scratch per instance, STEPWISE path       */
+} ar_stats;
+
+/* One launch of the STEPWISE path: a list of placement ranges.  In a range,
+ * every rank x works on placements p = p0 .. p0+count-1 (mod P); placement p
+ * of rank x is block (x - p) mod P of its vector (Sec. 5.1 with h =
+ * identity).  kind COPY: dst = src; REDUCE: dst = own (+) src; REDUCE2:
+ * dst = own (+) src and dst2 = own2 (+) src.  own/dst buffers belong to rank
+ * x, src to rank (x + delta) mod P; all at the same block.  Buffer ids: 0 is
+ * the caller's rank buffer, 1 and 2 the plan's two scratch buffers, -1 none. */
+typedef struct {
+  int32_t phase;     /* 0 reduction, 1 distribution, 2 local copy */
+  int32_t n_ranges;
+} ar_launch_desc;
+
+typedef struct {
+  int32_t p0, count, kind, delta;
+  int32_t dst, own, dst2, own2, src;
+} ar_range_desc;
+
+enum { AR_KIND_COPY = 0, AR_KIND_REDUCE = 1, AR_KIND_REDUCE2 = 2 };
+
+/* Build the schedule for P ranks, n elements per rank and k_steps steps
+ * (Secs. 7-9).  Host work only: validates, derives the per-step placement
+ * ranges, assigns buffers, proves every launch free of read/write overlap
+ * between ranks, and computes the sizes.  No device memory is touched.
+ *   P in [1, 128]; n >= 0; k_steps in [ceil(log2 P), 2*ceil(log2 P)]
+ *   (k_steps = 0 for P = 1); dtype/op from the enums above.
+ * Errors: AR_ERR_INVALID_ARG (range), AR_ERR_UNSUPPORTED (dtype/op),
+ * AR_ERR_INTERNAL (consistency check failed).  *out_plan is set on AR_OK. */
+ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_plan** out_plan);
+
+/* Choose the execution path (default AR_PATH_AUTO).  AR_ERR_UNSUPPORTED if
+ * FUSED is asked for and the plan cannot run fused. */
+ar_status ar_plan_set_path(ar_plan* plan, ar_path path);
+
+/* Allreduce in place.  rank_buffers: host array of P device pointers, rank
+ * x's n elements at rank_buffers[x].  Pointers must be 4-byte aligned and
+ * must not overlap (AR_ERR_ALIAS); 16-byte aligned buffers take the
+ * vectorised kernels.  The first call on a plan that needs scratch (r > 0,
+ * STEPWISE) allocates it on the current device; it is reused afterwards.
+ * A plan must not run on two streams at once (shared scratch). */
+ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t stream);
+
+/* `batch` independent Allreduce instances per rank: instance j of rank x is
+ * the n elements at rank_buffers[x] + j * instance_stride (in elements,
+ * instance_stride >= n).  Each instance is split into blocks on its own. */
+ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
+                             hipStream_t stream);
+
+/* Sizes of the plan; AR_ERR_INVALID_ARG for NULL arguments. */
+ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out);
+
+/* Introspection of the STEPWISE launches (host side, for tests and tools):
+ * number of launches, and launch i's description with up to `cap` ranges. */
+ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* out);
+ar_status ar_plan_launch(const ar_plan* plan, int32_t i, ar_launch_desc* desc, ar_range_desc* ranges, int32_t cap);
+
+/* Wait for the plan's last stream, free its scratch and the plan.  NULL is
+ * accepted.  Must not be called while another thread executes the plan. */
+void ar_plan_destroy(ar_plan* plan);
+
+/* Static text for a status code. */
+const char* ar_status_string(ar_status s);
+
+/* Detail of the last failure on the calling thread ("" if none). */
+const char* ar_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AR_H_ */

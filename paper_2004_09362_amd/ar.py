@@ -1,0 +1,219 @@
+"""Thin Python binding of libar.so (``include/ar.h``).
+
+Argument marshalling only: every function forwards to the C entry point of
+the same name, and all arithmetic happens in the library's HIP kernels.
+PyTorch is used for device memory and streams: rank buffers are torch
+tensors (or raw device addresses), the stream is torch's current stream
+unless one is given.  There is no fallback: if the built library is absent
+the import fails, and on a machine without a GPU the execute calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+import torch  # noqa: F401  (loads the HIP runtime torch was built with, before libar.so)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libar.so")
+
+AR_OK, AR_ERR_INVALID_ARG, AR_ERR_UNSUPPORTED, AR_ERR_ALIAS = 0, 1, 2, 3
+AR_ERR_OUT_OF_MEMORY, AR_ERR_HIP, AR_ERR_NO_DEVICE, AR_ERR_INTERNAL = 4, 5, 6, 7
+AR_INT32, AR_FLOAT32 = 0, 1
+AR_SUM, AR_MAX = 0, 1
+AR_PATH_AUTO, AR_PATH_STEPWISE, AR_PATH_FUSED = 0, 1, 2
+AR_KIND_COPY, AR_KIND_REDUCE, AR_KIND_REDUCE2 = 0, 1, 2
+
+EXPORTS = [
+    "ar_plan_create", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
+    "ar_plan_num_launches", "ar_plan_launch", "ar_plan_destroy", "ar_status_string", "ar_last_error",
+]
+
+
+class ArError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        super().__init__("%s: %s (%s)" % (where, detail, status_name(status)))
+        self.status = status
+
+
+class Stats(ctypes.Structure):
+    _fields_ = [
+        ("P", ctypes.c_int32), ("L", ctypes.c_int32), ("k", ctypes.c_int32), ("r", ctypes.c_int32),
+        ("w", ctypes.c_int32), ("rs_steps", ctypes.c_int32), ("ag_steps", ctypes.c_int32),
+        ("launches", ctypes.c_int32), ("fused_ok", ctypes.c_int32),
+        ("n", ctypes.c_int64), ("elem_bytes", ctypes.c_int64),
+        ("blocks_pulled_per_rank", ctypes.c_int64),
+        ("bytes_pulled_per_rank_min", ctypes.c_int64), ("bytes_pulled_per_rank_max", ctypes.c_int64),
+        ("bytes_pulled_total", ctypes.c_int64), ("combines_per_rank", ctypes.c_int64),
+        ("hbm_bytes_stepwise", ctypes.c_int64), ("hbm_bytes_fused", ctypes.c_int64),
+        ("workspace_bytes", ctypes.c_int64),
+    ]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class LaunchDesc(ctypes.Structure):
+    _fields_ = [("phase", ctypes.c_int32), ("n_ranges", ctypes.c_int32)]
+
+
+class RangeDesc(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int32) for name in
+                ("p0", "count", "kind", "delta", "dst", "own", "dst2", "own2", "src")]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libar.so is not built (%s); run `python -m paper_2004_09362_amd.build`" % LIB_PATH)
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    L.ar_plan_create.argtypes = [i32, i64, ctypes.c_int, ctypes.c_int, i32, ctypes.POINTER(vp)]
+    L.ar_plan_set_path.argtypes = [vp, ctypes.c_int]
+    L.ar_execute.argtypes = [vp, ctypes.POINTER(vp), vp]
+    L.ar_execute_batched.argtypes = [vp, ctypes.POINTER(vp), i64, i64, vp]
+    L.ar_plan_stats.argtypes = [vp, ctypes.POINTER(Stats)]
+    L.ar_plan_num_launches.argtypes = [vp, ctypes.POINTER(i32)]
+    L.ar_plan_launch.argtypes = [vp, i32, ctypes.POINTER(LaunchDesc), ctypes.POINTER(RangeDesc), i32]
+    L.ar_plan_destroy.argtypes = [vp]
+    L.ar_plan_destroy.restype = None
+    L.ar_status_string.argtypes = [ctypes.c_int]
+    L.ar_status_string.restype = ctypes.c_char_p
+    L.ar_last_error.argtypes = []
+    L.ar_last_error.restype = ctypes.c_char_p
+    for name in ("ar_plan_create", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
+                 "ar_plan_num_launches", "ar_plan_launch"):
+        getattr(L, name).restype = ctypes.c_int
+    return L
+
+
+lib = _load()
+
+
+def status_name(s: int) -> str:
+    return lib.ar_status_string(int(s)).decode()
+
+
+def ar_last_error() -> str:
+    return lib.ar_last_error().decode()
+
+
+def ar_status_string(s: int) -> str:
+    return status_name(s)
+
+
+def _check(st: int, where: str):
+    if st != AR_OK:
+        raise ArError(st, where, ar_last_error())
+
+
+def _dtype_code(dtype) -> int:
+    if dtype in (torch.int32, "int32", AR_INT32):
+        return AR_INT32
+    if dtype in (torch.float32, "float32", AR_FLOAT32):
+        return AR_FLOAT32
+    raise ArError(AR_ERR_UNSUPPORTED, "dtype", "int32 or float32 only, got %r" % (dtype,))
+
+
+def _op_code(op) -> int:
+    return {"sum": AR_SUM, "max": AR_MAX, AR_SUM: AR_SUM, AR_MAX: AR_MAX}[op]
+
+
+def ar_plan_create(P: int, n: int, dtype, op, k_steps: int) -> int:
+    h = ctypes.c_void_p()
+    _check(lib.ar_plan_create(P, n, _dtype_code(dtype), _op_code(op), k_steps, ctypes.byref(h)), "ar_plan_create")
+    return h.value
+
+
+def ar_plan_set_path(plan: int, path: int):
+    _check(lib.ar_plan_set_path(plan, int(path)), "ar_plan_set_path")
+
+
+def _ptr_table(rank_buffers) -> ctypes.Array:
+    addrs = []
+    for b in rank_buffers:
+        addrs.append(b.data_ptr() if isinstance(b, torch.Tensor) else int(b))
+    return (ctypes.c_void_p * len(addrs))(*addrs)
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def ar_execute(plan: int, rank_buffers: Sequence, stream=None):
+    tbl = _ptr_table(rank_buffers)
+    _check(lib.ar_execute(plan, tbl, _stream_handle(stream)), "ar_execute")
+
+
+def ar_execute_batched(plan: int, rank_buffers: Sequence, batch: int, instance_stride: int, stream=None):
+    tbl = _ptr_table(rank_buffers)
+    _check(lib.ar_execute_batched(plan, tbl, batch, instance_stride, _stream_handle(stream)), "ar_execute_batched")
+
+
+def ar_plan_stats(plan: int) -> Stats:
+    s = Stats()
+    _check(lib.ar_plan_stats(plan, ctypes.byref(s)), "ar_plan_stats")
+    return s
+
+
+def ar_plan_num_launches(plan: int) -> int:
+    v = ctypes.c_int32()
+    _check(lib.ar_plan_num_launches(plan, ctypes.byref(v)), "ar_plan_num_launches")
+    return v.value
+
+
+def ar_plan_launch(plan: int, i: int):
+    d = LaunchDesc()
+    _check(lib.ar_plan_launch(plan, i, ctypes.byref(d), None, 0), "ar_plan_launch")
+    rs = (RangeDesc * max(1, d.n_ranges))()
+    _check(lib.ar_plan_launch(plan, i, ctypes.byref(d), rs, d.n_ranges), "ar_plan_launch")
+    return d.phase, [rs[j].as_dict() for j in range(d.n_ranges)]
+
+
+def ar_plan_destroy(plan: int):
+    lib.ar_plan_destroy(plan)
+
+
+class Plan:
+    """Owning handle around ``ar_plan*``."""
+
+    def __init__(self, P: int, n: int, dtype, op="sum", k: int | None = None, path: int = AR_PATH_AUTO):
+        L = max(0, (P - 1).bit_length())
+        self.P, self.n = P, n
+        self.k = 2 * L if k is None else k
+        self.handle = ar_plan_create(P, n, dtype, op, self.k)
+        if path != AR_PATH_AUTO:
+            ar_plan_set_path(self.handle, path)
+
+    def set_path(self, path: int):
+        ar_plan_set_path(self.handle, path)
+
+    def stats(self) -> Stats:
+        return ar_plan_stats(self.handle)
+
+    def launches(self):
+        return [ar_plan_launch(self.handle, i) for i in range(ar_plan_num_launches(self.handle))]
+
+    def __call__(self, rank_buffers, stream=None):
+        ar_execute(self.handle, rank_buffers, stream)
+
+    def batched(self, rank_buffers, batch: int, instance_stride: int, stream=None):
+        ar_execute_batched(self.handle, rank_buffers, batch, instance_stride, stream)
+
+    def close(self):
+        if self.handle:
+            ar_plan_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,93 @@
+// ar_internal.hpp -- types shared by the host plan generator, the C ABI and
+// the HIP kernels of libar.so.
+#pragma once
+
+#include <cstdint>
+#include <string>
+#include <vector>
+
+namespace ar {
+
+constexpr int kMaxP = 128;       // largest supported number of ranks
+constexpr int kMaxRanges = 8;    // placement ranges per launch
+constexpr int kFusedMaxP = 16;   // largest P of the register-resident fused kernel
+
+enum Buf : int32_t { kBufNone = -1, kBufU = 0, kBufX = 1, kBufY = 2 };
+enum Kind : int32_t { kCopy = 0, kReduce = 1, kReduce2 = 2 };
+enum Phase : int32_t { kPhaseReduce = 0, kPhaseDistribute = 1, kPhaseLocal = 2 };
+
+// One range of placements worked on by every rank in a launch.
+struct Range {
+  int32_t p0, count, kind, delta;
+  int32_t dst, own, dst2, own2, src;
+};
+
+struct Launch {
+  int32_t phase;
+  std::vector<Range> ranges;
+};
+
+// The schedule and its sizes; built on the host (plan.cpp).
+struct Schedule {
+  int32_t P = 1, L = 0, k = 0, r = 0, w = 1;
+  int64_t n = 0;
+  std::vector<int32_t> N, f, c;  // N_i, floor(N_i/2), ceil(N_i/2)
+  std::vector<Launch> launches;
+  int32_t rs_steps = 0, ag_steps = 0;
+  bool uses_scratch = false;
+  // sizes per instance
+  int64_t blocks_pulled_per_rank = 0;
+  int64_t combines_per_rank = 0;
+  int64_t hbm_blocks = 0;  // block reads + writes per rank, STEPWISE path
+};
+
+// Builds the schedule; returns an empty string or the reason it failed.
+std::string build_schedule(int32_t P, int64_t n, int32_t k, Schedule* out);
+
+// Verifies that no launch of `s` lets one work item write a location that a
+// different work item reads or writes.  Returns "" or a description.
+std::string check_hazards(const Schedule& s);
+
+// Balanced partition: block b of n elements over P blocks.
+inline int64_t block_off(int64_t n, int32_t P, int32_t b) {
+  const int64_t q = n / P, m = n % P;
+  return b * q + (b < m ? b : m);
+}
+inline int64_t block_len(int64_t n, int32_t P, int32_t b) {
+  const int64_t q = n / P, m = n % P;
+  return q + (b < m ? 1 : 0);
+}
+
+// ----- device launch interface (kernels.hip) -----
+
+struct DevRange {
+  int32_t p0, count, kind, delta;
+  int32_t dst, own, dst2, own2, src;
+  int32_t first;  // index of the range's first op among the launch's ops
+};
+
+struct StepArgs {
+  void* user[kMaxP];        // rank buffers
+  char* scratch[2];         // X and Y: rank y's region at scratch[i] + y * scratch_rank_stride elements
+  int64_t scratch_rank_stride;
+  int64_t n, stride, batch;
+  int64_t q, m;             // n / P, n % P
+  int64_t tiles_per_seg;
+  int32_t P, n_ranges, total_ops, pad;
+  DevRange ranges[kMaxRanges];
+};
+
+struct FusedArgs {
+  void* user[kMaxP];
+  int64_t n, stride, batch;
+  int64_t groups;           // column groups (vector path) or columns (scalar path)
+};
+
+// dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.
+int launch_step(const StepArgs& a, int dtype, int op, bool vec, int grid, void* stream);
+int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, bool vec, int grid, void* stream);
+// Workgroups a step launch would use for `total_waves` wave tiles.
+int step_grid(int64_t total_tiles);
+int64_t step_tile_elems(bool vec);
+
+}  // namespace ar

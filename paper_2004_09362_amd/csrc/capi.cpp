@@ -1,0 +1,324 @@
+// capi.cpp -- the C ABI of libar.so (declared in include/ar.h).
+//
+// Argument checking, workspace management and launch orchestration.  The
+// schedule comes from plan.cpp, the kernels from kernels.hip; nothing here
+// computes on the host.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/ar.h"
+#include "ar_internal.hpp"
+
+struct ar_plan {
+  ar::Schedule s;
+  int32_t dtype = 0, op = 0;
+  int32_t path = AR_PATH_AUTO;
+  bool fused_ok = false;
+  void* scratch = nullptr;
+  size_t scratch_bytes = 0;
+  int scratch_device = -1;
+  hipStream_t last_stream = nullptr;
+  bool ran = false;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+ar_status fail(ar_status s, const std::string& msg) {
+  g_err = msg;
+  return s;
+}
+
+ar_status hip_fail(hipError_t e, const char* what) {
+  g_err = std::string(what) + ": " + hipGetErrorString(e);
+  return AR_ERR_HIP;
+}
+
+int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+
+// Check the table of rank pointers: non-null, 4-byte aligned, no overlap.
+// Returns AR_OK and whether every buffer is 16-byte aligned.
+ar_status check_buffers(const ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool* all16) {
+  const int32_t P = pl->s.P;
+  const int64_t extent = ((batch - 1) * stride + pl->s.n) * 4;
+  std::vector<std::pair<uintptr_t, int32_t>> sorted;
+  sorted.reserve(P);
+  *all16 = true;
+  for (int32_t x = 0; x < P; ++x) {
+    const uintptr_t p = reinterpret_cast<uintptr_t>(bufs[x]);
+    if (p == 0) return fail(AR_ERR_INVALID_ARG, "rank buffer " + std::to_string(x) + " is NULL");
+    if (p % 4 != 0) return fail(AR_ERR_INVALID_ARG, "rank buffer " + std::to_string(x) + " is not 4-byte aligned");
+    if (p % 16 != 0) *all16 = false;
+    sorted.push_back({p, x});
+  }
+  std::sort(sorted.begin(), sorted.end());
+  for (size_t i = 1; i < sorted.size(); ++i)
+    if (extent > 0 && sorted[i].first < sorted[i - 1].first + uintptr_t(extent))
+      return fail(AR_ERR_ALIAS, "rank buffers " + std::to_string(sorted[i - 1].second) + " and " +
+                                    std::to_string(sorted[i].second) + " overlap");
+  return AR_OK;
+}
+
+ar_status ensure_scratch(ar_plan* pl, size_t need, int device) {
+  if (pl->scratch && pl->scratch_bytes >= need && pl->scratch_device == device) return AR_OK;
+  if (pl->scratch) {
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(pl->scratch_device);
+    hipError_t e = hipFree(pl->scratch);  // waits for work that still uses it
+    (void)hipSetDevice(cur);
+    pl->scratch = nullptr;
+    pl->scratch_bytes = 0;
+    if (e != hipSuccess) return hip_fail(e, "hipFree(scratch)");
+  }
+  void* p = nullptr;
+  hipError_t e = hipMalloc(&p, need);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AR_ERR_OUT_OF_MEMORY, "scratch of " + std::to_string(need) + " bytes: " + hipGetErrorString(e));
+  }
+  pl->scratch = p;
+  pl->scratch_bytes = need;
+  pl->scratch_device = device;
+  return AR_OK;
+}
+
+ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool vec, hipStream_t stream,
+                       int device) {
+  const ar::Schedule& s = pl->s;
+  ar::StepArgs a;
+  std::memset(&a, 0, sizeof a);
+  for (int32_t x = 0; x < s.P; ++x) a.user[x] = bufs[x];
+  a.P = s.P;
+  a.n = s.n;
+  a.stride = stride;
+  a.batch = batch;
+  a.q = s.n / s.P;
+  a.m = s.n % s.P;
+  if (s.uses_scratch) {
+    // Scratch mirrors the caller's layout (same element index, same 16-byte
+    // phase), one region per rank, X then Y.
+    const int64_t rank_stride = round_up((batch - 1) * stride + s.n, 64);
+    const size_t need = size_t(2) * s.P * size_t(rank_stride) * 4;
+    ar_status st = ensure_scratch(pl, need, device);
+    if (st != AR_OK) return st;
+    a.scratch_rank_stride = rank_stride;
+    a.scratch[0] = static_cast<char*>(pl->scratch);
+    a.scratch[1] = static_cast<char*>(pl->scratch) + size_t(s.P) * size_t(rank_stride) * 4;
+  }
+  const int64_t max_len = a.q + (a.m ? 1 : 0);
+  const int64_t tile = ar::step_tile_elems(vec);
+  a.tiles_per_seg = std::max<int64_t>(1, (max_len + tile - 1) / tile);
+  for (const ar::Launch& l : s.launches) {
+    a.n_ranges = int32_t(l.ranges.size());
+    int32_t first = 0;
+    for (int32_t i = 0; i < a.n_ranges; ++i) {
+      const ar::Range& r = l.ranges[i];
+      a.ranges[i] = ar::DevRange{r.p0, r.count, r.kind, r.delta, r.dst, r.own, r.dst2, r.own2, r.src, first};
+      first += r.count;
+    }
+    a.total_ops = first;
+    const int64_t total_tiles = int64_t(s.P) * a.total_ops * batch * a.tiles_per_seg;
+    const int grid = ar::step_grid(total_tiles);
+    const int e = ar::launch_step(a, pl->dtype, pl->op, vec, grid, stream);
+    if (e != 0) return hip_fail(hipError_t(e), "step kernel launch");
+  }
+  return AR_OK;
+}
+
+ar_status run_fused(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool all16, hipStream_t stream) {
+  const ar::Schedule& s = pl->s;
+  ar::FusedArgs a;
+  std::memset(&a, 0, sizeof a);
+  for (int32_t x = 0; x < s.P; ++x) a.user[x] = bufs[x];
+  a.n = s.n;
+  a.stride = stride;
+  a.batch = batch;
+  const int64_t cols = batch * s.n;
+  const bool contiguous = (batch == 1 || stride == s.n);
+  const bool vec = all16 && contiguous && cols % 4 == 0;
+  a.groups = vec ? cols / 4 : cols;
+  int64_t blocks = (a.groups + 255) / 256;
+  blocks = std::min<int64_t>(std::max<int64_t>(blocks, 1), 256 * 64);
+  const int e = ar::launch_fused_lo(a, s.P, pl->dtype, pl->op, vec, int(blocks), stream);
+  if (e != 0) return hip_fail(hipError_t(e), "fused kernel launch");
+  return AR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_plan** out_plan) {
+  if (!out_plan) return fail(AR_ERR_INVALID_ARG, "out_plan is NULL");
+  *out_plan = nullptr;
+  if (int(dtype) != AR_INT32 && int(dtype) != AR_FLOAT32) return fail(AR_ERR_UNSUPPORTED, "dtype must be int32 or float32");
+  if (int(op) != AR_SUM && int(op) != AR_MAX) return fail(AR_ERR_UNSUPPORTED, "op must be sum or max");
+  ar_plan* pl = new (std::nothrow) ar_plan;
+  if (!pl) return fail(AR_ERR_OUT_OF_MEMORY, "plan allocation");
+  const std::string err = ar::build_schedule(P, n, k_steps, &pl->s);
+  if (!err.empty()) {
+    delete pl;
+    return fail(err.rfind("internal", 0) == 0 ? AR_ERR_INTERNAL : AR_ERR_INVALID_ARG, err);
+  }
+  pl->dtype = int32_t(dtype);
+  pl->op = int32_t(op);
+  pl->fused_ok = pl->s.P >= 2 && pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L;
+  *out_plan = pl;
+  g_err.clear();
+  return AR_OK;
+}
+
+ar_status ar_plan_set_path(ar_plan* plan, ar_path path) {
+  if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+  if (path != AR_PATH_AUTO && path != AR_PATH_STEPWISE && path != AR_PATH_FUSED)
+    return fail(AR_ERR_INVALID_ARG, "unknown path");
+  if (path == AR_PATH_FUSED && !plan->fused_ok)
+    return fail(AR_ERR_UNSUPPORTED, "the fused path runs latency-optimal plans with 2 <= P <= 16 only");
+  plan->path = path;
+  return AR_OK;
+}
+
+ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
+                             hipStream_t stream) {
+  if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+  if (!rank_buffers) return fail(AR_ERR_INVALID_ARG, "rank_buffers is NULL");
+  if (batch < 1) return fail(AR_ERR_INVALID_ARG, "batch must be >= 1");
+  if (batch == 1 && instance_stride < plan->s.n) instance_stride = plan->s.n;
+  if (instance_stride < plan->s.n) return fail(AR_ERR_INVALID_ARG, "instance_stride must be >= n");
+  bool all16 = false;
+  ar_status st = check_buffers(plan, rank_buffers, batch, instance_stride, &all16);
+  if (st != AR_OK) return st;
+  if (plan->s.P == 1 || plan->s.n == 0) return AR_OK;  // nothing to combine
+  int device = -1;
+  hipError_t he = hipGetDevice(&device);
+  if (he != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AR_ERR_NO_DEVICE, std::string("no usable GPU: ") + hipGetErrorString(he));
+  }
+  const int64_t elems = int64_t(plan->s.P) * plan->s.n * batch;
+  if (elems / batch / plan->s.P != plan->s.n) return fail(AR_ERR_INVALID_ARG, "size overflow");
+  const bool fused = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok);
+  if (fused) {
+    st = run_fused(plan, rank_buffers, batch, instance_stride, all16, stream);
+  } else {
+    const bool vec = all16 && (batch == 1 || instance_stride % 4 == 0);
+    st = run_stepwise(plan, rank_buffers, batch, instance_stride, vec, stream, device);
+  }
+  if (st == AR_OK) {
+    plan->last_stream = stream;
+    plan->ran = true;
+  }
+  return st;
+}
+
+ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t stream) {
+  return ar_execute_batched(plan, rank_buffers, 1, plan ? plan->s.n : 0, stream);
+}
+
+ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
+  if (!plan || !out) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+  const ar::Schedule& s = plan->s;
+  std::memset(out, 0, sizeof *out);
+  out->P = s.P;
+  out->L = s.L;
+  out->k = s.k;
+  out->r = s.r;
+  out->w = s.w;
+  out->rs_steps = s.rs_steps;
+  out->ag_steps = s.ag_steps;
+  out->launches = int32_t(s.launches.size());
+  out->fused_ok = plan->fused_ok ? 1 : 0;
+  out->n = s.n;
+  out->elem_bytes = 4;
+  out->blocks_pulled_per_rank = s.blocks_pulled_per_rank;
+  // bytes: rank x pulls block (x - p) for every pulled placement p
+  int64_t mn = INT64_MAX, mx = 0, total = 0;
+  for (int32_t x = 0; x < s.P; ++x) {
+    int64_t bytes = 0;
+    for (const ar::Launch& l : s.launches) {
+      std::vector<char> seen(size_t(3) * s.P, 0);
+      for (const ar::Range& rg : l.ranges) {
+        if (rg.delta == 0) continue;
+        for (int32_t j = 0; j < rg.count; ++j) {
+          const int32_t p = (rg.p0 + j) % s.P;
+          char& sn = seen[size_t(rg.src) * s.P + p];
+          if (sn) continue;
+          sn = 1;
+          const int32_t b = ((x - p) % s.P + s.P) % s.P;
+          bytes += ar::block_len(s.n, s.P, b) * 4;
+        }
+      }
+    }
+    mn = std::min(mn, bytes);
+    mx = std::max(mx, bytes);
+    total += bytes;
+  }
+  out->bytes_pulled_per_rank_min = s.P ? mn : 0;
+  out->bytes_pulled_per_rank_max = mx;
+  out->bytes_pulled_total = total;
+  out->combines_per_rank = s.combines_per_rank;
+  out->hbm_bytes_stepwise = s.hbm_blocks * s.n * 4;
+  out->hbm_bytes_fused = s.P > 1 ? int64_t(2) * s.P * s.n * 4 : 0;
+  out->workspace_bytes = s.uses_scratch ? int64_t(2) * s.P * round_up(s.n, 64) * 4 : 0;
+  return AR_OK;
+}
+
+ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* out) {
+  if (!plan || !out) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+  *out = int32_t(plan->s.launches.size());
+  return AR_OK;
+}
+
+ar_status ar_plan_launch(const ar_plan* plan, int32_t i, ar_launch_desc* desc, ar_range_desc* ranges, int32_t cap) {
+  if (!plan || !desc) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+  if (i < 0 || i >= int32_t(plan->s.launches.size())) return fail(AR_ERR_INVALID_ARG, "launch index out of range");
+  const ar::Launch& l = plan->s.launches[i];
+  desc->phase = l.phase;
+  desc->n_ranges = int32_t(l.ranges.size());
+  if (ranges) {
+    for (int32_t j = 0; j < desc->n_ranges && j < cap; ++j) {
+      const ar::Range& r = l.ranges[j];
+      ranges[j] = ar_range_desc{r.p0, r.count, r.kind, r.delta, r.dst, r.own, r.dst2, r.own2, r.src};
+    }
+  }
+  return AR_OK;
+}
+
+void ar_plan_destroy(ar_plan* plan) {
+  if (!plan) return;
+  if (plan->scratch) {
+    // hipFree waits for the device to finish the work that still uses it
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(plan->scratch_device);
+    (void)hipFree(plan->scratch);
+    (void)hipSetDevice(cur);
+  }
+  delete plan;
+}
+
+const char* ar_status_string(ar_status s) {
+  switch (s) {
+    case AR_OK: return "ok";
+    case AR_ERR_INVALID_ARG: return "invalid argument";
+    case AR_ERR_UNSUPPORTED: return "unsupported";
+    case AR_ERR_ALIAS: return "rank buffers overlap";
+    case AR_ERR_OUT_OF_MEMORY: return "out of device memory";
+    case AR_ERR_HIP: return "HIP runtime error";
+    case AR_ERR_NO_DEVICE: return "no usable GPU";
+    case AR_ERR_INTERNAL: return "internal consistency check failed";
+  }
+  return "unknown status";
+}
+
+const char* ar_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

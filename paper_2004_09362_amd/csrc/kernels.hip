@@ -1,0 +1,355 @@
+// kernels.hip -- HIP kernels of the generalized Allreduce for CDNA4 (gfx950).
+//
+// Kolmakov & Zhang, "A Generalization of the Allreduce Operation"
+// (arXiv:2004.09362).  Two kernels:
+//
+//  step_kernel   one communication step of the schedule (Secs. 7-9): every
+//                rank x, for each of its placements p in the launch's ranges,
+//                combines (or copies) block b = (x - p) mod P of its own
+//                buffer with the same block of rank (x + delta) mod P.  The
+//                work is pure streaming -- three (copy: two, dual: five)
+//                block-sized HBM accesses per item, one add per element --
+//                so the kernel is built for HBM bandwidth: 64-lane waves,
+//                16-byte loads, several loads in flight per lane before the
+//                first store, and no LDS (every byte is used exactly once,
+//                there is nothing to share across lanes).
+//
+//  fused_lo_kernel  the whole latency-optimal schedule (Sec. 9) for one
+//                column of P values held in registers: the primed vector
+//                R[x] and the starred S[x] of every rank, updated as the
+//                reduction steps prescribe, then S[x] written to rank x.
+//                The pairs combined are exactly those of the step-by-step
+//                path, so the results are bit-identical, but each input is
+//                read once and each output written once (2*P*n elements).
+//
+// Compiled with packed-fp32 instructions disabled; only adds and compares,
+// so no contraction question arises.
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "ar_internal.hpp"
+
+namespace ar {
+
+namespace {
+
+constexpr int kWave = 64;
+constexpr int kBlock = 256;           // 4 waves per workgroup
+constexpr int kUnrollVec = 4;         // 16-byte vectors per lane per tile
+constexpr int kUnrollScalar = 8;      // elements per lane per tile, scalar path
+constexpr int64_t kTileVec = int64_t(kWave) * 4 * kUnrollVec;     // 1024 elements
+constexpr int64_t kTileScalar = int64_t(kWave) * kUnrollScalar;   // 512 elements
+
+template <typename T>
+struct alignas(16) V4 {
+  T v[4];
+};
+
+template <int OP>
+__device__ __forceinline__ float comb(float a, float b) {
+  if constexpr (OP == 0) return a + b;
+  else return b > a ? b : a;
+}
+
+template <int OP>
+__device__ __forceinline__ int32_t comb(int32_t a, int32_t b) {
+  if constexpr (OP == 0) return int32_t(uint32_t(a) + uint32_t(b));
+  else return b > a ? b : a;
+}
+
+template <int OP, typename T>
+__device__ __forceinline__ V4<T> comb4(const V4<T>& a, const V4<T>& b) {
+  V4<T> r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) r.v[i] = comb<OP>(a.v[i], b.v[i]);
+  return r;
+}
+
+template <typename T>
+__device__ __forceinline__ T* buf_ptr(const StepArgs& a, int32_t buf, int32_t rank) {
+  if (buf == kBufU) return reinterpret_cast<T*>(a.user[rank]);
+  return reinterpret_cast<T*>(a.scratch[buf - 1]) + int64_t(rank) * a.scratch_rank_stride;
+}
+
+// One tile of one segment (one block of one rank for one placement), by one
+// wave.  The pointers are at the segment's first element; e0 is that
+// element's index inside the rank buffer (its 16-byte phase).
+template <typename T, int OP, int KIND, bool VEC>
+__device__ __forceinline__ void seg_tile(T* __restrict__ dst, const T* __restrict__ own, T* __restrict__ dst2,
+                                         const T* __restrict__ own2, const T* __restrict__ src, int64_t len,
+                                         int64_t e0, int64_t tile, int lane) {
+  if constexpr (VEC) {
+    int64_t head = (4 - (e0 & 3)) & 3;
+    if (head > len) head = len;
+    const int64_t nvec = (len - head) >> 2;
+    const int64_t tail0 = head + (nvec << 2);
+    const int64_t v0 = tile * (int64_t(kWave) * kUnrollVec);
+    if (v0 < nvec) {
+      const V4<T>* s4 = reinterpret_cast<const V4<T>*>(src + head);
+      const V4<T>* o4 = reinterpret_cast<const V4<T>*>(own + head);
+      const V4<T>* o24 = reinterpret_cast<const V4<T>*>(own2 + head);
+      V4<T>* d4 = reinterpret_cast<V4<T>*>(dst + head);
+      V4<T>* d24 = reinterpret_cast<V4<T>*>(dst2 + head);
+      V4<T> sv[kUnrollVec], ov[kUnrollVec], o2v[kUnrollVec];
+#pragma unroll
+      for (int u = 0; u < kUnrollVec; ++u) {
+        const int64_t v = v0 + u * kWave + lane;
+        if (v < nvec) {
+          sv[u] = s4[v];
+          if constexpr (KIND != kCopy) ov[u] = o4[v];
+          if constexpr (KIND == kReduce2) o2v[u] = o24[v];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kUnrollVec; ++u) {
+        const int64_t v = v0 + u * kWave + lane;
+        if (v < nvec) {
+          if constexpr (KIND == kCopy) {
+            d4[v] = sv[u];
+          } else {
+            d4[v] = comb4<OP>(ov[u], sv[u]);
+            if constexpr (KIND == kReduce2) d24[v] = comb4<OP>(o2v[u], sv[u]);
+          }
+        }
+      }
+    }
+    if (tile == 0) {
+      // at most 3 leading and 3 trailing elements, one per lane
+      int64_t e = -1;
+      if (lane < head) e = lane;
+      else if (lane >= 4 && lane - 4 < len - tail0) e = tail0 + (lane - 4);
+      if (e >= 0) {
+        if constexpr (KIND == kCopy) {
+          dst[e] = src[e];
+        } else {
+          const T sv1 = src[e];
+          dst[e] = comb<OP>(own[e], sv1);
+          if constexpr (KIND == kReduce2) dst2[e] = comb<OP>(own2[e], sv1);
+        }
+      }
+    }
+  } else {
+    const int64_t i0 = tile * kTileScalar;
+    T sv[kUnrollScalar], ov[kUnrollScalar], o2v[kUnrollScalar];
+#pragma unroll
+    for (int u = 0; u < kUnrollScalar; ++u) {
+      const int64_t e = i0 + u * kWave + lane;
+      if (e < len) {
+        sv[u] = src[e];
+        if constexpr (KIND != kCopy) ov[u] = own[e];
+        if constexpr (KIND == kReduce2) o2v[u] = own2[e];
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kUnrollScalar; ++u) {
+      const int64_t e = i0 + u * kWave + lane;
+      if (e < len) {
+        if constexpr (KIND == kCopy) {
+          dst[e] = sv[u];
+        } else {
+          dst[e] = comb<OP>(ov[u], sv[u]);
+          if constexpr (KIND == kReduce2) dst2[e] = comb<OP>(o2v[u], sv[u]);
+        }
+      }
+    }
+  }
+}
+
+// Work decomposition: tile t of the launch -> (rank x, op j, instance, tile
+// within the segment); consecutive waves stream consecutive tiles of one
+// block.  All of it is wave-uniform scalar arithmetic.
+template <typename T, int OP, bool VEC>
+__global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  // the wave index is uniform across the wave: keep the decomposition scalar
+  const int wave_in_block = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
+  const int64_t wave = int64_t(blockIdx.x) * (kBlock / kWave) + wave_in_block;
+  const int64_t nwaves = int64_t(gridDim.x) * (kBlock / kWave);
+  const int64_t tps = a.tiles_per_seg;
+  const int64_t total = int64_t(a.P) * a.total_ops * a.batch * tps;
+  const int32_t P = a.P;
+  for (int64_t t = wave; t < total; t += nwaves) {
+    const int64_t seg = t / tps;
+    const int64_t tile = t - seg * tps;
+    const int64_t inst = seg % a.batch;
+    const int64_t rest = seg / a.batch;
+    const int32_t j = int32_t(rest % a.total_ops);
+    const int32_t x = int32_t(rest / a.total_ops);
+    int ri = 0;
+    while (ri + 1 < a.n_ranges && j >= a.ranges[ri + 1].first) ++ri;
+    const DevRange& R = a.ranges[ri];
+    const int32_t p = (R.p0 + (j - R.first)) % P;
+    const int32_t b = (x - p + P) % P;
+    const int64_t len = a.q + (b < a.m ? 1 : 0);
+    const int64_t off = int64_t(b) * a.q + (b < a.m ? b : a.m);
+    const int64_t e0 = inst * a.stride + off;
+    const int32_t y = ((x + R.delta) % P + P) % P;
+    T* dst = buf_ptr<T>(a, R.dst, x) + e0;
+    const T* src = buf_ptr<T>(a, R.src, y) + e0;
+    if (R.kind == kCopy) {
+      seg_tile<T, OP, kCopy, VEC>(dst, nullptr, nullptr, nullptr, src, len, e0, tile, lane);
+    } else if (R.kind == kReduce) {
+      const T* own = buf_ptr<T>(a, R.own, x) + e0;
+      seg_tile<T, OP, kReduce, VEC>(dst, own, nullptr, nullptr, src, len, e0, tile, lane);
+    } else {
+      const T* own = buf_ptr<T>(a, R.own, x) + e0;
+      T* dst2 = buf_ptr<T>(a, R.dst2, x) + e0;
+      const T* own2 = buf_ptr<T>(a, R.own2, x) + e0;
+      seg_tile<T, OP, kReduce2, VEC>(dst, own, dst2, own2, src, len, e0, tile, lane);
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Fused latency-optimal kernel
+// ---------------------------------------------------------------------------
+
+constexpr int lo_L(int P) {
+  int L = 0;
+  while ((1 << L) < P) ++L;
+  return L;
+}
+constexpr int lo_N(int P, int i) {
+  int N = P;
+  for (int j = 0; j < i; ++j) N -= N / 2;
+  return N;
+}
+
+template <typename V, int OP>
+struct Comb;
+template <typename T, int OP>
+struct Comb<V4<T>, OP> {
+  __device__ __forceinline__ static V4<T> f(const V4<T>& a, const V4<T>& b) { return comb4<OP>(a, b); }
+};
+template <int OP>
+struct Comb<float, OP> {
+  __device__ __forceinline__ static float f(float a, float b) { return comb<OP>(a, b); }
+};
+template <int OP>
+struct Comb<int32_t, OP> {
+  __device__ __forceinline__ static int32_t f(int32_t a, int32_t b) { return comb<OP>(a, b); }
+};
+
+// Reduction step I of the latency-optimal schedule on one column: with
+// f = floor(N_I/2), every rank receives the primed vector of rank x + f;
+// starred sums take it on even N_I, primed sums on every step but the last.
+// Before the first odd step S and R hold the same values, and the compiler
+// computes their identical combinations once.
+template <int P, int I, int OP, typename V>
+__device__ __forceinline__ void lo_steps(V (&R)[P], V (&S)[P]) {
+  constexpr int L = lo_L(P);
+  if constexpr (I < L) {
+    constexpr int N = lo_N(P, I);
+    constexpr int f = N / 2;
+    constexpr bool even = (N % 2) == 0;
+    constexpr bool last = (I == L - 1);
+    V Rn[P];
+#pragma unroll
+    for (int x = 0; x < P; ++x) {
+      const V recv = R[(x + f) % P];
+      if constexpr (even) S[x] = Comb<V, OP>::f(S[x], recv);
+      if constexpr (!last) Rn[x] = Comb<V, OP>::f(R[x], recv);
+    }
+    if constexpr (!last) {
+#pragma unroll
+      for (int x = 0; x < P; ++x) R[x] = Rn[x];
+    }
+    lo_steps<P, I + 1, OP, V>(R, S);
+  }
+}
+
+template <int P, typename T, int OP, bool VEC>
+__global__ __launch_bounds__(kBlock) void fused_lo_kernel(const FusedArgs a) {
+  const int64_t nthreads = int64_t(gridDim.x) * kBlock;
+  for (int64_t g = int64_t(blockIdx.x) * kBlock + threadIdx.x; g < a.groups; g += nthreads) {
+    if constexpr (VEC) {
+      // contiguous instances: column group g = elements [4g, 4g+4) of every rank
+      V4<T> R[P], S[P];
+#pragma unroll
+      for (int x = 0; x < P; ++x) {
+        R[x] = reinterpret_cast<const V4<T>*>(a.user[x])[g];
+        S[x] = R[x];
+      }
+      lo_steps<P, 0, OP, V4<T>>(R, S);
+#pragma unroll
+      for (int x = 0; x < P; ++x) reinterpret_cast<V4<T>*>(a.user[x])[g] = S[x];
+    } else {
+      // any layout: column g = element (g % n) of instance (g / n)
+      const int64_t inst = g / a.n;
+      const int64_t e = inst * a.stride + (g - inst * a.n);
+      T R[P], S[P];
+#pragma unroll
+      for (int x = 0; x < P; ++x) {
+        R[x] = reinterpret_cast<const T*>(a.user[x])[e];
+        S[x] = R[x];
+      }
+      lo_steps<P, 0, OP, T>(R, S);
+#pragma unroll
+      for (int x = 0; x < P; ++x) reinterpret_cast<T*>(a.user[x])[e] = S[x];
+    }
+  }
+}
+
+template <typename T, int OP>
+int launch_step_t(const StepArgs& a, bool vec, int grid, hipStream_t s) {
+  if (vec) hipLaunchKernelGGL((step_kernel<T, OP, true>), dim3(grid), dim3(kBlock), 0, s, a);
+  else hipLaunchKernelGGL((step_kernel<T, OP, false>), dim3(grid), dim3(kBlock), 0, s, a);
+  return int(hipGetLastError());
+}
+
+template <int P, typename T, int OP>
+int launch_fused_p(const FusedArgs& a, bool vec, int grid, hipStream_t s) {
+  if (vec) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, true>), dim3(grid), dim3(kBlock), 0, s, a);
+  else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, false>), dim3(grid), dim3(kBlock), 0, s, a);
+  return int(hipGetLastError());
+}
+
+template <typename T, int OP>
+int launch_fused_t(const FusedArgs& a, int P, bool vec, int grid, hipStream_t s) {
+  switch (P) {
+    case 2: return launch_fused_p<2, T, OP>(a, vec, grid, s);
+    case 3: return launch_fused_p<3, T, OP>(a, vec, grid, s);
+    case 4: return launch_fused_p<4, T, OP>(a, vec, grid, s);
+    case 5: return launch_fused_p<5, T, OP>(a, vec, grid, s);
+    case 6: return launch_fused_p<6, T, OP>(a, vec, grid, s);
+    case 7: return launch_fused_p<7, T, OP>(a, vec, grid, s);
+    case 8: return launch_fused_p<8, T, OP>(a, vec, grid, s);
+    case 9: return launch_fused_p<9, T, OP>(a, vec, grid, s);
+    case 10: return launch_fused_p<10, T, OP>(a, vec, grid, s);
+    case 11: return launch_fused_p<11, T, OP>(a, vec, grid, s);
+    case 12: return launch_fused_p<12, T, OP>(a, vec, grid, s);
+    case 13: return launch_fused_p<13, T, OP>(a, vec, grid, s);
+    case 14: return launch_fused_p<14, T, OP>(a, vec, grid, s);
+    case 15: return launch_fused_p<15, T, OP>(a, vec, grid, s);
+    case 16: return launch_fused_p<16, T, OP>(a, vec, grid, s);
+    default: return int(hipErrorInvalidValue);
+  }
+}
+
+}  // namespace
+
+int64_t step_tile_elems(bool vec) { return vec ? kTileVec : kTileScalar; }
+
+int step_grid(int64_t total_tiles) {
+  const int64_t waves_per_block = kBlock / kWave;
+  int64_t blocks = (total_tiles + waves_per_block - 1) / waves_per_block;
+  const int64_t cap = 256 * 32;  // 256 CUs, enough resident waves to cover HBM latency
+  if (blocks > cap) blocks = cap;
+  if (blocks < 1) blocks = 1;
+  return int(blocks);
+}
+
+int launch_step(const StepArgs& a, int dtype, int op, bool vec, int grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (dtype == 0) return op == 0 ? launch_step_t<int32_t, 0>(a, vec, grid, s) : launch_step_t<int32_t, 1>(a, vec, grid, s);
+  return op == 0 ? launch_step_t<float, 0>(a, vec, grid, s) : launch_step_t<float, 1>(a, vec, grid, s);
+}
+
+int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, bool vec, int grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (dtype == 0) return op == 0 ? launch_fused_t<int32_t, 0>(a, P, vec, grid, s) : launch_fused_t<int32_t, 1>(a, P, vec, grid, s);
+  return op == 0 ? launch_fused_t<float, 0>(a, P, vec, grid, s) : launch_fused_t<float, 1>(a, P, vec, grid, s);
+}
+
+}  // namespace ar
