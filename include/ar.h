@@ -125,7 +125,8 @@ ar_status ar_plan_set_path(ar_plan* plan, ar_path path);
 /* Allreduce in place.  rank_buffers: host array of P device pointers, rank
  * x's n elements at rank_buffers[x].  Pointers must be 4-byte aligned and
  * must not overlap (AR_ERR_ALIAS); 16-byte aligned buffers take the
- * vectorised kernels.  The first call on a plan that needs scratch (r > 0,
+ * vectorised kernels.  With n = 0 nothing is touched and the pointers may be
+ * NULL.  The first call on a plan that needs scratch (r > 0,
  * STEPWISE) allocates it on the current device; it is reused afterwards.
  * A plan must not run on two streams at once (shared scratch). */
 ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t stream);

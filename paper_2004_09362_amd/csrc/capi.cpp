@@ -193,10 +193,11 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
   if (batch < 1) return fail(AR_ERR_INVALID_ARG, "batch must be >= 1");
   if (batch == 1 && instance_stride < plan->s.n) instance_stride = plan->s.n;
   if (instance_stride < plan->s.n) return fail(AR_ERR_INVALID_ARG, "instance_stride must be >= n");
+  if (plan->s.n == 0) return AR_OK;  // nothing is read or written; the pointers may be NULL
   bool all16 = false;
   ar_status st = check_buffers(plan, rank_buffers, batch, instance_stride, &all16);
   if (st != AR_OK) return st;
-  if (plan->s.P == 1 || plan->s.n == 0) return AR_OK;  // nothing to combine
+  if (plan->s.P == 1) return AR_OK;  // nothing to combine
   int device = -1;
   hipError_t he = hipGetDevice(&device);
   if (he != hipSuccess) {
