@@ -58,6 +58,27 @@ inline int64_t block_len(int64_t n, int32_t P, int32_t b) {
   return q + (b < m ? 1 : 0);
 }
 
+// Division of 32-bit numbers by a divisor fixed for a launch: a multiply-high
+// and two shifts instead of a division sequence (unsigned division by
+// invariant integers, Granlund & Montgomery 1994, "round-up" variant).
+struct FastDiv {
+  uint32_t d, m, l;  // divisor, magic multiplier, ceil(log2 d)
+};
+
+inline FastDiv make_fastdiv(uint32_t d) {
+  FastDiv f{d, 0, 0};
+  while ((uint64_t(1) << f.l) < d) ++f.l;
+  f.m = uint32_t(((uint64_t(1) << 32) * ((uint64_t(1) << f.l) - d)) / d + 1);
+  return f;
+}
+
+// Host reference of the device quotient (used by the tests).
+inline uint32_t fastdiv_host(uint32_t n, const FastDiv& f) {
+  if (f.l == 0) return n;
+  const uint32_t t = uint32_t((uint64_t(n) * f.m) >> 32);
+  return (t + ((n - t) >> 1)) >> (f.l - 1);
+}
+
 // ----- device launch interface (kernels.hip) -----
 
 struct DevRange {
@@ -70,10 +91,11 @@ struct StepArgs {
   void* user[kMaxP];        // rank buffers
   char* scratch[2];         // X and Y: rank y's region at scratch[i] + y * scratch_rank_stride elements
   int64_t scratch_rank_stride;
-  int64_t n, stride, batch;
+  int64_t n, stride;
   int64_t q, m;             // n / P, n % P
-  int64_t tiles_per_seg;
-  int32_t P, n_ranges, total_ops, pad;
+  uint32_t total_tiles;     // P * total_ops * batch * tiles_per_seg (< 2^31)
+  FastDiv tps, batch, ops;  // tiles per segment, instances, ops per rank
+  int32_t P, n_ranges;
   DevRange ranges[kMaxRanges];
 };
 
@@ -84,10 +106,10 @@ struct FusedArgs {
 };
 
 // dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.
-int launch_step(const StepArgs& a, int dtype, int op, bool vec, int grid, void* stream);
+int launch_step(const StepArgs& a, int dtype, int op, bool vec, bool nt, int grid, void* stream);
 int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, bool vec, int grid, void* stream);
-// Workgroups a step launch would use for `total_waves` wave tiles.
+// Workgroups of a step launch over `total_tiles` wave tiles, and the tile size.
 int step_grid(int64_t total_tiles);
-int64_t step_tile_elems(bool vec);
+int64_t step_tile_elems();
 
 }  // namespace ar

@@ -8,6 +8,7 @@
 #include <algorithm>
 #include <cstdint>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <string>
 #include <vector>
@@ -15,9 +16,13 @@
 #include "../../include/ar.h"
 #include "ar_internal.hpp"
 
+// Launches moving at least this many bytes use nontemporal loads and stores.
+constexpr int64_t kNtThresholdBytes = int64_t(512) << 20;
+
 struct ar_plan {
   ar::Schedule s;
   int32_t dtype = 0, op = 0;
+  int32_t nt_mode = -1;  // -1 by launch size, 0 never, 1 always (AR_STEP_NT)
   int32_t path = AR_PATH_AUTO;
   bool fused_ok = false;
   void* scratch = nullptr;
@@ -99,7 +104,6 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   a.P = s.P;
   a.n = s.n;
   a.stride = stride;
-  a.batch = batch;
   a.q = s.n / s.P;
   a.m = s.n % s.P;
   if (s.uses_scratch) {
@@ -114,8 +118,11 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
     a.scratch[1] = static_cast<char*>(pl->scratch) + size_t(s.P) * size_t(rank_stride) * 4;
   }
   const int64_t max_len = a.q + (a.m ? 1 : 0);
-  const int64_t tile = ar::step_tile_elems(vec);
-  a.tiles_per_seg = std::max<int64_t>(1, (max_len + tile - 1) / tile);
+  const int64_t tile = ar::step_tile_elems();
+  // +32: a tile grid shifted onto 128-byte lines may need one more tile
+  const int64_t tps = std::max<int64_t>(1, (max_len + 32 + tile - 1) / tile);
+  a.tps = ar::make_fastdiv(uint32_t(std::min<int64_t>(tps, INT32_MAX)));
+  a.batch = ar::make_fastdiv(uint32_t(std::min<int64_t>(batch, INT32_MAX)));
   for (const ar::Launch& l : s.launches) {
     a.n_ranges = int32_t(l.ranges.size());
     int32_t first = 0;
@@ -124,10 +131,20 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
       a.ranges[i] = ar::DevRange{r.p0, r.count, r.kind, r.delta, r.dst, r.own, r.dst2, r.own2, r.src, first};
       first += r.count;
     }
-    a.total_ops = first;
-    const int64_t total_tiles = int64_t(s.P) * a.total_ops * batch * a.tiles_per_seg;
+    a.ops = ar::make_fastdiv(uint32_t(first));
+    const int64_t total_tiles = int64_t(s.P) * first * batch * tps;
+    if (total_tiles >= (int64_t(1) << 31))
+      return fail(AR_ERR_UNSUPPORTED, "one step would need 2^31 or more tiles; split the batch");
+    a.total_tiles = uint32_t(total_tiles);
     const int grid = ar::step_grid(total_tiles);
-    const int e = ar::launch_step(a, pl->dtype, pl->op, vec, grid, stream);
+    // Nontemporal accesses for launches that stream far more than the
+    // Infinity Cache holds; smaller ones keep their output cached for the
+    // next step, which reads it.
+    int64_t blocks_touched = 0;
+    for (const ar::Range& r : l.ranges) blocks_touched += int64_t(r.count) * (r.kind == ar::kCopy ? 2 : r.kind == ar::kReduce ? 3 : 5);
+    const int64_t launch_bytes = blocks_touched * s.n * batch * 4;
+    const bool nt = pl->nt_mode == 1 || (pl->nt_mode < 0 && launch_bytes >= kNtThresholdBytes);
+    const int e = ar::launch_step(a, pl->dtype, pl->op, vec, nt, grid, stream);
     if (e != 0) return hip_fail(hipError_t(e), "step kernel launch");
   }
   return AR_OK;
@@ -170,6 +187,7 @@ ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t
   }
   pl->dtype = int32_t(dtype);
   pl->op = int32_t(op);
+  if (const char* e = std::getenv("AR_STEP_NT")) pl->nt_mode = (e[0] == '1') ? 1 : (e[0] == '0') ? 0 : -1;
   pl->fused_ok = pl->s.P >= 2 && pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L;
   *out_plan = pl;
   g_err.clear();

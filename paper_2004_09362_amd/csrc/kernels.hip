@@ -35,16 +35,48 @@ namespace ar {
 namespace {
 
 constexpr int kWave = 64;
-constexpr int kBlock = 256;           // 4 waves per workgroup
-constexpr int kUnrollVec = 4;         // 16-byte vectors per lane per tile
-constexpr int kUnrollScalar = 8;      // elements per lane per tile, scalar path
-constexpr int64_t kTileVec = int64_t(kWave) * 4 * kUnrollVec;     // 1024 elements
-constexpr int64_t kTileScalar = int64_t(kWave) * kUnrollScalar;   // 512 elements
+constexpr int kBlock = 256;                 // 4 waves per workgroup
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int64_t kTile = int64_t(kWave) * 4;  // elements per wave tile: one 16-byte vector per lane
+constexpr int64_t kMaxGrid = int64_t(1) << 22; // workgroups per launch; beyond it waves loop
 
 template <typename T>
 struct alignas(16) V4 {
   T v[4];
 };
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+template <typename T> struct Ext;
+template <> struct Ext<float> { using type = f32x4; };
+template <> struct Ext<int32_t> { using type = i32x4; };
+
+// 16-byte load/store; NT marks them nontemporal (streamed past the caches),
+// which pays for launches far larger than the 256 MB Infinity Cache.
+template <bool NT, typename T>
+__device__ __forceinline__ V4<T> ld4(const V4<T>* p) {
+  if constexpr (NT) {
+    using E = typename Ext<T>::type;
+    const E e = __builtin_nontemporal_load(reinterpret_cast<const E*>(p));
+    V4<T> r;
+    r.v[0] = e[0]; r.v[1] = e[1]; r.v[2] = e[2]; r.v[3] = e[3];
+    return r;
+  } else {
+    return *p;
+  }
+}
+
+template <bool NT, typename T>
+__device__ __forceinline__ void st4(V4<T>* p, const V4<T>& v) {
+  if constexpr (NT) {
+    using E = typename Ext<T>::type;
+    E e;
+    e[0] = v.v[0]; e[1] = v.v[1]; e[2] = v.v[2]; e[3] = v.v[3];
+    __builtin_nontemporal_store(e, reinterpret_cast<E*>(p));
+  } else {
+    *p = v;
+  }
+}
 
 template <int OP>
 __device__ __forceinline__ float comb(float a, float b) {
@@ -66,16 +98,27 @@ __device__ __forceinline__ V4<T> comb4(const V4<T>& a, const V4<T>& b) {
   return r;
 }
 
+__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
+  if (f.l == 0) return n;
+  const uint32_t t = __umulhi(n, f.m);
+  return (t + ((n - t) >> 1)) >> (f.l - 1);
+}
+
 template <typename T>
 __device__ __forceinline__ T* buf_ptr(const StepArgs& a, int32_t buf, int32_t rank) {
   if (buf == kBufU) return reinterpret_cast<T*>(a.user[rank]);
   return reinterpret_cast<T*>(a.scratch[buf - 1]) + int64_t(rank) * a.scratch_rank_stride;
 }
 
-// One tile of one segment (one block of one rank for one placement), by one
-// wave.  The pointers are at the segment's first element; e0 is that
-// element's index inside the rank buffer (its 16-byte phase).
-template <typename T, int OP, int KIND, bool VEC>
+// One wave tile of one segment -- one block of one rank for one placement.
+// The pointers are at the segment's first element; e0 is that element's
+// index inside the rank buffer, which fixes its 16-byte phase (all buffers
+// share it).  Vector path: the 16-byte aligned body is cut into 1 KB tiles
+// that start on 128-byte lines of the destination, so every store covers
+// whole lines; lane i handles vector tile*64 - lo8 + i, and tile 0 also does
+// the <= 3 leading and <= 3 trailing elements.  Scalar path: four elements
+// per lane, 64 apart.
+template <typename T, int OP, int KIND, bool VEC, bool NT>
 __device__ __forceinline__ void seg_tile(T* __restrict__ dst, const T* __restrict__ own, T* __restrict__ dst2,
                                          const T* __restrict__ own2, const T* __restrict__ src, int64_t len,
                                          int64_t e0, int64_t tile, int lane) {
@@ -84,38 +127,22 @@ __device__ __forceinline__ void seg_tile(T* __restrict__ dst, const T* __restric
     if (head > len) head = len;
     const int64_t nvec = (len - head) >> 2;
     const int64_t tail0 = head + (nvec << 2);
-    const int64_t v0 = tile * (int64_t(kWave) * kUnrollVec);
-    if (v0 < nvec) {
-      const V4<T>* s4 = reinterpret_cast<const V4<T>*>(src + head);
-      const V4<T>* o4 = reinterpret_cast<const V4<T>*>(own + head);
-      const V4<T>* o24 = reinterpret_cast<const V4<T>*>(own2 + head);
-      V4<T>* d4 = reinterpret_cast<V4<T>*>(dst + head);
-      V4<T>* d24 = reinterpret_cast<V4<T>*>(dst2 + head);
-      V4<T> sv[kUnrollVec], ov[kUnrollVec], o2v[kUnrollVec];
-#pragma unroll
-      for (int u = 0; u < kUnrollVec; ++u) {
-        const int64_t v = v0 + u * kWave + lane;
-        if (v < nvec) {
-          sv[u] = s4[v];
-          if constexpr (KIND != kCopy) ov[u] = o4[v];
-          if constexpr (KIND == kReduce2) o2v[u] = o24[v];
+    const int64_t lo8 = (reinterpret_cast<uintptr_t>(dst + head) >> 4) & 7;
+    const int64_t v = tile * kWave - lo8 + lane;
+    if (v >= 0 && v < nvec) {
+      const V4<T> sv = ld4<NT>(reinterpret_cast<const V4<T>*>(src + head) + v);
+      if constexpr (KIND == kCopy) {
+        st4<NT>(reinterpret_cast<V4<T>*>(dst + head) + v, sv);
+      } else {
+        const V4<T> ov = ld4<NT>(reinterpret_cast<const V4<T>*>(own + head) + v);
+        if constexpr (KIND == kReduce2) {
+          const V4<T> o2v = ld4<NT>(reinterpret_cast<const V4<T>*>(own2 + head) + v);
+          st4<NT>(reinterpret_cast<V4<T>*>(dst2 + head) + v, comb4<OP>(o2v, sv));
         }
-      }
-#pragma unroll
-      for (int u = 0; u < kUnrollVec; ++u) {
-        const int64_t v = v0 + u * kWave + lane;
-        if (v < nvec) {
-          if constexpr (KIND == kCopy) {
-            d4[v] = sv[u];
-          } else {
-            d4[v] = comb4<OP>(ov[u], sv[u]);
-            if constexpr (KIND == kReduce2) d24[v] = comb4<OP>(o2v[u], sv[u]);
-          }
-        }
+        st4<NT>(reinterpret_cast<V4<T>*>(dst + head) + v, comb4<OP>(ov, sv));
       }
     }
     if (tile == 0) {
-      // at most 3 leading and 3 trailing elements, one per lane
       int64_t e = -1;
       if (lane < head) e = lane;
       else if (lane >= 4 && lane - 4 < len - tail0) e = tail0 + (lane - 4);
@@ -123,17 +150,17 @@ __device__ __forceinline__ void seg_tile(T* __restrict__ dst, const T* __restric
         if constexpr (KIND == kCopy) {
           dst[e] = src[e];
         } else {
-          const T sv1 = src[e];
-          dst[e] = comb<OP>(own[e], sv1);
-          if constexpr (KIND == kReduce2) dst2[e] = comb<OP>(own2[e], sv1);
+          const T s1 = src[e];
+          if constexpr (KIND == kReduce2) dst2[e] = comb<OP>(own2[e], s1);
+          dst[e] = comb<OP>(own[e], s1);
         }
       }
     }
   } else {
-    const int64_t i0 = tile * kTileScalar;
-    T sv[kUnrollScalar], ov[kUnrollScalar], o2v[kUnrollScalar];
+    const int64_t i0 = tile * kTile;
+    T sv[4], ov[4], o2v[4];
 #pragma unroll
-    for (int u = 0; u < kUnrollScalar; ++u) {
+    for (int u = 0; u < 4; ++u) {
       const int64_t e = i0 + u * kWave + lane;
       if (e < len) {
         sv[u] = src[e];
@@ -142,61 +169,67 @@ __device__ __forceinline__ void seg_tile(T* __restrict__ dst, const T* __restric
       }
     }
 #pragma unroll
-    for (int u = 0; u < kUnrollScalar; ++u) {
+    for (int u = 0; u < 4; ++u) {
       const int64_t e = i0 + u * kWave + lane;
       if (e < len) {
         if constexpr (KIND == kCopy) {
           dst[e] = sv[u];
         } else {
-          dst[e] = comb<OP>(ov[u], sv[u]);
           if constexpr (KIND == kReduce2) dst2[e] = comb<OP>(o2v[u], sv[u]);
+          dst[e] = comb<OP>(ov[u], sv[u]);
         }
       }
     }
   }
 }
 
-// Work decomposition: tile t of the launch -> (rank x, op j, instance, tile
-// within the segment); consecutive waves stream consecutive tiles of one
-// block.  All of it is wave-uniform scalar arithmetic.
-template <typename T, int OP, bool VEC>
+// Wave tile t of the launch -> (rank x, op j, instance, tile within the
+// segment); consecutive waves stream consecutive tiles of one block, so a
+// workgroup covers 4 KB of each stream and small segments share workgroups.
+// The launch has one wave per tile (up to kMaxGrid workgroups).  The
+// decomposition is wave-uniform 32-bit scalar arithmetic with precomputed
+// divisions, short enough that a wave reaches its loads almost at once:
+// with one 16-byte vector per lane in flight, a long prologue would leave
+// the memory system idle.
+template <typename T, int OP, bool VEC, bool NT>
 __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
-  // the wave index is uniform across the wave: keep the decomposition scalar
-  const int wave_in_block = __builtin_amdgcn_readfirstlane(int(threadIdx.x) / kWave);
-  const int64_t wave = int64_t(blockIdx.x) * (kBlock / kWave) + wave_in_block;
-  const int64_t nwaves = int64_t(gridDim.x) * (kBlock / kWave);
-  const int64_t tps = a.tiles_per_seg;
-  const int64_t total = int64_t(a.P) * a.total_ops * a.batch * tps;
+  const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int32_t P = a.P;
-  for (int64_t t = wave; t < total; t += nwaves) {
-    const int64_t seg = t / tps;
-    const int64_t tile = t - seg * tps;
-    const int64_t inst = seg % a.batch;
-    const int64_t rest = seg / a.batch;
-    const int32_t j = int32_t(rest % a.total_ops);
-    const int32_t x = int32_t(rest / a.total_ops);
+  for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
+       t += gridDim.x * uint32_t(kWavesPerBlock)) {
+    const uint32_t seg = fdiv(t, a.tps);
+    const uint32_t tile = t - seg * a.tps.d;
+    const uint32_t rest = fdiv(seg, a.batch);
+    const uint32_t inst = seg - rest * a.batch.d;
+    const uint32_t x32 = fdiv(rest, a.ops);
+    const int32_t j = int32_t(rest - x32 * a.ops.d);
+    const int32_t x = int32_t(x32);
     int ri = 0;
     while (ri + 1 < a.n_ranges && j >= a.ranges[ri + 1].first) ++ri;
     const DevRange& R = a.ranges[ri];
-    const int32_t p = (R.p0 + (j - R.first)) % P;
-    const int32_t b = (x - p + P) % P;
+    int32_t p = R.p0 + (j - R.first);  // < 2P
+    if (p >= P) p -= P;
+    int32_t b = x - p;
+    if (b < 0) b += P;
+    int32_t y = x + R.delta;            // |delta| < P
+    if (y >= P) y -= P;
+    if (y < 0) y += P;
     const int64_t len = a.q + (b < a.m ? 1 : 0);
     const int64_t off = int64_t(b) * a.q + (b < a.m ? b : a.m);
-    const int64_t e0 = inst * a.stride + off;
-    const int32_t y = ((x + R.delta) % P + P) % P;
+    const int64_t e0 = int64_t(inst) * a.stride + off;
     T* dst = buf_ptr<T>(a, R.dst, x) + e0;
     const T* src = buf_ptr<T>(a, R.src, y) + e0;
     if (R.kind == kCopy) {
-      seg_tile<T, OP, kCopy, VEC>(dst, nullptr, nullptr, nullptr, src, len, e0, tile, lane);
+      seg_tile<T, OP, kCopy, VEC, NT>(dst, nullptr, nullptr, nullptr, src, len, e0, tile, lane);
     } else if (R.kind == kReduce) {
       const T* own = buf_ptr<T>(a, R.own, x) + e0;
-      seg_tile<T, OP, kReduce, VEC>(dst, own, nullptr, nullptr, src, len, e0, tile, lane);
+      seg_tile<T, OP, kReduce, VEC, NT>(dst, own, nullptr, nullptr, src, len, e0, tile, lane);
     } else {
       const T* own = buf_ptr<T>(a, R.own, x) + e0;
       T* dst2 = buf_ptr<T>(a, R.dst2, x) + e0;
       const T* own2 = buf_ptr<T>(a, R.own2, x) + e0;
-      seg_tile<T, OP, kReduce2, VEC>(dst, own, dst2, own2, src, len, e0, tile, lane);
+      seg_tile<T, OP, kReduce2, VEC, NT>(dst, own, dst2, own2, src, len, e0, tile, lane);
     }
   }
 }
@@ -292,9 +325,10 @@ __global__ __launch_bounds__(kBlock) void fused_lo_kernel(const FusedArgs a) {
 }
 
 template <typename T, int OP>
-int launch_step_t(const StepArgs& a, bool vec, int grid, hipStream_t s) {
-  if (vec) hipLaunchKernelGGL((step_kernel<T, OP, true>), dim3(grid), dim3(kBlock), 0, s, a);
-  else hipLaunchKernelGGL((step_kernel<T, OP, false>), dim3(grid), dim3(kBlock), 0, s, a);
+int launch_step_t(const StepArgs& a, bool vec, bool nt, int grid, hipStream_t s) {
+  if (vec && nt) hipLaunchKernelGGL((step_kernel<T, OP, true, true>), dim3(grid), dim3(kBlock), 0, s, a);
+  else if (vec) hipLaunchKernelGGL((step_kernel<T, OP, true, false>), dim3(grid), dim3(kBlock), 0, s, a);
+  else hipLaunchKernelGGL((step_kernel<T, OP, false, false>), dim3(grid), dim3(kBlock), 0, s, a);
   return int(hipGetLastError());
 }
 
@@ -329,21 +363,20 @@ int launch_fused_t(const FusedArgs& a, int P, bool vec, int grid, hipStream_t s)
 
 }  // namespace
 
-int64_t step_tile_elems(bool vec) { return vec ? kTileVec : kTileScalar; }
+int64_t step_tile_elems() { return kTile; }
 
 int step_grid(int64_t total_tiles) {
-  const int64_t waves_per_block = kBlock / kWave;
-  int64_t blocks = (total_tiles + waves_per_block - 1) / waves_per_block;
-  const int64_t cap = 256 * 32;  // 256 CUs, enough resident waves to cover HBM latency
-  if (blocks > cap) blocks = cap;
+  int64_t blocks = (total_tiles + kWavesPerBlock - 1) / kWavesPerBlock;
+  if (blocks > kMaxGrid) blocks = kMaxGrid;
   if (blocks < 1) blocks = 1;
   return int(blocks);
 }
 
-int launch_step(const StepArgs& a, int dtype, int op, bool vec, int grid, void* stream) {
+int launch_step(const StepArgs& a, int dtype, int op, bool vec, bool nt, int grid, void* stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (dtype == 0) return op == 0 ? launch_step_t<int32_t, 0>(a, vec, grid, s) : launch_step_t<int32_t, 1>(a, vec, grid, s);
-  return op == 0 ? launch_step_t<float, 0>(a, vec, grid, s) : launch_step_t<float, 1>(a, vec, grid, s);
+  if (dtype == 0)
+    return op == 0 ? launch_step_t<int32_t, 0>(a, vec, nt, grid, s) : launch_step_t<int32_t, 1>(a, vec, nt, grid, s);
+  return op == 0 ? launch_step_t<float, 0>(a, vec, nt, grid, s) : launch_step_t<float, 1>(a, vec, nt, grid, s);
 }
 
 int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, bool vec, int grid, void* stream) {
