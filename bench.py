@@ -151,6 +151,26 @@ def cpu_baseline(jobs, host_sets, budget_s=12.0):
             "sample": "; ".join(parts) + " (single-threaded C replay, %.1f s)" % total_t}
 
 
+def copy_probe(nbytes, reps):
+    """A plain copy kernel of known size: reads and writes nbytes per launch.
+    Its FETCH_SIZE / WRITE_SIZE readings calibrate the HBM counters."""
+    import torch
+
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda:0")
+    b = torch.empty_like(a)
+    b.copy_(a)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    print(json.dumps({"copy_probe_bytes": nbytes, "reps": reps, "ms": round(ms, 5),
+                      "GBps": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -161,6 +181,8 @@ def main():
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--path", choices=["auto", "stepwise", "fused"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
+                    help="instead: time a plain device-to-device copy of BYTES (counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -173,6 +195,10 @@ def main():
     import torch
 
     from paper_2004_09362_amd import ar, synth
+
+    if args.copy_probe:
+        copy_probe(args.copy_probe, args.steps or 10)
+        return
 
     steps = args.steps if args.steps is not None else (10 if args.workload == "large" else 20)
     warmup = args.warmup if args.warmup is not None else (2 if args.workload == "large" else 5)
@@ -207,21 +233,28 @@ def main():
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
+    # the dominant job: the one moving the most algorithmic bytes
+    def alg_bytes(j, p):
+        st_ = p.stats()
+        fused_ = (path == ar.AR_PATH_FUSED) or (path == ar.AR_PATH_AUTO and st_.fused_ok)
+        return (st_.hbm_bytes_fused if fused_ else st_.hbm_bytes_stepwise) * j["batch"], fused_, st_
+    dom = max(range(len(jobs)), key=lambda jj: alg_bytes(jobs[jj], plans[jj])[0])
 
-    def run_step(s, events=None):
+    def run_step(s, ev=None):
         for jj, (j, p) in enumerate(zip(jobs, plans)):
-            if events is not None:
-                events[jj].record(stream)
+            if ev is not None and jj == dom:
+                ev[0].record(stream)
             p.batched(ptr_tables[s % n_sets][jj], j["batch"], j["n"], stream)
-        if events is not None:
-            events[len(jobs)].record(stream)
+            if ev is not None and jj == dom:
+                ev[1].record(stream)
 
     for s in range(warmup):
         run_step(s)
     torch.cuda.synchronize()
 
-    # ---- timed region: exactly `steps` steps ----
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(len(jobs) + 1)] for _ in range(steps)]
+    # ---- timed region: exactly `steps` steps; HIP events bracket the
+    # dominant job's launch(es) on the launch stream ----
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -232,38 +265,27 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     total_ms = start.elapsed_time(stop)
-
-    per_job_ms = [0.0] * len(jobs)
-    for s in range(steps):
-        for jj in range(len(jobs)):
-            per_job_ms[jj] += ev[s][jj].elapsed_time(ev[s][jj + 1])
-    per_job_ms = [m / steps for m in per_job_ms]
+    dom_ms = sum(a.elapsed_time(b) for a, b in ev) / steps
 
     eff_bytes = sum(j["P"] * j["n"] * j["batch"] * j["dtype"].itemsize for j in jobs)
     ms_per_step = total_ms / steps
     value = eff_bytes / (ms_per_step * 1e-3) / 1e9
 
     # ---- roofline of the dominant kernel ----
-    dom = max(range(len(jobs)), key=lambda jj: per_job_ms[jj])
     dj, dp = jobs[dom], plans[dom]
-    st = dp.stats()
-    fused = (path == ar.AR_PATH_FUSED) or (path == ar.AR_PATH_AUTO and st.fused_ok)
-    alg_bytes = (st.hbm_bytes_fused if fused else st.hbm_bytes_stepwise) * dj["batch"]
+    alg, fused, st = alg_bytes(dj, dp)
     launches = 1 if fused else st.launches
-    bytes_per_launch = alg_bytes / launches
-    launch_ms = per_job_ms[dom] / launches
+    bytes_per_launch = alg / launches
+    launch_ms = dom_ms / launches
     achieved = bytes_per_launch / (launch_ms * 1e-3) / 1e9
     kname = ("fused_lo_kernel<P=%d>" % dj["P"]) if fused else "step_kernel"
     src_hash = kernel_source_hash()
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": traffic_from_profiles(args.workload, kname, src_hash),
-            "kernel": kname, "bytes_per_launch": int(bytes_per_launch), "launch_ms": round(launch_ms, 5),
-            "launches_per_step": launches}
-    step_alg = 0
-    for j, p in zip(jobs, plans):
-        s2 = p.stats()
-        f2 = (path == ar.AR_PATH_FUSED) or (path == ar.AR_PATH_AUTO and s2.fused_ok)
-        step_alg += (s2.hbm_bytes_fused if f2 else s2.hbm_bytes_stepwise) * j["batch"]
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic_from_profiles(args.workload, kname, src_hash),
+            "kernel": kname, "job_P": dj["P"], "bytes_per_launch": int(bytes_per_launch),
+            "launch_ms": round(launch_ms, 5), "launches_per_step": launches}
+    step_alg = sum(alg_bytes(j, p)[0] for j, p in zip(jobs, plans))
 
     desc = DESCRIPTIONS[args.workload]
     if "%d" in desc:
@@ -277,7 +299,6 @@ def main():
                    "k": [j["k"] for j in jobs], "op": jobs[0]["op"],
                    "path": "fused" if fused else "stepwise", "parallelism": "1 GPU, P virtual ranks"},
         "hbm_algorithmic_GBps_step": round(step_alg / (ms_per_step * 1e-3) / 1e9, 1),
-        "per_job_ms": {str(j["P"]): round(m, 5) for j, m in zip(jobs, per_job_ms)},
         "wall_s_timed": round(wall, 4),
         "roofline": roof,
         "source_hash": src_hash,
