@@ -59,10 +59,12 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *   STEPWISE: one kernel launch per communication step of the schedule
  *             (2*ceil(log2 P) - r launches, plus one local copy when P = 2,
  *             k = 1), each pulling the peer's blocks out of HBM.
- *   FUSED:    one launch that keeps every step of the latency-optimal
- *             schedule in registers, column by column, for many
- *             independent instances (small messages, Sec. 1's 425-byte
- *             average); only latency-optimal plans with P <= 16.
+ *   FUSED:    one launch that runs every step of the schedule on element
+ *             columns held in registers, reading each input and writing
+ *             each output once: bandwidth-optimal plans for any P (the Sec. 7
+ *             fold of a column, result handed to every rank), and
+ *             latency-optimal plans with P <= 16 (Sec. 9, many independent
+ *             small instances, Sec. 1's 425-byte average).
  *   AUTO:     FUSED where it applies, STEPWISE otherwise.
  * Both paths combine exactly the same operand pairs in the same order, so
  * their results are bit-identical. */

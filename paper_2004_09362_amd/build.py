@@ -1,10 +1,12 @@
 """Build libar.so (HIP kernels for gfx950 + host plan generator + C ABI).
 
-Run ``python -m paper_2004_09362_amd.build`` or call :func:`build`.  The
-library is written in-tree next to this file.
+Run ``python -m paper_2004_09362_amd.build`` or call :func:`build`.  Every
+translation unit is compiled in parallel into ``_build/`` and linked into
+``libar.so`` next to this file.
 """
 from __future__ import annotations
 
+import concurrent.futures
 import os
 import subprocess
 import sys
@@ -14,14 +16,17 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libar.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("plan.cpp", "capi.cpp", "kernels.hip")]
-HEADERS = [os.path.join(CSRC, "ar_internal.hpp"), os.path.join(ROOT, "include", "ar.h")]
+SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip"] +
+           ["fused_bo_g%d.hip" % i for i in range(8)]]
+HEADERS = [os.path.join(CSRC, f) for f in ("ar_internal.hpp", "device_common.hpp", "fused_bo.hpp")] + [
+    os.path.join(ROOT, "include", "ar.h")]
+OBJDIR = os.path.join(HERE, "_build")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 
 FLAGS = [
-    "-O3", "-std=c++17", "-fPIC", "-shared", "--offload-arch=" + ARCH,
+    "-O3", "-std=c++17", "-fPIC", "--offload-arch=" + ARCH,
     # packed fp32 instructions stay off in all device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-ffp-contract=off", "-fno-fast-math",
@@ -30,21 +35,35 @@ FLAGS = [
 ]
 
 
+def _compile(src: str) -> tuple[str, str]:
+    obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
+    res = subprocess.run([HIPCC] + FLAGS + ["-c", src, "-o", obj], capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError("hipcc failed on %s:\n%s%s" % (src, res.stdout, res.stderr))
+    warn = [ln for ln in res.stderr.splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
+    return obj, "\n".join(warn)
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every source into libar.so (always recompiles)."""
-    tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-o", tmp] + SOURCES
+    """Compile every source (in parallel) and link libar.so; always rebuilds."""
     t0 = time.time()
+    os.makedirs(OBJDIR, exist_ok=True)
+    workers = max(1, min(len(SOURCES), int(os.environ.get("MAX_JOBS", os.cpu_count() or 1))))
+    with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
+        results = list(ex.map(_compile, SOURCES))
+    if verbose:
+        for _, warn in results:
+            if warn:
+                sys.stderr.write(warn + "\n")
+    tmp = LIB + ".tmp%d" % os.getpid()
+    cmd = [HIPCC, "-shared", "-fPIC", "--offload-arch=" + ARCH, "-o", tmp] + [o for o, _ in results]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("hipcc failed building libar.so")
-    if verbose:
-        warn = [ln for ln in res.stderr.splitlines() if "packed-fp32-ops" not in ln and ln.strip()]
-        if warn:
-            sys.stderr.write("\n".join(warn) + "\n")
-        print("built %s in %.1fs" % (LIB, time.time() - t0))
+        raise RuntimeError("linking libar.so failed")
     os.replace(tmp, LIB)
+    if verbose:
+        print("built %s in %.1fs (%d units, %d parallel)" % (LIB, time.time() - t0, len(SOURCES), workers))
     return LIB
 
 

@@ -102,12 +102,30 @@ struct StepArgs {
 struct FusedArgs {
   void* user[kMaxP];
   int64_t n, stride, batch;
-  int64_t groups;           // column groups (vector path) or columns (scalar path)
+  int64_t groups;           // column groups (16-byte mode) or columns (other modes)
+};
+
+// Column kernels: wave tile t -> (instance, block, 64 columns of the block).
+// The rank table is stored twice over (user[x] == user[x + P]) so that the
+// ranks b, b+1, ..., b+P-1 of a rotation are consecutive entries.
+struct ColArgs {
+  void* user[2 * kMaxP];
+  int64_t stride, q, m;     // instance stride, n / P, n % P
+  uint32_t total_tiles;     // batch * P * tiles (< 2^31)
+  FastDiv tiles, pdiv;      // column tiles per block, P
+  int32_t P;
 };
 
 // dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.
 int launch_step(const StepArgs& a, int dtype, int op, bool vec, bool nt, int grid, void* stream);
-int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, bool vec, int grid, void* stream);
+// Fused latency-optimal kernel; mode 0: 16-byte columns groups, 1: one
+// element per lane (contiguous instances), 2: any instance stride.
+int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, int mode, bool nt, int grid, void* stream);
+// Column-fused bandwidth-optimal kernel, one instantiation per P
+// (fused_bo_g*.hip), and its dispatcher over P = 2..128.
+template <int P>
+int launch_fused_bo(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream);
+int launch_fused_bo_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream);
 // Workgroups of a step launch over `total_tiles` wave tiles, and the tile size.
 int step_grid(int64_t total_tiles);
 int64_t step_tile_elems();

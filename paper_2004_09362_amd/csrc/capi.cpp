@@ -16,14 +16,24 @@
 #include "../../include/ar.h"
 #include "ar_internal.hpp"
 
-// Launches moving at least this many bytes use nontemporal loads and stores.
+// Step launches moving at least this many bytes use nontemporal loads and
+// stores; the fused kernels, whose many concurrent streams gain from it at
+// smaller sizes, switch at a lower mark.
 constexpr int64_t kNtThresholdBytes = int64_t(512) << 20;
+constexpr int64_t kFusedNtThresholdBytes = int64_t(128) << 20;
+
+// Which single-launch kernel can run a plan.
+enum FusedKind { kFusedNone = 0, kFusedLo = 1, kFusedBo = 2 };
 
 struct ar_plan {
   ar::Schedule s;
   int32_t dtype = 0, op = 0;
-  int32_t nt_mode = -1;  // -1 by launch size, 0 never, 1 always (AR_STEP_NT)
+  // Tuning overrides read from the environment at plan creation:
+  // AR_STEP_NT / AR_FUSED_NT = 0|1 (nontemporal never / always; default by
+  // launch size), AR_FUSED_MODE = 0|1 (16-byte or 4-byte columns).
+  int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1;
   int32_t path = AR_PATH_AUTO;
+  int32_t fused_kind = kFusedNone;
   bool fused_ok = false;
   void* scratch = nullptr;
   size_t scratch_bytes = 0;
@@ -95,6 +105,10 @@ ar_status ensure_scratch(ar_plan* pl, size_t need, int device) {
   return AR_OK;
 }
 
+bool use_nt(int32_t mode, int64_t bytes, int64_t threshold = kNtThresholdBytes) {
+  return mode == 1 || (mode < 0 && bytes >= threshold);
+}
+
 ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool vec, hipStream_t stream,
                        int device) {
   const ar::Schedule& s = pl->s;
@@ -143,14 +157,14 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
     int64_t blocks_touched = 0;
     for (const ar::Range& r : l.ranges) blocks_touched += int64_t(r.count) * (r.kind == ar::kCopy ? 2 : r.kind == ar::kReduce ? 3 : 5);
     const int64_t launch_bytes = blocks_touched * s.n * batch * 4;
-    const bool nt = pl->nt_mode == 1 || (pl->nt_mode < 0 && launch_bytes >= kNtThresholdBytes);
+    const bool nt = use_nt(pl->nt_mode, launch_bytes);
     const int e = ar::launch_step(a, pl->dtype, pl->op, vec, nt, grid, stream);
     if (e != 0) return hip_fail(hipError_t(e), "step kernel launch");
   }
   return AR_OK;
 }
 
-ar_status run_fused(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool all16, hipStream_t stream) {
+ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool all16, hipStream_t stream) {
   const ar::Schedule& s = pl->s;
   ar::FusedArgs a;
   std::memset(&a, 0, sizeof a);
@@ -160,12 +174,38 @@ ar_status run_fused(ar_plan* pl, void* const* bufs, int64_t batch, int64_t strid
   a.batch = batch;
   const int64_t cols = batch * s.n;
   const bool contiguous = (batch == 1 || stride == s.n);
-  const bool vec = all16 && contiguous && cols % 4 == 0;
-  a.groups = vec ? cols / 4 : cols;
+  int mode = 2;
+  if (contiguous) mode = (pl->fused_mode == 0 && all16 && cols % 4 == 0) ? 0 : 1;
+  a.groups = mode == 0 ? cols / 4 : cols;
   int64_t blocks = (a.groups + 255) / 256;
-  blocks = std::min<int64_t>(std::max<int64_t>(blocks, 1), 256 * 64);
-  const int e = ar::launch_fused_lo(a, s.P, pl->dtype, pl->op, vec, int(blocks), stream);
-  if (e != 0) return hip_fail(hipError_t(e), "fused kernel launch");
+  blocks = std::min<int64_t>(std::max<int64_t>(blocks, 1), int64_t(1) << 22);
+  const bool nt = mode != 2 && use_nt(pl->fused_nt_mode, int64_t(2) * s.P * cols * 4, kFusedNtThresholdBytes);
+  const int e = ar::launch_fused_lo(a, s.P, pl->dtype, pl->op, mode, nt, int(blocks), stream);
+  if (e != 0) return hip_fail(hipError_t(e), "fused latency-optimal kernel launch");
+  return AR_OK;
+}
+
+ar_status run_fused_bo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, hipStream_t stream) {
+  const ar::Schedule& s = pl->s;
+  ar::ColArgs a;
+  std::memset(&a, 0, sizeof a);
+  for (int32_t x = 0; x < 2 * s.P; ++x) a.user[x] = bufs[x % s.P];
+  a.P = s.P;
+  a.stride = stride;
+  a.q = s.n / s.P;
+  a.m = s.n % s.P;
+  const int64_t max_len = a.q + (a.m ? 1 : 0);
+  // +63: the tile grid of a block is shifted onto 256-byte boundaries
+  const int64_t tiles = std::max<int64_t>(1, (max_len + 63 + 63) / 64);
+  const int64_t total = batch * s.P * tiles;
+  if (total >= (int64_t(1) << 31))
+    return fail(AR_ERR_UNSUPPORTED, "the fused kernel would need 2^31 or more tiles; split the batch");
+  a.total_tiles = uint32_t(total);
+  a.tiles = ar::make_fastdiv(uint32_t(tiles));
+  a.pdiv = ar::make_fastdiv(uint32_t(s.P));
+  const bool nt = use_nt(pl->fused_nt_mode, int64_t(2) * s.P * s.n * batch * 4, kFusedNtThresholdBytes);
+  const int e = ar::launch_fused_bo_any(a, s.P, pl->dtype, pl->op, nt, ar::step_grid(total), stream);
+  if (e != 0) return hip_fail(hipError_t(e), "fused bandwidth-optimal kernel launch");
   return AR_OK;
 }
 
@@ -187,8 +227,16 @@ ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t
   }
   pl->dtype = int32_t(dtype);
   pl->op = int32_t(op);
-  if (const char* e = std::getenv("AR_STEP_NT")) pl->nt_mode = (e[0] == '1') ? 1 : (e[0] == '0') ? 0 : -1;
-  pl->fused_ok = pl->s.P >= 2 && pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L;
+  auto env_mode = [](const char* name) {
+    const char* e = std::getenv(name);
+    return e == nullptr ? -1 : (e[0] == '1') ? 1 : (e[0] == '0') ? 0 : -1;
+  };
+  pl->nt_mode = env_mode("AR_STEP_NT");
+  pl->fused_nt_mode = env_mode("AR_FUSED_NT");
+  pl->fused_mode = env_mode("AR_FUSED_MODE");
+  if (pl->s.P >= 2 && pl->s.r == 0) pl->fused_kind = kFusedBo;
+  else if (pl->s.P >= 2 && pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L) pl->fused_kind = kFusedLo;
+  pl->fused_ok = pl->fused_kind != kFusedNone;
   *out_plan = pl;
   g_err.clear();
   return AR_OK;
@@ -199,7 +247,8 @@ ar_status ar_plan_set_path(ar_plan* plan, ar_path path) {
   if (path != AR_PATH_AUTO && path != AR_PATH_STEPWISE && path != AR_PATH_FUSED)
     return fail(AR_ERR_INVALID_ARG, "unknown path");
   if (path == AR_PATH_FUSED && !plan->fused_ok)
-    return fail(AR_ERR_UNSUPPORTED, "the fused path runs latency-optimal plans with 2 <= P <= 16 only");
+    return fail(AR_ERR_UNSUPPORTED,
+                "the fused path runs bandwidth-optimal plans, and latency-optimal plans with P <= 16");
   plan->path = path;
   return AR_OK;
 }
@@ -225,8 +274,10 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
   const int64_t elems = int64_t(plan->s.P) * plan->s.n * batch;
   if (elems / batch / plan->s.P != plan->s.n) return fail(AR_ERR_INVALID_ARG, "size overflow");
   const bool fused = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok);
-  if (fused) {
-    st = run_fused(plan, rank_buffers, batch, instance_stride, all16, stream);
+  if (fused && plan->fused_kind == kFusedBo) {
+    st = run_fused_bo(plan, rank_buffers, batch, instance_stride, stream);
+  } else if (fused) {
+    st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream);
   } else {
     const bool vec = all16 && (batch == 1 || instance_stride % 4 == 0);
     st = run_stepwise(plan, rank_buffers, batch, instance_stride, vec, stream, device);

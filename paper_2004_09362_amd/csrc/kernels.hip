@@ -22,6 +22,8 @@
 //                path, so the results are bit-identical, but each input is
 //                read once and each output written once (2*P*n elements).
 //
+// The column-fused bandwidth-optimal kernel is in fused_bo.hpp.
+//
 // Compiled with packed-fp32 instructions disabled; only adds and compares,
 // so no contraction question arises.
 #include <hip/hip_runtime.h>
@@ -29,80 +31,11 @@
 #include <cstdint>
 
 #include "ar_internal.hpp"
+#include "device_common.hpp"
 
 namespace ar {
 
 namespace {
-
-constexpr int kWave = 64;
-constexpr int kBlock = 256;                 // 4 waves per workgroup
-constexpr int kWavesPerBlock = kBlock / kWave;
-constexpr int64_t kTile = int64_t(kWave) * 4;  // elements per wave tile: one 16-byte vector per lane
-constexpr int64_t kMaxGrid = int64_t(1) << 22; // workgroups per launch; beyond it waves loop
-
-template <typename T>
-struct alignas(16) V4 {
-  T v[4];
-};
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
-template <typename T> struct Ext;
-template <> struct Ext<float> { using type = f32x4; };
-template <> struct Ext<int32_t> { using type = i32x4; };
-
-// 16-byte load/store; NT marks them nontemporal (streamed past the caches),
-// which pays for launches far larger than the 256 MB Infinity Cache.
-template <bool NT, typename T>
-__device__ __forceinline__ V4<T> ld4(const V4<T>* p) {
-  if constexpr (NT) {
-    using E = typename Ext<T>::type;
-    const E e = __builtin_nontemporal_load(reinterpret_cast<const E*>(p));
-    V4<T> r;
-    r.v[0] = e[0]; r.v[1] = e[1]; r.v[2] = e[2]; r.v[3] = e[3];
-    return r;
-  } else {
-    return *p;
-  }
-}
-
-template <bool NT, typename T>
-__device__ __forceinline__ void st4(V4<T>* p, const V4<T>& v) {
-  if constexpr (NT) {
-    using E = typename Ext<T>::type;
-    E e;
-    e[0] = v.v[0]; e[1] = v.v[1]; e[2] = v.v[2]; e[3] = v.v[3];
-    __builtin_nontemporal_store(e, reinterpret_cast<E*>(p));
-  } else {
-    *p = v;
-  }
-}
-
-template <int OP>
-__device__ __forceinline__ float comb(float a, float b) {
-  if constexpr (OP == 0) return a + b;
-  else return b > a ? b : a;
-}
-
-template <int OP>
-__device__ __forceinline__ int32_t comb(int32_t a, int32_t b) {
-  if constexpr (OP == 0) return int32_t(uint32_t(a) + uint32_t(b));
-  else return b > a ? b : a;
-}
-
-template <int OP, typename T>
-__device__ __forceinline__ V4<T> comb4(const V4<T>& a, const V4<T>& b) {
-  V4<T> r;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) r.v[i] = comb<OP>(a.v[i], b.v[i]);
-  return r;
-}
-
-__device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
-  if (f.l == 0) return n;
-  const uint32_t t = __umulhi(n, f.m);
-  return (t + ((n - t) >> 1)) >> (f.l - 1);
-}
 
 template <typename T>
 __device__ __forceinline__ T* buf_ptr(const StepArgs& a, int32_t buf, int32_t rank) {
@@ -292,34 +225,39 @@ __device__ __forceinline__ void lo_steps(V (&R)[P], V (&S)[P]) {
   }
 }
 
-template <int P, typename T, int OP, bool VEC>
+// MODE 0: contiguous instances, column group g = elements [4g, 4g+4) of
+//         every rank (16-byte accesses);
+// MODE 1: contiguous instances, column g = element g (4-byte accesses);
+// MODE 2: any instance stride, column g = element g % n of instance g / n.
+template <int P, typename T, int OP, int MODE, bool NT>
 __global__ __launch_bounds__(kBlock) void fused_lo_kernel(const FusedArgs a) {
   const int64_t nthreads = int64_t(gridDim.x) * kBlock;
   for (int64_t g = int64_t(blockIdx.x) * kBlock + threadIdx.x; g < a.groups; g += nthreads) {
-    if constexpr (VEC) {
-      // contiguous instances: column group g = elements [4g, 4g+4) of every rank
+    if constexpr (MODE == 0) {
       V4<T> R[P], S[P];
 #pragma unroll
       for (int x = 0; x < P; ++x) {
-        R[x] = reinterpret_cast<const V4<T>*>(a.user[x])[g];
+        R[x] = ld4<NT>(reinterpret_cast<const V4<T>*>(a.user[x]) + g);
         S[x] = R[x];
       }
       lo_steps<P, 0, OP, V4<T>>(R, S);
 #pragma unroll
-      for (int x = 0; x < P; ++x) reinterpret_cast<V4<T>*>(a.user[x])[g] = S[x];
+      for (int x = 0; x < P; ++x) st4<NT>(reinterpret_cast<V4<T>*>(a.user[x]) + g, S[x]);
     } else {
-      // any layout: column g = element (g % n) of instance (g / n)
-      const int64_t inst = g / a.n;
-      const int64_t e = inst * a.stride + (g - inst * a.n);
+      int64_t e = g;
+      if constexpr (MODE == 2) {
+        const int64_t inst = g / a.n;
+        e = inst * a.stride + (g - inst * a.n);
+      }
       T R[P], S[P];
 #pragma unroll
       for (int x = 0; x < P; ++x) {
-        R[x] = reinterpret_cast<const T*>(a.user[x])[e];
+        R[x] = ld1<NT>(reinterpret_cast<const T*>(a.user[x]) + e);
         S[x] = R[x];
       }
       lo_steps<P, 0, OP, T>(R, S);
 #pragma unroll
-      for (int x = 0; x < P; ++x) reinterpret_cast<T*>(a.user[x])[e] = S[x];
+      for (int x = 0; x < P; ++x) st1<NT>(reinterpret_cast<T*>(a.user[x]) + e, S[x]);
     }
   }
 }
@@ -333,30 +271,29 @@ int launch_step_t(const StepArgs& a, bool vec, bool nt, int grid, hipStream_t s)
 }
 
 template <int P, typename T, int OP>
-int launch_fused_p(const FusedArgs& a, bool vec, int grid, hipStream_t s) {
-  if (vec) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, true>), dim3(grid), dim3(kBlock), 0, s, a);
-  else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, false>), dim3(grid), dim3(kBlock), 0, s, a);
+int launch_fused_p(const FusedArgs& a, int mode, bool nt, int grid, hipStream_t s) {
+  const dim3 g(grid), blk(kBlock);
+  if (mode == 0) {
+    if (nt) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 0, true>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 0, false>), g, blk, 0, s, a);
+  } else if (mode == 1) {
+    if (nt) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 1, true>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 1, false>), g, blk, 0, s, a);
+  } else {
+    hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 2, false>), g, blk, 0, s, a);
+  }
   return int(hipGetLastError());
 }
 
 template <typename T, int OP>
-int launch_fused_t(const FusedArgs& a, int P, bool vec, int grid, hipStream_t s) {
+int launch_fused_t(const FusedArgs& a, int P, int mode, bool nt, int grid, hipStream_t s) {
   switch (P) {
-    case 2: return launch_fused_p<2, T, OP>(a, vec, grid, s);
-    case 3: return launch_fused_p<3, T, OP>(a, vec, grid, s);
-    case 4: return launch_fused_p<4, T, OP>(a, vec, grid, s);
-    case 5: return launch_fused_p<5, T, OP>(a, vec, grid, s);
-    case 6: return launch_fused_p<6, T, OP>(a, vec, grid, s);
-    case 7: return launch_fused_p<7, T, OP>(a, vec, grid, s);
-    case 8: return launch_fused_p<8, T, OP>(a, vec, grid, s);
-    case 9: return launch_fused_p<9, T, OP>(a, vec, grid, s);
-    case 10: return launch_fused_p<10, T, OP>(a, vec, grid, s);
-    case 11: return launch_fused_p<11, T, OP>(a, vec, grid, s);
-    case 12: return launch_fused_p<12, T, OP>(a, vec, grid, s);
-    case 13: return launch_fused_p<13, T, OP>(a, vec, grid, s);
-    case 14: return launch_fused_p<14, T, OP>(a, vec, grid, s);
-    case 15: return launch_fused_p<15, T, OP>(a, vec, grid, s);
-    case 16: return launch_fused_p<16, T, OP>(a, vec, grid, s);
+#define AR_LO_CASE(PP) \
+  case PP: return launch_fused_p<PP, T, OP>(a, mode, nt, grid, s);
+    AR_LO_CASE(2) AR_LO_CASE(3) AR_LO_CASE(4) AR_LO_CASE(5) AR_LO_CASE(6) AR_LO_CASE(7) AR_LO_CASE(8)
+    AR_LO_CASE(9) AR_LO_CASE(10) AR_LO_CASE(11) AR_LO_CASE(12) AR_LO_CASE(13) AR_LO_CASE(14)
+    AR_LO_CASE(15) AR_LO_CASE(16)
+#undef AR_LO_CASE
     default: return int(hipErrorInvalidValue);
   }
 }
@@ -379,10 +316,27 @@ int launch_step(const StepArgs& a, int dtype, int op, bool vec, bool nt, int gri
   return op == 0 ? launch_step_t<float, 0>(a, vec, nt, grid, s) : launch_step_t<float, 1>(a, vec, nt, grid, s);
 }
 
-int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, bool vec, int grid, void* stream) {
+int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, int mode, bool nt, int grid, void* stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (dtype == 0) return op == 0 ? launch_fused_t<int32_t, 0>(a, P, vec, grid, s) : launch_fused_t<int32_t, 1>(a, P, vec, grid, s);
-  return op == 0 ? launch_fused_t<float, 0>(a, P, vec, grid, s) : launch_fused_t<float, 1>(a, P, vec, grid, s);
+  if (dtype == 0)
+    return op == 0 ? launch_fused_t<int32_t, 0>(a, P, mode, nt, grid, s) : launch_fused_t<int32_t, 1>(a, P, mode, nt, grid, s);
+  return op == 0 ? launch_fused_t<float, 0>(a, P, mode, nt, grid, s) : launch_fused_t<float, 1>(a, P, mode, nt, grid, s);
+}
+
+int launch_fused_bo_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream) {
+  switch (P) {
+#define AR_BO_CASE(PP) \
+  case PP: return launch_fused_bo<PP>(a, dtype, op, nt, grid, stream);
+#define AR_BO_CASE8(B) AR_BO_CASE(B) AR_BO_CASE(B + 1) AR_BO_CASE(B + 2) AR_BO_CASE(B + 3) \
+  AR_BO_CASE(B + 4) AR_BO_CASE(B + 5) AR_BO_CASE(B + 6) AR_BO_CASE(B + 7)
+    AR_BO_CASE8(2) AR_BO_CASE8(10) AR_BO_CASE8(18) AR_BO_CASE8(26) AR_BO_CASE8(34) AR_BO_CASE8(42)
+    AR_BO_CASE8(50) AR_BO_CASE8(58) AR_BO_CASE8(66) AR_BO_CASE8(74) AR_BO_CASE8(82) AR_BO_CASE8(90)
+    AR_BO_CASE8(98) AR_BO_CASE8(106) AR_BO_CASE8(114) AR_BO_CASE(122) AR_BO_CASE(123) AR_BO_CASE(124)
+    AR_BO_CASE(125) AR_BO_CASE(126) AR_BO_CASE(127) AR_BO_CASE(128)
+#undef AR_BO_CASE8
+#undef AR_BO_CASE
+    default: return int(hipErrorInvalidValue);
+  }
 }
 
 }  // namespace ar

@@ -44,6 +44,13 @@ def run_plan(P, n, dtype, op, k, X, path=ar.AR_PATH_AUTO):
     plan.close()
 
 
+def paths(P, k):
+    """Every execution path that can run the plan: step-wise always, and the
+    single-launch fused kernel where it applies."""
+    st = ar.Plan(P, 8, "float32", "sum", k).stats()
+    return [ar.AR_PATH_STEPWISE, ar.AR_PATH_FUSED] if st.fused_ok else [ar.AR_PATH_STEPWISE]
+
+
 def bits(a):
     a = np.ascontiguousarray(a)
     return a.view(np.uint32) if a.dtype == np.float32 else a
@@ -107,11 +114,12 @@ def test_tag_brute_force(P):
     """Rank x adds 1 << x: any missed or doubled term shows."""
     for k in ks(P):
         for n in (P - 1, 4 * P + 3, 1000):
-            note("tags P=%d k=%d n=%d" % (P, k, n))
-            x = np.stack([np.full(n, 1 << y, np.int32) for y in range(P)])
-            X = torch.from_numpy(x).to(DEV)
-            run_plan(P, n, "int32", "sum", k, X)
-            assert np.all(X.cpu().numpy() == (1 << P) - 1), (P, k, n)
+            for path in paths(P, k):
+                note("tags P=%d k=%d n=%d path=%d" % (P, k, n, path))
+                x = np.stack([np.full(n, 1 << y, np.int32) for y in range(P)])
+                X = torch.from_numpy(x).to(DEV)
+                run_plan(P, n, "int32", "sum", k, X, path)
+                assert np.all(X.cpu().numpy() == (1 << P) - 1), (P, k, n, path)
 
 
 @pytest.mark.parametrize("P", range(2, 129))
@@ -120,12 +128,14 @@ def test_fp32_every_P_every_k(P):
     n = 3 * P + 5
     x = (rng.normal(size=(P, n)) * np.exp2(rng.integers(-6, 6, size=(P, n)))).astype(np.float32)
     for k in ks(P):
-        note("fp32 P=%d k=%d n=%d" % (P, k, n))
-        X = torch.from_numpy(x).to(DEV)
-        run_plan(P, n, "float32", "sum", k, X)
-        got = X.cpu().numpy()
-        assert np.array_equal(bits(got), bits(oracle.allreduce(x, k, "sum"))), (P, k)
-        assert_fp32_bound(got, x)
+        want = oracle.allreduce(x, k, "sum")
+        for path in paths(P, k):
+            note("fp32 P=%d k=%d n=%d path=%d" % (P, k, n, path))
+            X = torch.from_numpy(x).to(DEV)
+            run_plan(P, n, "float32", "sum", k, X, path)
+            got = X.cpu().numpy()
+            assert np.array_equal(bits(got), bits(want)), (P, k, path)
+            assert_fp32_bound(got, x)
 
 
 @pytest.mark.parametrize("P,n", [(3, 100003), (5, 50001), (7, 65543), (24, 99991), (37, 74000), (64, 131072),
@@ -136,14 +146,15 @@ def test_several_tiles_per_block(P, n):
     rng = np.random.default_rng(n)
     x = rng.uniform(-1, 1, size=(P, n)).astype(np.float32)
     for k in sorted({ks(P)[0], ks(P)[len(ks(P)) // 2], ks(P)[-1]}):
-        note("tiles P=%d n=%d k=%d" % (P, n, k))
-        X = torch.from_numpy(x).to(DEV)
-        run_plan(P, n, "float32", "sum", k, X)
-        got = X.cpu().numpy()
         cols = sample_cols(n, P, per_block=96, seed=k)
         want = oracle.allreduce(np.ascontiguousarray(x[:, cols]), k, "sum", n=n, cols=cols)
-        assert np.array_equal(bits(got[:, cols]), bits(want))
-        assert_fp32_bound(got, x)
+        for path in paths(P, k):
+            note("tiles P=%d n=%d k=%d path=%d" % (P, n, k, path))
+            X = torch.from_numpy(x).to(DEV)
+            run_plan(P, n, "float32", "sum", k, X, path)
+            got = X.cpu().numpy()
+            assert np.array_equal(bits(got[:, cols]), bits(want)), path
+            assert_fp32_bound(got, x)
 
 
 @pytest.mark.parametrize("P", [2, 3, 6, 13, 37, 100])
@@ -155,16 +166,17 @@ def test_max_exact(P):
     xf[0, :3] = -0.0
     xf[1 % P, :3] = 0.0
     for k in ks(P):
-        note("max P=%d k=%d" % (P, k))
-        Xi = torch.from_numpy(xi).to(DEV)
-        run_plan(P, n, "int32", "max", k, Xi)
-        assert np.array_equal(Xi.cpu().numpy(), oracle.allreduce(xi, k, "max"))
-        Xf = torch.from_numpy(xf).to(DEV)
-        run_plan(P, n, "float32", "max", k, Xf)
-        assert np.array_equal(bits(Xf.cpu().numpy()), bits(oracle.allreduce(xf, k, "max")))
-        Xs = torch.from_numpy(xi).to(DEV)
-        run_plan(P, n, "int32", "sum", k, Xs)
-        assert np.array_equal(Xs.cpu().numpy(), oracle.allreduce(xi, k, "sum"))
+        for path in paths(P, k):
+            note("max P=%d k=%d path=%d" % (P, k, path))
+            Xi = torch.from_numpy(xi).to(DEV)
+            run_plan(P, n, "int32", "max", k, Xi, path)
+            assert np.array_equal(Xi.cpu().numpy(), oracle.allreduce(xi, k, "max"))
+            Xf = torch.from_numpy(xf).to(DEV)
+            run_plan(P, n, "float32", "max", k, Xf, path)
+            assert np.array_equal(bits(Xf.cpu().numpy()), bits(oracle.allreduce(xf, k, "max")))
+            Xs = torch.from_numpy(xi).to(DEV)
+            run_plan(P, n, "int32", "sum", k, Xs, path)
+            assert np.array_equal(Xs.cpu().numpy(), oracle.allreduce(xi, k, "sum"))
 
 
 # ---------------------------------------------------------------------------
@@ -175,11 +187,12 @@ def test_degenerate_sizes():
     rng = np.random.default_rng(9)
     for P, n in [(5, 0), (5, 1), (5, 3), (37, 36), (2, 1), (2, 2), (2, 7), (1, 10)]:
         for k in ks(P):
-            note("degenerate P=%d n=%d k=%d" % (P, n, k))
             x = rng.normal(size=(P, n)).astype(np.float32)
-            X = torch.from_numpy(x).to(DEV)
-            run_plan(P, n, "float32", "sum", k, X)
-            assert np.array_equal(bits(X.cpu().numpy()), bits(oracle.allreduce(x, k, "sum"))), (P, n, k)
+            for path in paths(P, k):
+                note("degenerate P=%d n=%d k=%d path=%d" % (P, n, k, path))
+                X = torch.from_numpy(x).to(DEV)
+                run_plan(P, n, "float32", "sum", k, X, path)
+                assert np.array_equal(bits(X.cpu().numpy()), bits(oracle.allreduce(x, k, "sum"))), (P, n, k, path)
 
 
 @pytest.mark.parametrize("shift", [1, 2, 3])
@@ -195,15 +208,16 @@ def test_unaligned_rank_buffers(shift):
             big[i, s:s + n] = torch.from_numpy(x[i]).to(DEV)
             views.append(big[i, s:s + n])
         for k in ks(P):
-            note("unaligned P=%d n=%d k=%d shift=%d" % (P, n, k, shift))
-            for i in range(P):
-                s = shift if i % 2 else 0
-                big[i, s:s + n] = torch.from_numpy(x[i]).to(DEV)
-            plan = ar.Plan(P, n, "float32", "sum", k)
-            plan(views)
-            torch.cuda.synchronize()
-            got = np.stack([v.cpu().numpy() for v in views])
-            assert np.array_equal(bits(got), bits(oracle.allreduce(x, k, "sum"))), (P, n, k)
+            for path in paths(P, k):
+                note("unaligned P=%d n=%d k=%d shift=%d path=%d" % (P, n, k, shift, path))
+                for i in range(P):
+                    s = shift if i % 2 else 0
+                    big[i, s:s + n] = torch.from_numpy(x[i]).to(DEV)
+                plan = ar.Plan(P, n, "float32", "sum", k, path=path)
+                plan(views)
+                torch.cuda.synchronize()
+                got = np.stack([v.cpu().numpy() for v in views])
+                assert np.array_equal(bits(got), bits(oracle.allreduce(x, k, "sum"))), (P, n, k, path)
 
 
 def test_separate_allocations_and_shuffled_order():
@@ -259,20 +273,51 @@ def test_fused_latency_optimal_matches_oracle_and_stepwise(P):
         assert np.array_equal(X.cpu().numpy(), oracle.allreduce_batched(xi, L, op))
 
 
-@pytest.mark.parametrize("P,k", [(5, 3), (7, 4), (12, 6), (24, 10), (37, 8)])
+@pytest.mark.parametrize("P", [3, 5, 12, 16])
+def test_fused_column_modes_agree(P, monkeypatch):
+    """The fused latency-optimal kernel's 16-byte and 4-byte column modes and
+    its nontemporal variant produce the same bits as the oracle."""
+    rng = np.random.default_rng(77 + P)
+    n, B = 64, 40
+    L = ceil_log2(P)
+    x = rng.normal(size=(P, B, n)).astype(np.float32)
+    want = oracle.allreduce_batched(x, L, "sum")
+    for mode in ("0", "1"):
+        for nt in ("0", "1"):
+            monkeypatch.setenv("AR_FUSED_MODE", mode)
+            monkeypatch.setenv("AR_FUSED_NT", nt)
+            note("fused LO modes P=%d mode=%s nt=%s" % (P, mode, nt))
+            X = torch.from_numpy(x).to(DEV)
+            plan = ar.Plan(P, n, "float32", "sum", L, path=ar.AR_PATH_FUSED)
+            plan.batched([X[i] for i in range(P)], B, n)
+            torch.cuda.synchronize()
+            assert np.array_equal(bits(X.cpu().numpy()), bits(want)), (mode, nt)
+    for nt in ("0", "1"):
+        monkeypatch.setenv("AR_FUSED_NT", nt)
+        note("fused BO nt=%s P=%d" % (nt, P))
+        x2 = rng.normal(size=(P, 1001)).astype(np.float32)
+        X = torch.from_numpy(x2).to(DEV)
+        plan = ar.Plan(P, 1001, "float32", "sum", 2 * L, path=ar.AR_PATH_FUSED)
+        plan([X[i] for i in range(P)])
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(X.cpu().numpy()), bits(oracle.allreduce(x2, 2 * L, "sum"))), nt
+
+
+@pytest.mark.parametrize("P,k", [(5, 3), (7, 4), (7, 6), (12, 6), (12, 8), (24, 10), (37, 8), (37, 12)])
 def test_batched_with_gaps_leaves_gaps_untouched(P, k):
     rng = np.random.default_rng(P * 31 + k)
     n, B, stride = 53, 9, 61
     x = rng.normal(size=(P, B, stride)).astype(np.float32)
-    X = torch.from_numpy(x).to(DEV)
-    note("batched gaps P=%d k=%d" % (P, k))
-    plan = ar.Plan(P, n, "float32", "sum", k)
-    plan.batched([X[i] for i in range(P)], B, stride)
-    torch.cuda.synchronize()
-    got = X.cpu().numpy()
     want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, "sum")
-    assert np.array_equal(bits(got[:, :, :n]), bits(want))
-    assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:]))
+    for path in paths(P, k):
+        X = torch.from_numpy(x).to(DEV)
+        note("batched gaps P=%d k=%d path=%d" % (P, k, path))
+        plan = ar.Plan(P, n, "float32", "sum", k, path=path)
+        plan.batched([X[i] for i in range(P)], B, stride)
+        torch.cuda.synchronize()
+        got = X.cpu().numpy()
+        assert np.array_equal(bits(got[:, :, :n]), bits(want)), path
+        assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), path
 
 
 def test_small_batch_workload_full_size():
@@ -316,23 +361,31 @@ def check_full_size(name, P, n, k, op, seed, dist):
     ct = torch.from_numpy(cols).to(DEV)
     xs = X[:, ct].cpu().numpy()
     ref_max = X.amax(dim=0) if op == "max" else None
-    note("%s P=%d n=%d k=%d op=%s: execute" % (name, P, n, k, op))
-    plan = ar.Plan(P, n, "float32", op, k)
-    plan([X[i] for i in range(P)])
-    torch.cuda.synchronize()
-    got = X[:, ct].cpu().numpy()
     want = oracle.allreduce(xs, k, op, n=n, cols=cols)
-    assert np.array_equal(bits(got), bits(want))
-    if op == "sum":
-        assert_fp32_bound(got, xs)
-        if k == 2 * ceil_log2(P):  # bandwidth-optimal: every rank holds the same bits
-            for i in range(1, P):
-                assert torch.equal(X[0].view(torch.int32), X[i].view(torch.int32))
-    else:
-        for i in range(P):
-            assert torch.equal(X[i], ref_max)
-    plan.close()
-    del X
+    X0 = X.clone() if len(paths(P, k)) > 1 else None
+    results = []
+    for path in paths(P, k):
+        if path != ar.AR_PATH_STEPWISE:
+            X.copy_(X0)
+        note("%s P=%d n=%d k=%d op=%s path=%d: execute" % (name, P, n, k, op, path))
+        plan = ar.Plan(P, n, "float32", op, k, path=path)
+        plan([X[i] for i in range(P)])
+        torch.cuda.synchronize()
+        got = X[:, ct].cpu().numpy()
+        assert np.array_equal(bits(got), bits(want)), path
+        if op == "sum":
+            assert_fp32_bound(got, xs)
+            if k == 2 * ceil_log2(P):  # bandwidth-optimal: every rank holds the same bits
+                for i in range(1, P):
+                    assert torch.equal(X[0].view(torch.int32), X[i].view(torch.int32))
+                results.append(X[0].clone())
+        else:
+            for i in range(P):
+                assert torch.equal(X[i], ref_max)
+        plan.close()
+    if len(results) == 2:  # the whole vector, not only the sampled columns, agrees across paths
+        assert torch.equal(results[0].view(torch.int32), results[1].view(torch.int32))
+    del X, X0, results
     torch.cuda.empty_cache()
 
 
