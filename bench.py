@@ -78,7 +78,7 @@ DESCRIPTIONS = {
 
 def kernel_source_hash():
     h = hashlib.sha256()
-    for f in ("kernels.hip", "capi.cpp", "plan.cpp", "ar_internal.hpp", "device_common.hpp", "fused_bo.hpp"):
+    for f in ("kernels.hip", "capi.cpp", "plan.cpp", "ar_internal.hpp", "device_common.hpp", "fused_col.hpp"):
         with open(os.path.join(ROOT, "paper_2004_09362_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -278,8 +278,14 @@ def main():
     bytes_per_launch = alg / launches
     launch_ms = dom_ms / launches
     achieved = bytes_per_launch / (launch_ms * 1e-3) / 1e9
-    kname = (("fused_bo_kernel<P=%d>" if st.r == 0 else "fused_lo_kernel<P=%d>") % dj["P"]) if fused \
-        else "step_kernel"
+    if not fused:
+        kname = "step_kernel"
+    elif st.r == 0:
+        kname = "fused_bo_kernel<P=%d>" % dj["P"]
+    elif st.r == st.L and dj["P"] <= 16:
+        kname = "fused_lo_kernel<P=%d>" % dj["P"]
+    else:
+        kname = "fused_mid_kernel<P=%d>" % dj["P"]
     src_hash = kernel_source_hash()
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),

@@ -17,8 +17,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libar.so")
 SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip"] +
-           ["fused_bo_g%d.hip" % i for i in range(8)]]
-HEADERS = [os.path.join(CSRC, f) for f in ("ar_internal.hpp", "device_common.hpp", "fused_bo.hpp")] + [
+           ["fused_col_g%d.hip" % i for i in range(8)]]
+HEADERS = [os.path.join(CSRC, f) for f in ("ar_internal.hpp", "device_common.hpp", "fused_col.hpp")] + [
     os.path.join(ROOT, "include", "ar.h")]
 OBJDIR = os.path.join(HERE, "_build")
 
@@ -35,8 +35,12 @@ FLAGS = [
 ]
 
 
-def _compile(src: str) -> tuple[str, str]:
+def _compile(src: str, incremental: bool = False) -> tuple[str, str]:
     obj = os.path.join(OBJDIR, os.path.basename(src) + ".o")
+    if incremental and os.path.exists(obj):
+        t = os.path.getmtime(obj)
+        if all(os.path.getmtime(f) <= t for f in [src] + HEADERS):
+            return obj, ""
     res = subprocess.run([HIPCC] + FLAGS + ["-c", src, "-o", obj], capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError("hipcc failed on %s:\n%s%s" % (src, res.stdout, res.stderr))
@@ -44,13 +48,14 @@ def _compile(src: str) -> tuple[str, str]:
     return obj, "\n".join(warn)
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source (in parallel) and link libar.so; always rebuilds."""
+def build(verbose: bool = False, incremental: bool = False) -> str:
+    """Compile every source (in parallel) and link libar.so.  Rebuilds every
+    unit unless ``incremental`` (then only units older than their sources)."""
     t0 = time.time()
     os.makedirs(OBJDIR, exist_ok=True)
     workers = max(1, min(len(SOURCES), int(os.environ.get("MAX_JOBS", os.cpu_count() or 1))))
     with concurrent.futures.ThreadPoolExecutor(max_workers=workers) as ex:
-        results = list(ex.map(_compile, SOURCES))
+        results = list(ex.map(lambda src: _compile(src, incremental), SOURCES))
     if verbose:
         for _, warn in results:
             if warn:
@@ -75,4 +80,4 @@ def stale() -> bool:
 
 
 if __name__ == "__main__":
-    build(verbose=True)
+    build(verbose=True, incremental="--incremental" in sys.argv)

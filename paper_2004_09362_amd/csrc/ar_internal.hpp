@@ -113,7 +113,7 @@ struct ColArgs {
   int64_t stride, q, m;     // instance stride, n / P, n % P
   uint32_t total_tiles;     // batch * P * tiles (< 2^31)
   FastDiv tiles, pdiv;      // column tiles per block, P
-  int32_t P;
+  int32_t P, r;             // r: distribution steps removed (kept shifts w = min(2^r, P))
 };
 
 // dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.
@@ -121,11 +121,14 @@ int launch_step(const StepArgs& a, int dtype, int op, bool vec, bool nt, int gri
 // Fused latency-optimal kernel; mode 0: 16-byte columns groups, 1: one
 // element per lane (contiguous instances), 2: any instance stride.
 int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, int mode, bool nt, int grid, void* stream);
-// Column-fused bandwidth-optimal kernel, one instantiation per P
-// (fused_bo_g*.hip), and its dispatcher over P = 2..128.
+// Column-fused kernels, one instantiation per P (fused_col_g*.hip):
+// bandwidth-optimal (r = 0) and shifted / latency-optimal (r >= 1), and
+// their dispatcher over P = 2..128.
 template <int P>
 int launch_fused_bo(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream);
-int launch_fused_bo_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream);
+template <int P>
+int launch_fused_mid(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream);
+int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream);
 // Workgroups of a step launch over `total_tiles` wave tiles, and the tile size.
 int step_grid(int64_t total_tiles);
 int64_t step_tile_elems();

@@ -22,8 +22,10 @@
 constexpr int64_t kNtThresholdBytes = int64_t(512) << 20;
 constexpr int64_t kFusedNtThresholdBytes = int64_t(128) << 20;
 
-// Which single-launch kernel can run a plan.
-enum FusedKind { kFusedNone = 0, kFusedLo = 1, kFusedBo = 2 };
+// Which single-launch kernel runs a plan on the FUSED path: the flat
+// latency-optimal kernel (small P; its columns need no block index) or the
+// block-tiled column kernels (every other plan).
+enum FusedKind { kFusedNone = 0, kFusedLo = 1, kFusedCol = 2 };
 
 struct ar_plan {
   ar::Schedule s;
@@ -185,12 +187,13 @@ ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   return AR_OK;
 }
 
-ar_status run_fused_bo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, hipStream_t stream) {
+ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, hipStream_t stream) {
   const ar::Schedule& s = pl->s;
   ar::ColArgs a;
   std::memset(&a, 0, sizeof a);
   for (int32_t x = 0; x < 2 * s.P; ++x) a.user[x] = bufs[x % s.P];
   a.P = s.P;
+  a.r = s.r;
   a.stride = stride;
   a.q = s.n / s.P;
   a.m = s.n % s.P;
@@ -204,8 +207,8 @@ ar_status run_fused_bo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   a.tiles = ar::make_fastdiv(uint32_t(tiles));
   a.pdiv = ar::make_fastdiv(uint32_t(s.P));
   const bool nt = use_nt(pl->fused_nt_mode, int64_t(2) * s.P * s.n * batch * 4, kFusedNtThresholdBytes);
-  const int e = ar::launch_fused_bo_any(a, s.P, pl->dtype, pl->op, nt, ar::step_grid(total), stream);
-  if (e != 0) return hip_fail(hipError_t(e), "fused bandwidth-optimal kernel launch");
+  const int e = ar::launch_fused_col_any(a, s.P, pl->dtype, pl->op, nt, ar::step_grid(total), stream);
+  if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");
   return AR_OK;
 }
 
@@ -234,8 +237,8 @@ ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t
   pl->nt_mode = env_mode("AR_STEP_NT");
   pl->fused_nt_mode = env_mode("AR_FUSED_NT");
   pl->fused_mode = env_mode("AR_FUSED_MODE");
-  if (pl->s.P >= 2 && pl->s.r == 0) pl->fused_kind = kFusedBo;
-  else if (pl->s.P >= 2 && pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L) pl->fused_kind = kFusedLo;
+  if (pl->s.P >= 2 && pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L) pl->fused_kind = kFusedLo;
+  else if (pl->s.P >= 2) pl->fused_kind = kFusedCol;
   pl->fused_ok = pl->fused_kind != kFusedNone;
   *out_plan = pl;
   g_err.clear();
@@ -247,8 +250,7 @@ ar_status ar_plan_set_path(ar_plan* plan, ar_path path) {
   if (path != AR_PATH_AUTO && path != AR_PATH_STEPWISE && path != AR_PATH_FUSED)
     return fail(AR_ERR_INVALID_ARG, "unknown path");
   if (path == AR_PATH_FUSED && !plan->fused_ok)
-    return fail(AR_ERR_UNSUPPORTED,
-                "the fused path runs bandwidth-optimal plans, and latency-optimal plans with P <= 16");
+    return fail(AR_ERR_UNSUPPORTED, "a single rank has nothing to fuse");
   plan->path = path;
   return AR_OK;
 }
@@ -274,8 +276,8 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
   const int64_t elems = int64_t(plan->s.P) * plan->s.n * batch;
   if (elems / batch / plan->s.P != plan->s.n) return fail(AR_ERR_INVALID_ARG, "size overflow");
   const bool fused = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok);
-  if (fused && plan->fused_kind == kFusedBo) {
-    st = run_fused_bo(plan, rank_buffers, batch, instance_stride, stream);
+  if (fused && plan->fused_kind == kFusedCol) {
+    st = run_fused_col(plan, rank_buffers, batch, instance_stride, stream);
   } else if (fused) {
     st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream);
   } else {

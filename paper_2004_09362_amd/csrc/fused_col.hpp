@@ -1,0 +1,248 @@
+// fused_col.hpp -- column-fused Allreduce kernels: every step of the
+// schedule applied to element columns held in registers.
+//
+// fused_bo_kernel: bandwidth-optimal schedules (r = 0).
+// Kolmakov & Zhang, "A Generalization of the Allreduce Operation"
+// (arXiv:2004.09362), Sec. 7.  For block b, placement p of the reduction
+// lives on rank b + p, so one element column of block b is the array
+// W[p] = V_{b+p}[e], p = 0..P-1.  Reduction step i (N_i vectors, f_i =
+// floor(N_i/2), c_i = ceil(N_i/2)) combines the kept placements
+// [c_i - f_i, c_i) with the received [c_i, N_i): W[p] = W[p] (+) W[p + f_i].
+// After ceil(log2 P) steps W[0] holds the reduction of the column, and the
+// distribution phase hands that same value to every rank.  Doing this per
+// column in registers combines exactly the operand pairs of the step-by-step
+// schedule, in the same order, so the bits are identical -- but every input
+// is read once and every output written once (2 * P * n elements of HBM
+// traffic instead of 5 * (P - 1) * n).
+//
+// One wave covers 64 consecutive columns of one block of one instance, one
+// 4-byte element per lane: the block, hence the rotation of the rank
+// pointers, is uniform across the wave and every access is a coalesced
+// 256-byte row of one rank buffer.  Blocks start at arbitrary elements, so
+// the tiles of a block are laid on 256-byte boundaries of the buffer (the
+// first and last tile of a block are partial): rows that straddled cache
+// lines cost a third more line transfers, and much more when streamed
+// nontemporally.  P is a template parameter so that W stays in registers
+// with static indices.
+#pragma once
+
+#include <type_traits>
+#include <utility>
+
+#include "device_common.hpp"
+
+namespace ar {
+
+constexpr int col_L(int P) {
+  int L = 0;
+  while ((1 << L) < P) ++L;
+  return L;
+}
+
+constexpr int col_N(int P, int i) {
+  int N = P;
+  for (int j = 0; j < i; ++j) N -= N / 2;
+  return N;
+}
+
+// Placement whose starred result reaches placement q through the
+// distribution phase, for 2^r shifted schedules (Secs. 7-8): placements
+// [0, w) are held after the reduction; the reversed step i (run only when
+// N_i exceeds the placements held so far, h) delivers [max(c_i, h), N_i)
+// from placement q - f_i of rank x - f_i, i.e. from the same block.
+constexpr int col_src(int P, int r, int q) {
+  const int L = col_L(P);
+  const int w = (1 << r) < P ? (1 << r) : P;
+  int lo[16] = {}, hi[16] = {}, fs[16] = {};
+  int k = 0, h = w;
+  for (int i = L - 1; i >= 0; --i) {
+    const int N = col_N(P, i);
+    if (N <= h) continue;
+    const int f = N / 2, c = N - f;
+    lo[k] = c > h ? c : h;
+    hi[k] = N;
+    fs[k] = f;
+    ++k;
+    h = N;
+  }
+  for (int t = k - 1; t >= 0; --t)
+    if (q >= lo[t] && q < hi[t]) q -= fs[t];
+  return q;
+}
+
+template <int N, int OP, typename T, int P>
+__device__ __forceinline__ void bo_fold(T (&w)[P]) {
+  if constexpr (N > 1) {
+    constexpr int f = N / 2;
+    constexpr int c = N - f;
+#pragma unroll
+    for (int j = c - f; j < c; ++j) w[j] = comb<OP>(w[j], w[j + f]);
+    bo_fold<c, OP, T, P>(w);
+  }
+}
+
+template <int P, typename T, int OP, bool NT>
+__global__ __launch_bounds__(kBlock) void fused_bo_kernel(const ColArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
+       t += gridDim.x * uint32_t(kWavesPerBlock)) {
+    const uint32_t seg = fdiv(t, a.tiles);  // seg = instance * P + block
+    const uint32_t tile = t - seg * a.tiles.d;
+    const uint32_t inst = fdiv(seg, a.pdiv);
+    const int32_t b = int32_t(seg - inst * a.pdiv.d);
+    const int64_t len = a.q + (b < a.m ? 1 : 0);
+    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+    void* const* rot = a.user + b;  // rot[d] is rank (b + d) mod P
+    // columns before the first 256-byte boundary of the root rank's row
+    const int64_t lo = ((reinterpret_cast<uintptr_t>(rot[0]) >> 2) + e0) & (kWave - 1);
+    const int64_t c = int64_t(tile) * kWave - lo + lane;
+    if (c >= 0 && c < len) {
+      const int64_t e = e0 + c;
+      T w[P];
+#pragma unroll
+      for (int d = 0; d < P; ++d) w[d] = ld1<NT>(static_cast<const T*>(rot[d]) + e);
+      bo_fold<P, OP, T, P>(w);
+#pragma unroll
+      for (int d = 0; d < P; ++d) st1<NT>(static_cast<T*>(rot[d]) + e, w[0]);
+    }
+  }
+}
+
+// fused_mid_kernel: shifted (intermediate) and latency-optimal schedules,
+// 1 <= r <= ceil(log2 P).  For block b the column is V[d] = V_{b+d}[e].  The
+// primed sums R[d] and starred sums S[d] of every offset d follow the
+// reduction steps of Secs. 8-9: with f = floor(N_i/2), S[d] takes R[d + f]
+// when N_i is even and R[d] takes R[d + f] on every step but the last.
+// S[s] is then the starred result of shift s, rooted at rank b + s -- the
+// recursion does not depend on how many shifts are kept -- and rank b + q
+// receives S[col_src(q)], the result the distribution phase brings it.
+// All P starred sums are computed whatever r is (at most P(2L - 2)
+// combines per column, far below the memory time), so one kernel per P
+// serves every r, and the store pattern is picked by a uniform branch.
+template <int P, int I, int OP, typename T>
+__device__ __forceinline__ void mid_steps(T (&R)[P], T (&S)[P]) {
+  constexpr int L = col_L(P);
+  if constexpr (I < L) {
+    constexpr int N = col_N(P, I);
+    constexpr int f = N / 2;
+    constexpr bool even = (N % 2) == 0;
+    constexpr bool last = (I == L - 1);
+    T Rn[P];
+#pragma unroll
+    for (int d = 0; d < P; ++d) {
+      const T recv = R[(d + f) % P];
+      if constexpr (even) S[d] = comb<OP>(S[d], recv);
+      if constexpr (!last) Rn[d] = comb<OP>(R[d], recv);
+    }
+    if constexpr (!last) {
+#pragma unroll
+      for (int d = 0; d < P; ++d) R[d] = Rn[d];
+    }
+    mid_steps<P, I + 1, OP, T>(R, S);
+  }
+}
+
+// Rank offset q stores S[col_src(q)]; the index is forced to a compile-time
+// constant so the table never reaches memory.
+template <int P, int RR, bool NT, typename T, int... Qs>
+__device__ __forceinline__ void mid_store_seq(void* const* rot, int64_t e, const T (&S)[P],
+                                              std::integer_sequence<int, Qs...>) {
+  (st1<NT>(static_cast<T*>(rot[Qs]) + e, S[std::integral_constant<int, col_src(P, RR, Qs)>::value]), ...);
+}
+
+template <int P, int RR, bool NT, typename T>
+__device__ __forceinline__ void mid_store(void* const* rot, int64_t e, const T (&S)[P]) {
+  mid_store_seq<P, RR, NT, T>(rot, e, S, std::make_integer_sequence<int, P>{});
+}
+
+template <int P, int RR, bool NT, typename T>
+__device__ __forceinline__ void mid_store_r(int r, void* const* rot, int64_t e, const T (&S)[P]) {
+  if constexpr (RR <= col_L(P)) {
+    if (r == RR) mid_store<P, RR, NT, T>(rot, e, S);
+    else mid_store_r<P, RR + 1, NT, T>(r, rot, e, S);
+  }
+}
+
+template <int P, typename T, int OP, bool NT>
+__global__ __launch_bounds__(kBlock) void fused_mid_kernel(const ColArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
+       t += gridDim.x * uint32_t(kWavesPerBlock)) {
+    const uint32_t seg = fdiv(t, a.tiles);
+    const uint32_t tile = t - seg * a.tiles.d;
+    const uint32_t inst = fdiv(seg, a.pdiv);
+    const int32_t b = int32_t(seg - inst * a.pdiv.d);
+    const int64_t len = a.q + (b < a.m ? 1 : 0);
+    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+    void* const* rot = a.user + b;
+    const int64_t lo = ((reinterpret_cast<uintptr_t>(rot[0]) >> 2) + e0) & (kWave - 1);
+    const int64_t c = int64_t(tile) * kWave - lo + lane;
+    if (c >= 0 && c < len) {
+      const int64_t e = e0 + c;
+      T R[P], S[P];
+#pragma unroll
+      for (int d = 0; d < P; ++d) {
+        R[d] = ld1<NT>(static_cast<const T*>(rot[d]) + e);
+        S[d] = R[d];
+      }
+      mid_steps<P, 0, OP, T>(R, S);
+      mid_store_r<P, 1, NT, T>(a.r, rot, e, S);
+    }
+  }
+}
+
+template <int P>
+int launch_fused_bo(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const dim3 g(grid), blk(kBlock);
+  if (dtype == 0) {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 1, false>), g, blk, 0, s, a);
+    }
+  } else {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, float, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_bo_kernel<P, float, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, float, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_bo_kernel<P, float, 1, false>), g, blk, 0, s, a);
+    }
+  }
+  return int(hipGetLastError());
+}
+
+}  // namespace ar
+
+namespace ar {
+
+template <int P>
+int launch_fused_mid(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const dim3 g(grid), blk(kBlock);
+  if (dtype == 0) {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 1, false>), g, blk, 0, s, a);
+    }
+  } else {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, float, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_mid_kernel<P, float, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, float, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_mid_kernel<P, float, 1, false>), g, blk, 0, s, a);
+    }
+  }
+  return int(hipGetLastError());
+}
+
+}  // namespace ar

@@ -1,0 +1,41 @@
+// fused_col_g2.hip -- instantiations of the column-fused kernels
+// (bandwidth-optimal and shifted/latency-optimal) for P = 4, 12, ..., 124 (every 8th P; the eight files share the
+// work evenly and compile in parallel).
+#include "fused_col.hpp"
+
+namespace ar {
+
+template int launch_fused_bo<4>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<4>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<12>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<12>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<20>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<20>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<28>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<28>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<36>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<36>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<44>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<44>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<52>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<52>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<60>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<60>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<68>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<68>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<76>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<76>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<84>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<84>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<92>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<92>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<100>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<100>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<108>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<108>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<116>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<116>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_bo<124>(const ColArgs&, int, int, bool, int, void*);
+template int launch_fused_mid<124>(const ColArgs&, int, int, bool, int, void*);
+
+}  // namespace ar

@@ -22,7 +22,7 @@
 //                path, so the results are bit-identical, but each input is
 //                read once and each output written once (2*P*n elements).
 //
-// The column-fused bandwidth-optimal kernel is in fused_bo.hpp.
+// The column-fused kernels are in fused_col.hpp.
 //
 // Compiled with packed-fp32 instructions disabled; only adds and compares,
 // so no contraction question arises.
@@ -323,10 +323,12 @@ int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, int mode, bool
   return op == 0 ? launch_fused_t<float, 0>(a, P, mode, nt, grid, s) : launch_fused_t<float, 1>(a, P, mode, nt, grid, s);
 }
 
-int launch_fused_bo_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream) {
+int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream) {
   switch (P) {
-#define AR_BO_CASE(PP) \
-  case PP: return launch_fused_bo<PP>(a, dtype, op, nt, grid, stream);
+#define AR_BO_CASE(PP)                                                                                \
+  case PP:                                                                                            \
+    return a.r == 0 ? launch_fused_bo<PP>(a, dtype, op, nt, grid, stream)                             \
+                    : launch_fused_mid<PP>(a, dtype, op, nt, grid, stream);
 #define AR_BO_CASE8(B) AR_BO_CASE(B) AR_BO_CASE(B + 1) AR_BO_CASE(B + 2) AR_BO_CASE(B + 3) \
   AR_BO_CASE(B + 4) AR_BO_CASE(B + 5) AR_BO_CASE(B + 6) AR_BO_CASE(B + 7)
     AR_BO_CASE8(2) AR_BO_CASE8(10) AR_BO_CASE8(18) AR_BO_CASE8(26) AR_BO_CASE8(34) AR_BO_CASE8(42)
