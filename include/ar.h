@@ -147,6 +147,26 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out);
 ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* out);
 ar_status ar_plan_launch(const ar_plan* plan, int32_t i, ar_launch_desc* desc, ar_range_desc* ranges, int32_t cap);
 
+/* Cost model (Sec. 2: a message of m bytes costs alpha + beta*m to send and
+ * gamma*m to combine; u = m/P per block).  ar_model_time evaluates the
+ * paper's cost equation for a k-step schedule of an m-byte vector over P
+ * ranks: the bandwidth-optimal one (Sec. 7, k = 2L), the intermediate one
+ * (Sec. 8, r = 2L - k removed steps) or the latency-optimal one (Sec. 9,
+ * k = L), L = ceil(log2 P).  The Sec. 8 equation assumes the 2^r shifted
+ * schedules do not wrap round the P placements; ar_plan_model_time prices
+ * a plan's exact steps, blocks received and combinations instead, which
+ * equal the equation's terms without wrap and fall below them with it.
+ * ar_model_best_k returns the k in [L, 2L] with the smallest
+ * ar_model_time, and the closed-form optimum r* of Sec. 8 (a real number;
+ * NaN where its logarithms are undefined, e.g. P <= 2).
+ * Errors: AR_ERR_INVALID_ARG for P outside [1, 128], k outside [L, 2L],
+ * negative m/alpha/beta/gamma or NULL outputs. */
+ar_status ar_model_time(int32_t P, double m_bytes, int32_t k_steps, double alpha, double beta, double gamma,
+                        double* tau_seconds);
+ar_status ar_model_best_k(int32_t P, double m_bytes, double alpha, double beta, double gamma, int32_t* k_steps,
+                          double* r_closed_form);
+ar_status ar_plan_model_time(const ar_plan* plan, double alpha, double beta, double gamma, double* tau_seconds);
+
 /* Wait for the plan's last stream, free its scratch and the plan.  NULL is
  * accepted.  Must not be called while another thread executes the plan. */
 void ar_plan_destroy(ar_plan* plan);

@@ -28,6 +28,7 @@ AR_KIND_COPY, AR_KIND_REDUCE, AR_KIND_REDUCE2 = 0, 1, 2
 EXPORTS = [
     "ar_plan_create", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
     "ar_plan_num_launches", "ar_plan_launch", "ar_plan_destroy", "ar_status_string", "ar_last_error",
+    "ar_model_time", "ar_model_best_k", "ar_plan_model_time",
 ]
 
 
@@ -80,12 +81,16 @@ def _load():
     L.ar_plan_launch.argtypes = [vp, i32, ctypes.POINTER(LaunchDesc), ctypes.POINTER(RangeDesc), i32]
     L.ar_plan_destroy.argtypes = [vp]
     L.ar_plan_destroy.restype = None
+    dbl = ctypes.c_double
+    L.ar_model_time.argtypes = [i32, dbl, i32, dbl, dbl, dbl, ctypes.POINTER(dbl)]
+    L.ar_model_best_k.argtypes = [i32, dbl, dbl, dbl, dbl, ctypes.POINTER(i32), ctypes.POINTER(dbl)]
+    L.ar_plan_model_time.argtypes = [vp, dbl, dbl, dbl, ctypes.POINTER(dbl)]
     L.ar_status_string.argtypes = [ctypes.c_int]
     L.ar_status_string.restype = ctypes.c_char_p
     L.ar_last_error.argtypes = []
     L.ar_last_error.restype = ctypes.c_char_p
     for name in ("ar_plan_create", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
-                 "ar_plan_num_launches", "ar_plan_launch"):
+                 "ar_plan_num_launches", "ar_plan_launch", "ar_model_time", "ar_model_best_k", "ar_plan_model_time"):
         getattr(L, name).restype = ctypes.c_int
     return L
 
@@ -175,6 +180,24 @@ def ar_plan_launch(plan: int, i: int):
     rs = (RangeDesc * max(1, d.n_ranges))()
     _check(lib.ar_plan_launch(plan, i, ctypes.byref(d), rs, d.n_ranges), "ar_plan_launch")
     return d.phase, [rs[j].as_dict() for j in range(d.n_ranges)]
+
+
+def ar_model_time(P: int, m_bytes: float, k_steps: int, alpha: float, beta: float, gamma: float) -> float:
+    t = ctypes.c_double()
+    _check(lib.ar_model_time(P, m_bytes, k_steps, alpha, beta, gamma, ctypes.byref(t)), "ar_model_time")
+    return t.value
+
+
+def ar_model_best_k(P: int, m_bytes: float, alpha: float, beta: float, gamma: float):
+    k, r = ctypes.c_int32(), ctypes.c_double()
+    _check(lib.ar_model_best_k(P, m_bytes, alpha, beta, gamma, ctypes.byref(k), ctypes.byref(r)), "ar_model_best_k")
+    return k.value, r.value
+
+
+def ar_plan_model_time(plan: int, alpha: float, beta: float, gamma: float) -> float:
+    t = ctypes.c_double()
+    _check(lib.ar_plan_model_time(plan, alpha, beta, gamma, ctypes.byref(t)), "ar_plan_model_time")
+    return t.value
 
 
 def ar_plan_destroy(plan: int):

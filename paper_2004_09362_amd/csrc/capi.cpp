@@ -6,6 +6,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <cmath>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -361,6 +362,71 @@ ar_status ar_plan_launch(const ar_plan* plan, int32_t i, ar_launch_desc* desc, a
       ranges[j] = ar_range_desc{r.p0, r.count, r.kind, r.delta, r.dst, r.own, r.dst2, r.own2, r.src};
     }
   }
+  return AR_OK;
+}
+
+ar_status ar_model_time(int32_t P, double m_bytes, int32_t k_steps, double alpha, double beta, double gamma,
+                        double* tau_seconds) {
+  if (!tau_seconds) return fail(AR_ERR_INVALID_ARG, "tau_seconds is NULL");
+  if (P < 1 || P > ar::kMaxP) return fail(AR_ERR_INVALID_ARG, "P must be in [1, 128]");
+  if (!(m_bytes >= 0) || !(alpha >= 0) || !(beta >= 0) || !(gamma >= 0))
+    return fail(AR_ERR_INVALID_ARG, "m, alpha, beta and gamma must be >= 0");
+  int32_t L = 0;
+  while ((1 << L) < P) ++L;
+  if (k_steps < L || k_steps > 2 * L) return fail(AR_ERR_INVALID_ARG, "k_steps outside [L, 2L]");
+  const int32_t r = 2 * L - k_steps;
+  const double u = m_bytes / P;
+  double t;
+  if (P == 1) {
+    t = 0.0;
+  } else if (r == 0) {  // Sec. 7
+    t = 2.0 * L * alpha + 2.0 * (P - 1) * u * beta + double(P - 1) * u * gamma;
+  } else if (r == L) {  // Sec. 9
+    t = double(L) * alpha + double(P) * L * u * beta + double(P) * (2 * L - 2) * u * gamma;
+  } else {              // Sec. 8
+    const double x = double((int64_t(1) << r) - 1);
+    t = double(2 * L - r) * alpha + (2.0 * (P - 1) + x * (L - 1)) * u * beta + ((P - 1) + x * (2 * L - 2)) * u * gamma;
+  }
+  *tau_seconds = t;
+  return AR_OK;
+}
+
+ar_status ar_model_best_k(int32_t P, double m_bytes, double alpha, double beta, double gamma, int32_t* k_steps,
+                          double* r_closed_form) {
+  if (!k_steps) return fail(AR_ERR_INVALID_ARG, "k_steps is NULL");
+  if (P < 1 || P > ar::kMaxP) return fail(AR_ERR_INVALID_ARG, "P must be in [1, 128]");
+  int32_t L = 0;
+  while ((1 << L) < P) ++L;
+  double best = 0;
+  int32_t best_k = -1;
+  for (int32_t k = L; k <= 2 * L; ++k) {
+    double t = 0;
+    const ar_status st = ar_model_time(P, m_bytes, k, alpha, beta, gamma, &t);
+    if (st != AR_OK) return st;
+    if (best_k < 0 || t < best) {
+      best = t;
+      best_k = k;
+    }
+  }
+  *k_steps = best_k;
+  if (r_closed_form) {
+    // Sec. 8: r* = log2(alpha / (m (beta + 2 gamma))) + log2(P / ((log2 P - 1) ln 2))
+    const double lp = std::log2(double(P));
+    const double den = m_bytes * (beta + 2 * gamma);
+    *r_closed_form = (P > 2 && den > 0 && alpha > 0)
+                         ? std::log2(alpha / den) + std::log2(double(P) / ((lp - 1.0) * std::log(2.0)))
+                         : std::nan("");
+  }
+  return AR_OK;
+}
+
+ar_status ar_plan_model_time(const ar_plan* plan, double alpha, double beta, double gamma, double* tau_seconds) {
+  if (!plan || !tau_seconds) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+  if (!(alpha >= 0) || !(beta >= 0) || !(gamma >= 0)) return fail(AR_ERR_INVALID_ARG, "negative model parameter");
+  const ar::Schedule& s = plan->s;
+  const double u = double(s.n) * 4 / s.P;  // bytes per (average) block
+  *tau_seconds = double(s.k) * alpha + double(s.blocks_pulled_per_rank) * u * beta +
+                 double(s.combines_per_rank) * u * gamma;
   return AR_OK;
 }
 

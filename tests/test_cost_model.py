@@ -1,0 +1,123 @@
+"""Cost model of the library (Sec. 2 model, Secs. 7-9 cost equations) on
+the host: against the paper's equations, its Table 2 parameters, its
+statements about which version wins, and the plans' exact counts."""
+import math
+
+import pytest
+
+from paper_2004_09362_amd import ar
+
+ALPHA, BETA, GAMMA = 3e-5, 1e-8, 2e-10   # Table 2: the authors' 10 GbE cluster
+
+
+def ceil_log2(P):
+    return max(0, (P - 1).bit_length())
+
+
+def paper_tau(P, m, k, a, b, g):
+    """The cost equations as printed (Sec. 7 bandwidth-optimal, Sec. 8 with
+    r removed steps, Sec. 9 latency-optimal), u = m / P."""
+    L = ceil_log2(P)
+    r = 2 * L - k
+    u = m / P
+    if P == 1:
+        return 0.0
+    if r == 0:
+        return 2 * L * a + 2 * (P - 1) * u * b + (P - 1) * u * g
+    if r == L:
+        return L * a + P * L * u * b + P * (2 * L - 2) * u * g
+    return (2 * L - r) * a + (2 * (P - 1) + (2 ** r - 1) * (L - 1)) * u * b + \
+        ((P - 1) + (2 ** r - 1) * (2 * L - 2)) * u * g
+
+
+@pytest.mark.parametrize("P", [1, 2, 3, 5, 7, 8, 12, 24, 37, 64, 100, 127, 128])
+def test_model_time_follows_the_cost_equations(P):
+    L = ceil_log2(P)
+    for m in (425.0, 9216.0, 1 << 20, 1 << 26):
+        for k in range(L, 2 * L + 1):
+            got = ar.ar_model_time(P, m, k, ALPHA, BETA, GAMMA)
+            assert got == pytest.approx(paper_tau(P, m, k, ALPHA, BETA, GAMMA), rel=1e-12, abs=1e-15)
+
+
+def test_small_messages_choose_the_latency_optimal_version():
+    """Sec. 10: at m = 425 B (the average message of Sec. 1) the proposed
+    algorithm runs its latency-optimal version for every P."""
+    for P in range(2, 129):
+        k, r = ar.ar_model_best_k(P, 425.0, ALPHA, BETA, GAMMA)
+        assert k == ceil_log2(P), P
+
+
+def test_large_messages_choose_the_bandwidth_optimal_version():
+    """(P = 2 is the exception: its latency-optimal version moves the same
+    data as the bandwidth-optimal one in one step fewer.)"""
+    assert ar.ar_model_best_k(2, float(1 << 28), ALPHA, BETA, GAMMA)[0] == 1
+    for P in range(3, 129):
+        k, _ = ar.ar_model_best_k(P, float(1 << 28), ALPHA, BETA, GAMMA)
+        assert k == 2 * ceil_log2(P), P
+
+
+def test_best_k_is_the_minimum_and_near_the_closed_form():
+    """ar_model_best_k is the discrete minimum over every k.  The Sec. 8
+    closed form r* = log(alpha / (m (beta + 2 gamma))) + log(P / ((log P - 1)
+    ln 2)) minimises the Sec. 8 equation, whose domain is 0 <= r < ceil(log P)
+    (the latency-optimal corner is priced separately, Sec. 9), after relaxing
+    ceil(log P) - 1 to log P - 1; rounded into that domain it lands within
+    one step of the equation's own discrete minimum."""
+    for P in (5, 12, 24, 37, 100, 127):
+        L = ceil_log2(P)
+        for e in range(6, 30):
+            m = float(2 ** e)
+            k, r = ar.ar_model_best_k(P, m, ALPHA, BETA, GAMMA)
+            times = [ar.ar_model_time(P, m, kk, ALPHA, BETA, GAMMA) for kk in range(L, 2 * L + 1)]
+            assert ar.ar_model_time(P, m, k, ALPHA, BETA, GAMMA) == min(times)
+            rr = math.log2(ALPHA / (m * (BETA + 2 * GAMMA))) + math.log2(P / ((math.log2(P) - 1) * math.log(2)))
+            assert r == pytest.approx(rr, rel=1e-12)
+            # minimum of the Sec. 8 equation alone, r in [0, L - 1]
+            mid = min(range(L + 1, 2 * L + 1), key=lambda kk: ar.ar_model_time(P, m, kk, ALPHA, BETA, GAMMA))
+            r_int = min(L - 1, max(0, round(r)))
+            assert abs((2 * L - r_int) - mid) <= 1, (P, e, r, mid)
+
+
+def test_table2_worked_numbers():
+    """Table 2 parameters at P = 127: m = 9 KiB is best at k = 11 (r* about
+    3.3), and P = 37, m = 16 MiB costs 330 ms bandwidth-optimal."""
+    k, r = ar.ar_model_best_k(127, 9216.0, ALPHA, BETA, GAMMA)
+    assert k == 11 and r == pytest.approx(3.26, abs=0.01)
+    assert ar.ar_model_time(127, 9216.0, 11, ALPHA, BETA, GAMMA) == pytest.approx(0.546e-3, rel=2e-3)
+    assert ar.ar_model_time(37, 16.0 * 2 ** 20, 12, ALPHA, BETA, GAMMA) == pytest.approx(0.3301, rel=1e-3)
+
+
+@pytest.mark.parametrize("P", range(2, 129))
+def test_plan_prices_exact_counts_against_the_equations(P):
+    """A plan's exact schedule costs what the equations say, except that the
+    Sec. 8 traffic term over-counts once the shifted schedules wrap round
+    the P placements (2^r > ceil(P/2) + 1), and the combination terms of
+    Secs. 8-9 are worst cases."""
+    L = ceil_log2(P)
+    n = 4 * P  # four elements per block: u = 16 bytes
+    m = 4.0 * n
+    for k in range(L, 2 * L + 1):
+        r = 2 * L - k
+        plan = ar.Plan(P, n, "float32", "sum", k)
+        assert ar.ar_plan_model_time(plan.handle, 1.0, 0.0, 0.0) == pytest.approx(k)
+        beta_plan = ar.ar_plan_model_time(plan.handle, 0.0, 1.0, 0.0)
+        beta_eq = ar.ar_model_time(P, m, k, 0.0, 1.0, 0.0)
+        if r in (0, L) or 2 ** r <= (P + 1) // 2 + 1:
+            assert beta_plan == pytest.approx(beta_eq)
+        else:
+            assert beta_plan < beta_eq
+        gamma_plan = ar.ar_plan_model_time(plan.handle, 0.0, 0.0, 1.0)
+        gamma_eq = ar.ar_model_time(P, m, k, 0.0, 0.0, 1.0)
+        assert gamma_plan <= gamma_eq * (1 + 1e-12) or P == 2
+        if r == 0:
+            assert gamma_plan == pytest.approx(gamma_eq)
+
+
+def test_model_rejects_bad_arguments():
+    for args in [(0, 1.0, 0), (129, 1.0, 14), (7, 1.0, 2), (7, -1.0, 3)]:
+        with pytest.raises(ar.ArError):
+            ar.ar_model_time(args[0], args[1], args[2], ALPHA, BETA, GAMMA)
+    with pytest.raises(ar.ArError):
+        ar.ar_model_time(7, 1.0, 3, -1.0, BETA, GAMMA)
+    k, r = ar.ar_model_best_k(2, 425.0, ALPHA, BETA, GAMMA)
+    assert k == 1 and math.isnan(r)
