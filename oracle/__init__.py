@@ -26,6 +26,8 @@ _SRC = os.path.join(_HERE, "oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
 I32_SUM, I32_MAX, F32_SUM, F32_MAX, TERM = 0, 1, 2, 3, 4
+GROUP_CYCLIC, GROUP_XOR = 0, 1
+SCHED_BUTTERFLY, SCHED_RING = 0, 1
 MAX_STEPS = 16
 MAXP = 128
 
@@ -76,6 +78,10 @@ def _configure(L):
     L.oracle_allreduce.argtypes = [i32, i64, i32, i32, vp, i64, vp, i64, vp, i64, vp, vp]
     L.oracle_allreduce_batched.restype = ctypes.c_int
     L.oracle_allreduce_batched.argtypes = [i32, i64, i32, i32, vp, vp, i64]
+    L.oracle_allreduce_ex.restype = ctypes.c_int
+    L.oracle_allreduce_ex.argtypes = [i32, i64, i32, i32, i32, i32, vp, i64, vp, i64, vp, i64, vp, vp]
+    L.oracle_allreduce_batched_ex.restype = ctypes.c_int
+    L.oracle_allreduce_batched_ex.argtypes = [i32, i64, i32, i32, i32, i32, vp, vp, i64]
     L.oracle_direct_sum_f64.restype = ctypes.c_int
     L.oracle_direct_sum_f64.argtypes = [i32, i64, vp, i64, vp]
     L.oracle_direct_i32.restype = ctypes.c_int
@@ -117,15 +123,26 @@ def _ptr(a: np.ndarray) -> int:
     return a.ctypes.data
 
 
+def _codes(group, schedule):
+    g = {"cyclic": GROUP_CYCLIC, "xor": GROUP_XOR, GROUP_CYCLIC: GROUP_CYCLIC, GROUP_XOR: GROUP_XOR}[group]
+    s = {"butterfly": SCHED_BUTTERFLY, "ring": SCHED_RING,
+         SCHED_BUTTERFLY: SCHED_BUTTERFLY, SCHED_RING: SCHED_RING}[schedule]
+    return g, s
+
+
 def allreduce(x: np.ndarray, k: int, op: str = "sum", n: int | None = None,
-              cols: np.ndarray | None = None, trace: bool = False, lib_=None):
+              cols: np.ndarray | None = None, trace: bool = False, lib_=None,
+              group="cyclic", schedule="butterfly"):
     """Replay the schedule.  ``x`` is [P, ncols] (int32 or float32).
 
     ``cols`` (optional) gives the global column index of each of the ncols
     columns (strictly increasing, in [0, n)); without it the columns are the
-    whole vector and n = ncols.  Returns the [P, ncols] results, and the trace
-    when ``trace`` is set.
+    whole vector and n = ncols.  ``group`` is "cyclic" or "xor" (power-of-two
+    P), ``schedule`` "butterfly" (k in [L, 2L]) or "ring" (cyclic group,
+    k = 2(P-1)).  Returns the [P, ncols] results, and the trace when
+    ``trace`` is set.
     """
+    g, sc = _codes(group, schedule)
     x = np.ascontiguousarray(x)
     P, ncols = x.shape
     kind = kind_of(x.dtype, op)
@@ -141,19 +158,20 @@ def allreduce(x: np.ndarray, k: int, op: str = "sum", n: int | None = None,
         cp = _ptr(cols)
     out = np.empty_like(x)
     tr = Trace() if trace else None
-    rc = (lib_ or lib()).oracle_allreduce(P, n, k, kind, _ptr(x), ncols, _ptr(out), ncols, cp, ncols,
-                                          None, ctypes.byref(tr) if tr is not None else None)
+    rc = (lib_ or lib()).oracle_allreduce_ex(P, n, k, kind, g, sc, _ptr(x), ncols, _ptr(out), ncols, cp, ncols,
+                                             None, ctypes.byref(tr) if tr is not None else None)
     if rc != 0:
-        raise ValueError("oracle_allreduce rejected P=%d n=%s k=%d" % (P, n, k))
+        raise ValueError("oracle_allreduce rejected P=%d n=%s k=%d group=%s schedule=%s" % (P, n, k, group, schedule))
     return (out, tr) if trace else out
 
 
-def allreduce_batched(x: np.ndarray, k: int, op: str = "sum") -> np.ndarray:
+def allreduce_batched(x: np.ndarray, k: int, op: str = "sum", group="cyclic", schedule="butterfly") -> np.ndarray:
     """Independent instances; ``x`` is [P, batch, n]."""
+    g, sc = _codes(group, schedule)
     x = np.ascontiguousarray(x)
     P, batch, n = x.shape
     out = np.empty_like(x)
-    rc = lib().oracle_allreduce_batched(P, n, k, kind_of(x.dtype, op), _ptr(x), _ptr(out), batch)
+    rc = lib().oracle_allreduce_batched_ex(P, n, k, kind_of(x.dtype, op), g, sc, _ptr(x), _ptr(out), batch)
     if rc != 0:
         raise ValueError("oracle_allreduce_batched rejected P=%d n=%d k=%d" % (P, n, k))
     return out
@@ -183,7 +201,8 @@ def direct(x: np.ndarray, op: str = "sum") -> np.ndarray:
 class Terms:
     """Symbolic replay: the reduction tree of every output value."""
 
-    def __init__(self, P: int, k: int, n: int | None = None, lib_=None):
+    def __init__(self, P: int, k: int, n: int | None = None, lib_=None, group="cyclic", schedule="butterfly"):
+        g, sc = _codes(group, schedule)
         self.P, self.k = P, k
         self.n = P if n is None else n
         self._lib = L = lib_ or lib()
@@ -193,8 +212,8 @@ class Terms:
         self.ids = np.empty((P, self.n), np.int32)
         self.trace = Trace()
         dummy = np.zeros((P, self.n), np.int32)
-        rc = L.oracle_allreduce(P, self.n, k, TERM, _ptr(dummy), self.n, _ptr(self.ids), self.n, None,
-                                self.n, self._h, ctypes.byref(self.trace))
+        rc = L.oracle_allreduce_ex(P, self.n, k, TERM, g, sc, _ptr(dummy), self.n, _ptr(self.ids), self.n, None,
+                                   self.n, self._h, ctypes.byref(self.trace))
         if rc != 0:
             L.oracle_terms_free(self._h)
             self._h = None

@@ -38,6 +38,19 @@
  *     Every shift is simulated as its own independent schedule.  Within a
  *     step all ranks send first (into per-rank receive buffers) and combine
  *     afterwards, i.e. the exchange is simultaneous (Sec. 5.3).
+ *     The same replay runs over the group of Sec. 4's Table 1b for
+ *     power-of-two P -- t_k(x) = x XOR k, every element self-inverse -- in
+ *     which the bandwidth-optimal schedule is Recursive Halving and the
+ *     latency-optimal one Recursive Doubling (Secs. 7 and 8, closing
+ *     remarks).  Group arithmetic is written through grp_mul / grp_inv:
+ *     placement of vector v of shift s is s.v, rank x holds block x.p^-1 of
+ *     placement p, a reduction step with operator t_f^-1 brings rank x the
+ *     vectors of rank x.f, and vector v lands as f^-1.v.
+ *  2b. oracle_allreduce_ex with the Ring schedule of Sec. 6: over the cyclic
+ *     group with the operator t at every step, P - 1 reduction steps (rank
+ *     x receives the partial sum of rank x - 1, placement i, and combines it
+ *     with its own placement i + 1) and P - 1 distribution steps with the
+ *     same operator.
  *  3. A symbolic "term" mode of the same replay: values are nodes of a
  *     hash-consed expression DAG, so the reduction tree of every output can
  *     be printed and compared with the paper's worked P = 7 example, every
@@ -69,6 +82,8 @@
 #define ORC_MAX_STEPS 16
 
 enum { ORC_I32_SUM = 0, ORC_I32_MAX = 1, ORC_F32_SUM = 2, ORC_F32_MAX = 3, ORC_TERM = 4 };
+enum { ORC_GROUP_CYCLIC = 0, ORC_GROUP_XOR = 1 };
+enum { ORC_SCHED_BUTTERFLY = 0, ORC_SCHED_RING = 1 };
 
 /* ------------------------------------------------------------------------ */
 /* Term DAG (symbolic mode)                                                  */
@@ -266,6 +281,17 @@ static int32_t mod_p(int64_t a, int32_t P) {
   return (int32_t)(v < 0 ? v + P : v);
 }
 
+/* Product and inverse in the group T_P acting on {0..P-1}: the cyclic group
+ * (t_a t_b = t_{a+b mod P}) or the group of Table 1b (t_a t_b = t_{a XOR b},
+ * P a power of two). */
+static int32_t grp_mul(int32_t g, int32_t a, int32_t b, int32_t P) {
+  return g == ORC_GROUP_XOR ? (a ^ b) : mod_p((int64_t)a + b, P);
+}
+
+static int32_t grp_inv(int32_t g, int32_t a, int32_t P) {
+  return g == ORC_GROUP_XOR ? a : mod_p(-(int64_t)a, P);
+}
+
 /* ------------------------------------------------------------------------ */
 /* Elementwise combination of two co-placed blocks (Sec. 5.4)                */
 /* ------------------------------------------------------------------------ */
@@ -319,7 +345,8 @@ static int combine_block(int32_t kind, orc_terms* terms, void* dst, const void* 
 typedef struct {
   int32_t P, L, k, r, w;
   int32_t rs_steps, ag_steps;
-  int32_t step_peer[ORC_MAX_STEPS];   /* receive from rank x + step_peer    */
+  int32_t step_peer[ORC_MAX_STEPS];   /* receive from rank x.step_peer (group
+                                         product; -1: from rank x - 1, Ring) */
   int32_t pulls[ORC_MAX_STEPS];       /* distinct vectors received, rank 0  */
   int32_t combines[ORC_MAX_STEPS];    /* distinct combine results, rank 0   */
   /* per step and rank: bitmask of the blocks received in that step */
@@ -366,11 +393,23 @@ static int idset_add(idset_t* s, int32_t id) {
  *   trace: optional; filled with the step sizes.
  * Returns 0, or -1 for bad arguments / allocation failure.
  */
-int oracle_allreduce(int32_t P, int64_t n, int32_t k, int32_t kind,
-                     const void* in, int64_t in_rank_stride,
-                     void* out, int64_t out_rank_stride,
-                     const int64_t* cols, int64_t ncols,
-                     orc_terms* terms, oracle_trace* trace) {
+static int ring_replay(int32_t P, int64_t n, int32_t k, int32_t kind, const void* in, int64_t in_rank_stride,
+                       void* out, int64_t out_rank_stride, const int64_t* cols, int64_t ncols, orc_terms* terms,
+                       oracle_trace* trace);
+
+int oracle_allreduce_ex(int32_t P, int64_t n, int32_t k, int32_t kind, int32_t group, int32_t schedule,
+                        const void* in, int64_t in_rank_stride,
+                        void* out, int64_t out_rank_stride,
+                        const int64_t* cols, int64_t ncols,
+                        orc_terms* terms, oracle_trace* trace) {
+  if (group != ORC_GROUP_CYCLIC && group != ORC_GROUP_XOR) return -1;
+  if (group == ORC_GROUP_XOR && (P & (P - 1)) != 0) return -1;   /* needs a power of two */
+  if (schedule == ORC_SCHED_RING) {
+    if (group != ORC_GROUP_CYCLIC) return -1;
+    return ring_replay(P, n, k, kind, in, in_rank_stride, out, out_rank_stride, cols, ncols, terms, trace);
+  }
+  if (schedule != ORC_SCHED_BUTTERFLY) return -1;
+  const int32_t g = group;
   sched_t s;
   if (sched_init(&s, P, k)) return -1;
   if (n < 0 || ncols < 0 || (!cols && ncols != n)) return -1;
@@ -427,13 +466,13 @@ int oracle_allreduce(int32_t P, int64_t n, int32_t k, int32_t kind,
     for (int32_t i = 0; i < s.L && rc == 0; ++i) {
       const int32_t f = s.f[i], c = s.c[i], N = s.N[i];
       if (trace) trace->step_peer[i] = f;
-      /* Send: rank y sends its blocks of vectors v in [c, N) of this shift
-       * to rank y - f; rank x therefore receives from x + f the block of
-       * vector v, which on rank x + f is block (x + f) - (sh + v). */
+      /* Send: with operator t_f^-1 rank y sends its blocks of vectors v in
+       * [c, N) of this shift to rank f^-1.y; rank x therefore receives from
+       * x.f the block of vector v, which on x.f is block (x.f).(sh.v)^-1. */
       for (int32_t x = 0; x < P; ++x) {
-        int32_t y = mod_p(x + f, P);
+        int32_t y = grp_mul(g, x, f, P);
         for (int32_t v = c; v < N; ++v) {
-          int32_t b = mod_p((int64_t)y - sh - v, P);
+          int32_t b = grp_mul(g, y, grp_inv(g, grp_mul(g, sh, v, P), P), P);
           for (int64_t j = gs[b]; j < gs[b + 1]; ++j) memcpy(CELL(M, x, j), CELL(W, y, j), ES);
           if (trace) mark_block(trace, i, x, b);
           if (trace && x == 0 && kind == ORC_TERM && gs[b + 1] > gs[b]) {
@@ -442,11 +481,13 @@ int oracle_allreduce(int32_t P, int64_t n, int32_t k, int32_t kind,
           }
         }
       }
-      /* Combine: the received vector v now sits at v - f, co-placed with the
-       * kept vector v - f; own value first, received second. */
+      /* Combine: the received vector v now sits where vector f^-1.v of the
+       * shift is kept (v - f, or v XOR f), co-placed with it; own value
+       * first, received second. */
       for (int32_t x = 0; x < P && rc == 0; ++x) {
         for (int32_t v = c; v < N; ++v) {
-          int32_t b = mod_p((int64_t)x - sh - (v - f), P);
+          int32_t kept = grp_mul(g, grp_inv(g, f, P), v, P);
+          int32_t b = grp_mul(g, x, grp_inv(g, grp_mul(g, sh, kept, P), P), P);
           int64_t j0 = gs[b], len = gs[b + 1] - gs[b];
           if (len == 0) continue;
           if (combine_block(kind, terms, CELL(W, x, j0), CELL(W, x, j0), CELL(M, x, j0), len)) { rc = -1; break; }
@@ -458,9 +499,9 @@ int oracle_allreduce(int32_t P, int64_t n, int32_t k, int32_t kind,
       }
     }
     /* After the last step vector 0 of this shift (placement sh) holds the
-     * complete result of block x - sh on every rank x. */
+     * complete result of block x.sh^-1 on every rank x. */
     for (int32_t x = 0; x < P; ++x) {
-      int32_t b = mod_p((int64_t)x - sh, P);
+      int32_t b = grp_mul(g, x, grp_inv(g, sh, P), P);
       for (int64_t j = gs[b]; j < gs[b + 1]; ++j) memcpy(CELL(F, x, j), CELL(W, x, j), ES);
     }
   }
@@ -473,19 +514,19 @@ int oracle_allreduce(int32_t P, int64_t n, int32_t k, int32_t kind,
     const int32_t f = s.f[i];
     const int32_t lo = s.c[i] > h ? s.c[i] : h;
     if (trace) trace->step_peer[step] = -f;
-    /* Operator t^{+f}: placement p - f of rank x - f moves to placement p of
+    /* Operator t_f: placement f^-1.p of rank x.f^-1 moves to placement p of
      * rank x (same block).  Receive everything first, then store. */
     for (int32_t x = 0; x < P; ++x) {
-      int32_t y = mod_p((int64_t)x - f, P);
+      int32_t y = grp_mul(g, x, grp_inv(g, f, P), P);
       for (int32_t p = lo; p < s.N[i]; ++p) {
-        int32_t b = mod_p((int64_t)x - p, P);
+        int32_t b = grp_mul(g, x, grp_inv(g, p, P), P);
         for (int64_t j = gs[b]; j < gs[b + 1]; ++j) memcpy(CELL(M, x, j), CELL(F, y, j), ES);
         if (trace) mark_block(trace, step, x, b);
       }
     }
     for (int32_t x = 0; x < P; ++x)
       for (int32_t p = lo; p < s.N[i]; ++p) {
-        int32_t b = mod_p((int64_t)x - p, P);
+        int32_t b = grp_mul(g, x, grp_inv(g, p, P), P);
         for (int64_t j = gs[b]; j < gs[b + 1]; ++j) memcpy(CELL(F, x, j), CELL(M, x, j), ES);
       }
     if (trace) trace->pulls[step] = s.N[i] - lo;
@@ -511,19 +552,123 @@ int oracle_allreduce(int32_t P, int64_t n, int32_t k, int32_t kind,
   return rc;
 }
 
+/* The cyclic group and the butterfly schedules of Secs. 7-9. */
+int oracle_allreduce(int32_t P, int64_t n, int32_t k, int32_t kind,
+                     const void* in, int64_t in_rank_stride,
+                     void* out, int64_t out_rank_stride,
+                     const int64_t* cols, int64_t ncols,
+                     orc_terms* terms, oracle_trace* trace) {
+  return oracle_allreduce_ex(P, n, k, kind, ORC_GROUP_CYCLIC, ORC_SCHED_BUTTERFLY, in, in_rank_stride, out,
+                             out_rank_stride, cols, ncols, terms, trace);
+}
+
+/*
+ * Ring schedule of Sec. 6 (cyclic group, operator t every step), k = 2(P-1).
+ * Placement p of rank x is block x - p.  Reduction step i = 0..P-2: the
+ * partial sum at placement i of rank x - 1 moves to placement i + 1 of rank
+ * x and is combined with rank x's own vector there (own first).  After
+ * P - 1 steps placement P - 1 holds the full result of block x + 1; the
+ * distribution steps j = 0..P-2 move placement j - 1 (mod P) of rank x - 1
+ * to placement j of rank x.  Trace sizes are kept for at most
+ * ORC_MAX_STEPS steps.
+ */
+static int ring_replay(int32_t P, int64_t n, int32_t k, int32_t kind, const void* in, int64_t in_rank_stride,
+                       void* out, int64_t out_rank_stride, const int64_t* cols, int64_t ncols, orc_terms* terms,
+                       oracle_trace* trace) {
+  if (P < 1 || P > ORC_MAXP || k != 2 * (P - 1)) return -1;
+  if (n < 0 || ncols < 0 || (!cols && ncols != n)) return -1;
+  if (kind < 0 || kind > ORC_TERM) return -1;
+  if (kind == ORC_TERM && !terms) return -1;
+  if (kind == ORC_TERM && terms_reset(terms, P)) return -1;
+  for (int64_t j = 0; j < ncols; ++j) {
+    int64_t e = cols ? cols[j] : j;
+    if (e < 0 || e >= n || (j > 0 && cols && cols[j] <= cols[j - 1])) return -1;
+  }
+  int64_t gs[ORC_MAXP + 1];
+  {
+    int32_t b = 0;
+    gs[0] = 0;
+    for (int64_t j = 0; j < ncols; ++j) {
+      int32_t bj = blk_of(n, P, cols ? cols[j] : j);
+      while (b < bj) gs[++b] = j;
+    }
+    while (b < P) gs[++b] = ncols;
+  }
+  const int64_t ES = 4;
+  int64_t cells = (int64_t)P * ncols;
+  char* W = (char*)malloc((size_t)(cells ? cells : 1) * ES);
+  char* M = (char*)malloc((size_t)(cells ? cells : 1) * ES);
+  if (!W || !M) { free(W); free(M); return -1; }
+#define RCELL(buf, x, j) ((buf) + ((int64_t)(x) * ncols + (j)) * ES)
+  for (int32_t x = 0; x < P; ++x)
+    for (int64_t j = 0; j < ncols; ++j) {
+      if (kind == ORC_TERM) {
+        int32_t id = x * P + blk_of(n, P, cols ? cols[j] : j);
+        memcpy(RCELL(W, x, j), &id, 4);
+      } else {
+        memcpy(RCELL(W, x, j), (const char*)in + ((int64_t)x * in_rank_stride + j) * ES, ES);
+      }
+    }
+  if (trace) {
+    memset(trace, 0, sizeof(*trace));
+    trace->P = P; trace->k = k; trace->rs_steps = P - 1; trace->ag_steps = P - 1;
+    trace->L = ceil_log2_i(P);
+  }
+  int rc = 0;
+  for (int32_t step = 0; step < 2 * (P - 1) && rc == 0; ++step) {
+    const int reduce = step < P - 1;
+    const int32_t from_p = reduce ? step : mod_p((int64_t)step - P, P);
+    const int32_t to_p = mod_p((int64_t)from_p + 1, P);
+    /* receive: rank x gets rank x-1's placement from_p, block (x-1) - from_p */
+    for (int32_t x = 0; x < P; ++x) {
+      int32_t y = mod_p((int64_t)x - 1, P);
+      int32_t b = mod_p((int64_t)y - from_p, P);
+      for (int64_t j = gs[b]; j < gs[b + 1]; ++j) memcpy(RCELL(M, x, j), RCELL(W, y, j), ES);
+      if (trace && step < ORC_MAX_STEPS) mark_block(trace, step, x, b);
+    }
+    /* combine (reduction) or store (distribution) at placement to_p */
+    for (int32_t x = 0; x < P && rc == 0; ++x) {
+      int32_t b = mod_p((int64_t)x - to_p, P);
+      int64_t j0 = gs[b], len = gs[b + 1] - gs[b];
+      if (len == 0) continue;
+      if (reduce) {
+        if (combine_block(kind, terms, RCELL(W, x, j0), RCELL(W, x, j0), RCELL(M, x, j0), len)) rc = -1;
+      } else {
+        memcpy(RCELL(W, x, j0), RCELL(M, x, j0), (size_t)len * ES);
+      }
+    }
+    if (trace && step < ORC_MAX_STEPS) {
+      trace->step_peer[step] = -1;
+      trace->pulls[step] = 1;
+      trace->combines[step] = reduce ? 1 : 0;
+    }
+  }
+  for (int32_t x = 0; x < P; ++x)
+    for (int64_t j = 0; j < ncols; ++j)
+      memcpy((char*)out + ((int64_t)x * out_rank_stride + j) * ES, RCELL(W, x, j), ES);
+#undef RCELL
+  free(W); free(M);
+  return rc;
+}
+
 /*
  * Independent instances (one Allreduce per instance, each with its own
  * block partition of n).  Layout of in and out: rank-major [P][batch][n].
  */
-int oracle_allreduce_batched(int32_t P, int64_t n, int32_t k, int32_t kind,
-                             const void* in, void* out, int64_t batch) {
+int oracle_allreduce_batched_ex(int32_t P, int64_t n, int32_t k, int32_t kind, int32_t group, int32_t schedule,
+                                const void* in, void* out, int64_t batch) {
   if (kind == ORC_TERM || batch < 0) return -1;
   for (int64_t t = 0; t < batch; ++t) {
-    int rc = oracle_allreduce(P, n, k, kind, (const char*)in + t * n * 4, batch * n,
-                              (char*)out + t * n * 4, batch * n, NULL, n, NULL, NULL);
+    int rc = oracle_allreduce_ex(P, n, k, kind, group, schedule, (const char*)in + t * n * 4, batch * n,
+                                 (char*)out + t * n * 4, batch * n, NULL, n, NULL, NULL);
     if (rc) return rc;
   }
   return 0;
+}
+
+int oracle_allreduce_batched(int32_t P, int64_t n, int32_t k, int32_t kind,
+                             const void* in, void* out, int64_t batch) {
+  return oracle_allreduce_batched_ex(P, n, k, kind, ORC_GROUP_CYCLIC, ORC_SCHED_BUTTERFLY, in, out, batch);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -9,6 +9,7 @@ import numpy as np
 import pytest
 
 import oracle
+from test_oracle_groups import group_root, load_group_golden, relabel, textbook_hybrid_xor, textbook_ring
 from test_oracle_pins import golden_root, load_golden, render, rotate
 
 SRC = os.path.join(os.path.dirname(oracle.__file__), "oracle.c")
@@ -23,16 +24,26 @@ MUTANTS = [
      "for (e = 0; e < len; ++e) d[e] = b[e] > a[e] ? b[e] : a[e];\n      return 0;\n    }\n    case ORC_TERM",
      "for (e = 0; e < len; ++e) d[e] = b[e] >= a[e] ? b[e] : a[e];\n      return 0;\n    }\n    case ORC_TERM"),
     ("receive from x - f in the reduction phase",
-     "int32_t y = mod_p(x + f, P);", "int32_t y = mod_p(x - f, P);"),
+     "int32_t y = grp_mul(g, x, f, P);", "int32_t y = grp_mul(g, x, grp_inv(g, f, P), P);"),
     ("one vector of the sent set dropped",
-     "for (int32_t v = c; v < N; ++v) {\n          int32_t b = mod_p((int64_t)x - sh - (v - f), P);",
-     "for (int32_t v = c + 1; v < N; ++v) {\n          int32_t b = mod_p((int64_t)x - sh - (v - f), P);"),
+     "for (int32_t v = c; v < N; ++v) {\n          int32_t kept",
+     "for (int32_t v = c + 1; v < N; ++v) {\n          int32_t kept"),
     ("distribution refetches held placements",
      "const int32_t lo = s.c[i] > h ? s.c[i] : h;", "const int32_t lo = s.c[i];"),
     ("shift count off by one",
      "s->w = (1 << s->r) < P ? (1 << s->r) : P;", "s->w = (1 << s->r) < P ? (1 << s->r) + (s->r > 0) - (s->r > 1) * 0 : P;"),
     ("distribution pulls from x + f",
-     "int32_t y = mod_p((int64_t)x - f, P);", "int32_t y = mod_p((int64_t)x + f, P);"),
+     "int32_t y = grp_mul(g, x, grp_inv(g, f, P), P);", "int32_t y = grp_mul(g, x, f, P);"),
+    ("XOR inverse taken as the cyclic negation",
+     "return g == ORC_GROUP_XOR ? a : mod_p(-(int64_t)a, P);", "return mod_p(-(int64_t)a, P);"),
+    ("XOR product taken as addition",
+     "return g == ORC_GROUP_XOR ? (a ^ b) : mod_p((int64_t)a + b, P);", "return mod_p((int64_t)a + b, P);"),
+    ("ring receives from x + 1",
+     "int32_t y = mod_p((int64_t)x - 1, P);", "int32_t y = mod_p((int64_t)x + 1, P);"),
+    ("ring combines the wrong placement",
+     "int32_t b = mod_p((int64_t)x - to_p, P);", "int32_t b = mod_p((int64_t)x - from_p, P);"),
+    ("ring stops one distribution step early",
+     "step < 2 * (P - 1) && rc == 0", "step < 2 * (P - 1) - 1 && rc == 0"),
 ]
 
 
@@ -49,6 +60,24 @@ def battery(L, golden_dir):
                         raise AssertionError
     except Exception:
         fails.append("golden trees")
+    # other groups and schedules: hand-derived trees and textbook formulations
+    try:
+        for group, sched, P, k, rule, tree, offs in load_group_golden(golden_dir):
+            t = oracle.Terms(P, k, lib_=L, group=group, schedule=sched)
+            for x in range(P):
+                for b in range(P):
+                    if t.tree(x, b) != render(relabel(tree, group_root(group, P, rule, offs, x, b), group, P)):
+                        raise AssertionError
+        for P in (4, 8, 16):
+            L2 = max(0, (P - 1).bit_length())
+            for k in range(L2, 2 * L2 + 1):
+                t, want = oracle.Terms(P, k, lib_=L, group="xor"), textbook_hybrid_xor(P, k)
+                assert all(t.tree(x, b) == render(want[x][b]) for x in range(P) for b in range(P))
+        for P in (2, 5, 9):
+            t, want = oracle.Terms(P, 2 * (P - 1), lib_=L, schedule="ring"), textbook_ring(P)
+            assert all(t.tree(x, b) == render(want[x][b]) for x in range(P) for b in range(P))
+    except Exception:
+        fails.append("groups")
     # exactly-once coverage and cost equations
     try:
         for P in (5, 6, 12, 37):
