@@ -13,6 +13,11 @@
  *     (Sec. 7), of which the first r are omitted (Sec. 8; r = ceil(log2 P)
  *     is the latency-optimal version of Sec. 9).
  * k_steps = 2*ceil(log2 P) - r, anywhere in [ceil(log2 P), 2*ceil(log2 P)].
+ * ar_plan_create_ex adds the special cases the paper derives from the same
+ * construction: the butterfly schedules over the group of Table 1b
+ * (power-of-two P, t_k(x) = x XOR k), which are Recursive Halving (k = 2L,
+ * Sec. 7), Recursive Doubling (k = L, Sec. 9) and their hybrid, and the Ring
+ * (Sec. 6: cyclic group, operator t at every step, k = 2(P-1)).
  *
  * Conventions shared by all entry points:
  *   - Every function returns an ar_status; AR_OK is 0.  On failure nothing
@@ -61,16 +66,29 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *             k = 1), each pulling the peer's blocks out of HBM.
  *   FUSED:    one launch that runs every step of the schedule on element
  *             columns held in registers, reading each input and writing
- *             each output once: bandwidth-optimal plans for any P (the Sec. 7
- *             fold of a column, result handed to every rank), and
- *             latency-optimal plans with P <= 16 (Sec. 9, many independent
- *             small instances, Sec. 1's 425-byte average).
- *   AUTO:     FUSED where it applies, STEPWISE otherwise.
+ *             each output once, for every plan with P >= 2: the Sec. 7 fold
+ *             of a column (bandwidth-optimal), the primed and starred sums of
+ *             Secs. 8-9 (fewer steps), the halving and doubling levels of the
+ *             XOR group and the Ring's chain; latency-optimal cyclic plans
+ *             with P <= 16 take a kernel without block tiling (many
+ *             independent small instances, Sec. 1's 425-byte average).
+ *   AUTO:     FUSED where it applies (P >= 2), STEPWISE otherwise.
  * Both paths combine exactly the same operand pairs in the same order, so
  * their results are bit-identical. */
 typedef enum { AR_PATH_AUTO = 0, AR_PATH_STEPWISE = 1, AR_PATH_FUSED = 2 } ar_path;
 
 typedef struct ar_plan ar_plan; /* opaque; owned by the caller between create and destroy */
+
+/* The group T_P of Sec. 5: AR_GROUP_CYCLIC, t_k(x) = (x + k) mod P (any P);
+ * AR_GROUP_XOR, t_k(x) = x XOR k (Table 1b; P a power of two).  Placement p
+ * of rank x holds block (x - p) mod P, respectively block x XOR p. */
+typedef enum { AR_GROUP_CYCLIC = 0, AR_GROUP_XOR = 1 } ar_group;
+
+/* AR_SCHEDULE_BUTTERFLY: the reduction / distribution schedules of Secs.
+ * 7-9, k_steps in [L, 2L].  AR_SCHEDULE_RING: Sec. 6, cyclic group only,
+ * k_steps = 2(P-1) (P - 1 reduction and P - 1 distribution steps, one block
+ * per rank each). */
+typedef enum { AR_SCHEDULE_BUTTERFLY = 0, AR_SCHEDULE_RING = 1 } ar_schedule;
 
 /* Sizes of a plan (per Allreduce instance).  Block counts follow the paper's
  * cost equations (Secs. 7-9): a rank receives 2(P-1) blocks in the
@@ -89,14 +107,16 @@ typedef struct {
   int64_t hbm_bytes_stepwise;        /* algorithmic HBM bytes of the STEPWISE path       */
   int64_t hbm_bytes_fused;           /* 2 * P * n * e: read every input, write every output */
   int64_t workspace_bytes;           /* device scratch per instance, STEPWISE path       */
+  int32_t group, schedule;           /* ar_group and ar_schedule of the plan              */
 } ar_stats;
 
 /* One launch of the STEPWISE path: a list of placement ranges.  In a range,
  * every rank x works on placements p = p0 .. p0+count-1 (mod P); placement p
  * of rank x is block (x - p) mod P of its vector (Sec. 5.1 with h =
- * identity).  kind COPY: dst = src; REDUCE: dst = own (+) src; REDUCE2:
- * dst = own (+) src and dst2 = own2 (+) src.  own/dst buffers belong to rank
- * x, src to rank (x + delta) mod P; all at the same block.  Buffer ids: 0 is
+ * identity; x XOR p in the XOR group).  kind COPY: dst = src; REDUCE: dst =
+ * own (+) src; REDUCE2: dst = own (+) src and dst2 = own2 (+) src.  own/dst
+ * buffers belong to rank x, src to rank (x + delta) mod P (x XOR delta in the
+ * XOR group); all at the same block.  Buffer ids: 0 is
  * the caller's rank buffer, 1 and 2 the plan's two scratch buffers, -1 none. */
 typedef struct {
   int32_t phase;     /* 0 reduction, 1 distribution, 2 local copy */
@@ -119,6 +139,17 @@ enum { AR_KIND_COPY = 0, AR_KIND_REDUCE = 1, AR_KIND_REDUCE2 = 2 };
  * Errors: AR_ERR_INVALID_ARG (range), AR_ERR_UNSUPPORTED (dtype/op),
  * AR_ERR_INTERNAL (consistency check failed).  *out_plan is set on AR_OK. */
 ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_plan** out_plan);
+
+/* As ar_plan_create (which is group AR_GROUP_CYCLIC, schedule
+ * AR_SCHEDULE_BUTTERFLY), for any group and schedule above.  Both paths
+ * serve every plan; FUSED runs the whole schedule in one launch (Recursive
+ * Halving / hybrid / Doubling: halving levels with the kept operand picked
+ * per block, then doubling levels; Ring: the chain of Sec. 6), bit-identical
+ * to STEPWISE.  Errors as ar_plan_create, and AR_ERR_INVALID_ARG for an
+ * unknown group or schedule, AR_GROUP_XOR with P not a power of two, the
+ * Ring over AR_GROUP_XOR, or a Ring k_steps other than 2(P-1). */
+ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_group group,
+                            ar_schedule schedule, ar_plan** out_plan);
 
 /* Choose the execution path (default AR_PATH_AUTO).  AR_ERR_UNSUPPORTED if
  * FUSED is asked for and the plan cannot run fused. */

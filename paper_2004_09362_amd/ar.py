@@ -24,9 +24,11 @@ AR_INT32, AR_FLOAT32 = 0, 1
 AR_SUM, AR_MAX = 0, 1
 AR_PATH_AUTO, AR_PATH_STEPWISE, AR_PATH_FUSED = 0, 1, 2
 AR_KIND_COPY, AR_KIND_REDUCE, AR_KIND_REDUCE2 = 0, 1, 2
+AR_GROUP_CYCLIC, AR_GROUP_XOR = 0, 1
+AR_SCHEDULE_BUTTERFLY, AR_SCHEDULE_RING = 0, 1
 
 EXPORTS = [
-    "ar_plan_create", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
+    "ar_plan_create", "ar_plan_create_ex", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
     "ar_plan_num_launches", "ar_plan_launch", "ar_plan_destroy", "ar_status_string", "ar_last_error",
     "ar_model_time", "ar_model_best_k", "ar_plan_model_time",
 ]
@@ -49,6 +51,7 @@ class Stats(ctypes.Structure):
         ("bytes_pulled_total", ctypes.c_int64), ("combines_per_rank", ctypes.c_int64),
         ("hbm_bytes_stepwise", ctypes.c_int64), ("hbm_bytes_fused", ctypes.c_int64),
         ("workspace_bytes", ctypes.c_int64),
+        ("group", ctypes.c_int32), ("schedule", ctypes.c_int32),
     ]
 
     def as_dict(self):
@@ -73,6 +76,8 @@ def _load():
     L = ctypes.CDLL(LIB_PATH)
     vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     L.ar_plan_create.argtypes = [i32, i64, ctypes.c_int, ctypes.c_int, i32, ctypes.POINTER(vp)]
+    L.ar_plan_create_ex.argtypes = [i32, i64, ctypes.c_int, ctypes.c_int, i32, ctypes.c_int, ctypes.c_int,
+                                    ctypes.POINTER(vp)]
     L.ar_plan_set_path.argtypes = [vp, ctypes.c_int]
     L.ar_execute.argtypes = [vp, ctypes.POINTER(vp), vp]
     L.ar_execute_batched.argtypes = [vp, ctypes.POINTER(vp), i64, i64, vp]
@@ -89,7 +94,7 @@ def _load():
     L.ar_status_string.restype = ctypes.c_char_p
     L.ar_last_error.argtypes = []
     L.ar_last_error.restype = ctypes.c_char_p
-    for name in ("ar_plan_create", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
+    for name in ("ar_plan_create", "ar_plan_create_ex", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
                  "ar_plan_num_launches", "ar_plan_launch", "ar_model_time", "ar_model_best_k", "ar_plan_model_time"):
         getattr(L, name).restype = ctypes.c_int
     return L
@@ -130,6 +135,23 @@ def _op_code(op) -> int:
 def ar_plan_create(P: int, n: int, dtype, op, k_steps: int) -> int:
     h = ctypes.c_void_p()
     _check(lib.ar_plan_create(P, n, _dtype_code(dtype), _op_code(op), k_steps, ctypes.byref(h)), "ar_plan_create")
+    return h.value
+
+
+def _group_code(group) -> int:
+    return {"cyclic": AR_GROUP_CYCLIC, "xor": AR_GROUP_XOR, AR_GROUP_CYCLIC: AR_GROUP_CYCLIC,
+            AR_GROUP_XOR: AR_GROUP_XOR}[group]
+
+
+def _schedule_code(schedule) -> int:
+    return {"butterfly": AR_SCHEDULE_BUTTERFLY, "ring": AR_SCHEDULE_RING, AR_SCHEDULE_BUTTERFLY: AR_SCHEDULE_BUTTERFLY,
+            AR_SCHEDULE_RING: AR_SCHEDULE_RING}[schedule]
+
+
+def ar_plan_create_ex(P: int, n: int, dtype, op, k_steps: int, group="cyclic", schedule="butterfly") -> int:
+    h = ctypes.c_void_p()
+    _check(lib.ar_plan_create_ex(P, n, _dtype_code(dtype), _op_code(op), k_steps, _group_code(group),
+                                 _schedule_code(schedule), ctypes.byref(h)), "ar_plan_create_ex")
     return h.value
 
 
@@ -205,13 +227,16 @@ def ar_plan_destroy(plan: int):
 
 
 class Plan:
-    """Owning handle around ``ar_plan*``."""
+    """Owning handle around ``ar_plan*``.  ``k`` defaults to the
+    bandwidth-optimal 2 ceil(log2 P) (the Ring: 2(P-1))."""
 
-    def __init__(self, P: int, n: int, dtype, op="sum", k: int | None = None, path: int = AR_PATH_AUTO):
+    def __init__(self, P: int, n: int, dtype, op="sum", k: int | None = None, path: int = AR_PATH_AUTO,
+                 group="cyclic", schedule="butterfly"):
         L = max(0, (P - 1).bit_length())
         self.P, self.n = P, n
-        self.k = 2 * L if k is None else k
-        self.handle = ar_plan_create(P, n, dtype, op, self.k)
+        ring = _schedule_code(schedule) == AR_SCHEDULE_RING
+        self.k = (2 * (P - 1) if ring else 2 * L) if k is None else k
+        self.handle = ar_plan_create_ex(P, n, dtype, op, self.k, group, schedule)
         if path != AR_PATH_AUTO:
             ar_plan_set_path(self.handle, path)
 

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libar.so")
-SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip"] +
+SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip", "fused_group.hip"] +
            ["fused_col_g%d.hip" % i for i in range(8)]]
 HEADERS = [os.path.join(CSRC, f) for f in ("ar_internal.hpp", "device_common.hpp", "fused_col.hpp")] + [
     os.path.join(ROOT, "include", "ar.h")]

@@ -15,8 +15,29 @@ constexpr int kFusedMaxP = 16;   // largest P of the register-resident fused ker
 enum Buf : int32_t { kBufNone = -1, kBufU = 0, kBufX = 1, kBufY = 2 };
 enum Kind : int32_t { kCopy = 0, kReduce = 1, kReduce2 = 2 };
 enum Phase : int32_t { kPhaseReduce = 0, kPhaseDistribute = 1, kPhaseLocal = 2 };
+// The group T_P (Sec. 5): cyclic, t_k(x) = x + k mod P, or the group of
+// Table 1b for power-of-two P, t_k(x) = x XOR k.  Schedules: the butterfly
+// family of Secs. 7-9 (any k in [L, 2L]) or the Ring of Sec. 6.
+enum Group : int32_t { kGroupCyclic = 0, kGroupXor = 1 };
+enum Sched : int32_t { kSchedButterfly = 0, kSchedRing = 1 };
 
-// One range of placements worked on by every rank in a launch.
+// Block held at placement p by rank x (h = identity), and the rank a step
+// with "delta" pulls from: x - p and x + delta mod P in the cyclic group,
+// x XOR p and x XOR delta in the XOR group.
+inline int32_t group_block(int32_t group, int32_t x, int32_t p, int32_t P) {
+  if (group == kGroupXor) return x ^ p;
+  const int32_t b = (x - p) % P;
+  return b < 0 ? b + P : b;
+}
+inline int32_t group_peer(int32_t group, int32_t x, int32_t delta, int32_t P) {
+  if (group == kGroupXor) return x ^ delta;
+  const int32_t y = (x + delta) % P;
+  return y < 0 ? y + P : y;
+}
+
+// One range of placements worked on by every rank in a launch.  delta names
+// the peer (group_peer); the peer's copy of the same block is its placement
+// p + delta (cyclic) or p XOR delta (XOR group).
 struct Range {
   int32_t p0, count, kind, delta;
   int32_t dst, own, dst2, own2, src;
@@ -30,6 +51,7 @@ struct Launch {
 // The schedule and its sizes; built on the host (plan.cpp).
 struct Schedule {
   int32_t P = 1, L = 0, k = 0, r = 0, w = 1;
+  int32_t group = kGroupCyclic, sched = kSchedButterfly;
   int64_t n = 0;
   std::vector<int32_t> N, f, c;  // N_i, floor(N_i/2), ceil(N_i/2)
   std::vector<Launch> launches;
@@ -43,6 +65,7 @@ struct Schedule {
 
 // Builds the schedule; returns an empty string or the reason it failed.
 std::string build_schedule(int32_t P, int64_t n, int32_t k, Schedule* out);
+std::string build_schedule_ex(int32_t P, int64_t n, int32_t k, int32_t group, int32_t sched, Schedule* out);
 
 // Verifies that no launch of `s` lets one work item write a location that a
 // different work item reads or writes.  Returns "" or a description.
@@ -96,6 +119,7 @@ struct StepArgs {
   uint32_t total_tiles;     // P * total_ops * batch * tiles_per_seg (< 2^31)
   FastDiv tps, batch, ops;  // tiles per segment, instances, ops per rank
   int32_t P, n_ranges;
+  int32_t group;            // kGroupCyclic or kGroupXor
   DevRange ranges[kMaxRanges];
 };
 
@@ -129,6 +153,11 @@ int launch_fused_bo(const ColArgs& a, int dtype, int op, bool nt, int grid, void
 template <int P>
 int launch_fused_mid(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream);
 int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream);
+// Column-fused kernels of the other schedules (fused_group.hip): the XOR
+// group's Recursive Halving / hybrid / Recursive Doubling for P = 2..128 a
+// power of two and any r, and the Ring for any P in 2..128.
+int launch_fused_xor(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream);
+int launch_fused_ring(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream);
 // Workgroups of a step launch over `total_tiles` wave tiles, and the tile size.
 int step_grid(int64_t total_tiles);
 int64_t step_tile_elems();

@@ -24,9 +24,10 @@ constexpr int64_t kNtThresholdBytes = int64_t(512) << 20;
 constexpr int64_t kFusedNtThresholdBytes = int64_t(128) << 20;
 
 // Which single-launch kernel runs a plan on the FUSED path: the flat
-// latency-optimal kernel (small P; its columns need no block index) or the
-// block-tiled column kernels (every other plan).
-enum FusedKind { kFusedNone = 0, kFusedLo = 1, kFusedCol = 2 };
+// latency-optimal kernel (small P; its columns need no block index), the
+// block-tiled column kernels (every other cyclic butterfly plan), or the
+// column kernels of the XOR group and of the Ring.
+enum FusedKind { kFusedNone = 0, kFusedLo = 1, kFusedCol = 2, kFusedXor = 3, kFusedRing = 4 };
 
 struct ar_plan {
   ar::Schedule s;
@@ -119,6 +120,7 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   std::memset(&a, 0, sizeof a);
   for (int32_t x = 0; x < s.P; ++x) a.user[x] = bufs[x];
   a.P = s.P;
+  a.group = s.group;
   a.n = s.n;
   a.stride = stride;
   a.q = s.n / s.P;
@@ -189,6 +191,8 @@ ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
 }
 
 ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, hipStream_t stream) {
+  // one ColArgs layout for every column kernel; the XOR kernel reads the
+  // first P entries of the rank table, the others a rotation of it
   const ar::Schedule& s = pl->s;
   ar::ColArgs a;
   std::memset(&a, 0, sizeof a);
@@ -208,7 +212,11 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   a.tiles = ar::make_fastdiv(uint32_t(tiles));
   a.pdiv = ar::make_fastdiv(uint32_t(s.P));
   const bool nt = use_nt(pl->fused_nt_mode, int64_t(2) * s.P * s.n * batch * 4, kFusedNtThresholdBytes);
-  const int e = ar::launch_fused_col_any(a, s.P, pl->dtype, pl->op, nt, ar::step_grid(total), stream);
+  const int grid = ar::step_grid(total);
+  int e;
+  if (pl->fused_kind == kFusedXor) e = ar::launch_fused_xor(a, s.P, pl->dtype, pl->op, nt, grid, stream);
+  else if (pl->fused_kind == kFusedRing) e = ar::launch_fused_ring(a, pl->dtype, pl->op, nt, grid, stream);
+  else e = ar::launch_fused_col_any(a, s.P, pl->dtype, pl->op, nt, grid, stream);
   if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");
   return AR_OK;
 }
@@ -217,14 +225,18 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
 
 extern "C" {
 
-ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_plan** out_plan) {
+ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_group group,
+                            ar_schedule schedule, ar_plan** out_plan) {
   if (!out_plan) return fail(AR_ERR_INVALID_ARG, "out_plan is NULL");
   *out_plan = nullptr;
   if (int(dtype) != AR_INT32 && int(dtype) != AR_FLOAT32) return fail(AR_ERR_UNSUPPORTED, "dtype must be int32 or float32");
   if (int(op) != AR_SUM && int(op) != AR_MAX) return fail(AR_ERR_UNSUPPORTED, "op must be sum or max");
+  if (int(group) != AR_GROUP_CYCLIC && int(group) != AR_GROUP_XOR) return fail(AR_ERR_INVALID_ARG, "unknown group");
+  if (int(schedule) != AR_SCHEDULE_BUTTERFLY && int(schedule) != AR_SCHEDULE_RING)
+    return fail(AR_ERR_INVALID_ARG, "unknown schedule");
   ar_plan* pl = new (std::nothrow) ar_plan;
   if (!pl) return fail(AR_ERR_OUT_OF_MEMORY, "plan allocation");
-  const std::string err = ar::build_schedule(P, n, k_steps, &pl->s);
+  const std::string err = ar::build_schedule_ex(P, n, k_steps, int32_t(group), int32_t(schedule), &pl->s);
   if (!err.empty()) {
     delete pl;
     return fail(err.rfind("internal", 0) == 0 ? AR_ERR_INTERNAL : AR_ERR_INVALID_ARG, err);
@@ -238,12 +250,19 @@ ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t
   pl->nt_mode = env_mode("AR_STEP_NT");
   pl->fused_nt_mode = env_mode("AR_FUSED_NT");
   pl->fused_mode = env_mode("AR_FUSED_MODE");
-  if (pl->s.P >= 2 && pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L) pl->fused_kind = kFusedLo;
-  else if (pl->s.P >= 2) pl->fused_kind = kFusedCol;
+  if (pl->s.P < 2) pl->fused_kind = kFusedNone;
+  else if (pl->s.sched == ar::kSchedRing) pl->fused_kind = kFusedRing;
+  else if (pl->s.group == ar::kGroupXor) pl->fused_kind = kFusedXor;
+  else if (pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L) pl->fused_kind = kFusedLo;
+  else pl->fused_kind = kFusedCol;
   pl->fused_ok = pl->fused_kind != kFusedNone;
   *out_plan = pl;
   g_err.clear();
   return AR_OK;
+}
+
+ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_plan** out_plan) {
+  return ar_plan_create_ex(P, n, dtype, op, k_steps, AR_GROUP_CYCLIC, AR_SCHEDULE_BUTTERFLY, out_plan);
 }
 
 ar_status ar_plan_set_path(ar_plan* plan, ar_path path) {
@@ -277,7 +296,7 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
   const int64_t elems = int64_t(plan->s.P) * plan->s.n * batch;
   if (elems / batch / plan->s.P != plan->s.n) return fail(AR_ERR_INVALID_ARG, "size overflow");
   const bool fused = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok);
-  if (fused && plan->fused_kind == kFusedCol) {
+  if (fused && plan->fused_kind != kFusedLo) {
     st = run_fused_col(plan, rank_buffers, batch, instance_stride, stream);
   } else if (fused) {
     st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream);
@@ -325,7 +344,7 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
           char& sn = seen[size_t(rg.src) * s.P + p];
           if (sn) continue;
           sn = 1;
-          const int32_t b = ((x - p) % s.P + s.P) % s.P;
+          const int32_t b = ar::group_block(s.group, x, p, s.P);
           bytes += ar::block_len(s.n, s.P, b) * 4;
         }
       }
@@ -341,6 +360,8 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
   out->hbm_bytes_stepwise = s.hbm_blocks * s.n * 4;
   out->hbm_bytes_fused = s.P > 1 ? int64_t(2) * s.P * s.n * 4 : 0;
   out->workspace_bytes = s.uses_scratch ? int64_t(2) * s.P * round_up(s.n, 64) * 4 : 0;
+  out->group = s.group;
+  out->schedule = s.sched;
   return AR_OK;
 }
 

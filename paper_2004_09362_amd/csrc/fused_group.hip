@@ -1,0 +1,212 @@
+// fused_group.hip -- column-fused kernels of the schedules the paper derives
+// as special cases of its algorithm (Kolmakov & Zhang, "A Generalization of
+// the Allreduce Operation", arXiv:2004.09362):
+//
+// fused_xor_kernel: the butterfly schedules over the group of Table 1b
+// (power-of-two P, t_k(x) = x XOR k) -- Recursive Halving for k = 2L
+// (Sec. 7, closing remark), Recursive Doubling for k = L (Sec. 9, closing
+// remark) and the hybrid between them (Sec. 8).  Placement p of rank x holds
+// block x XOR p and step i (f_i = P / 2^(i+1)) pulls from rank x XOR f_i.
+// For block b the reduction of one element column, written by rank rather
+// than by placement, is: while f >= w = 2^r, every pair of slots {y, y|f}
+// (bit f of y clear) combines into slot y, the kept operand being the rank
+// whose bit f agrees with b's (it holds the block's placement in [0, f));
+// after these halving levels slot y < w holds the partial sum rooted at the
+// rank of b's w-group whose low bits are y.  While f < w every slot y < w
+// combines with slot y XOR f, own value first (the doubling levels).  Rank
+// x's result is the one rooted at the rank of b's w-group with x's low
+// bits: slot x mod w.  The pairs and operand order are exactly those of the
+// step-by-step schedule, so the bits are identical.  Because the slots are
+// ranks, every block uses the same pointer table and all indices are
+// compile-time constants; only the operand order of a halving level depends
+// on b, through a wave-uniform select.
+//
+// fused_ring_kernel: the Ring (Sec. 6).  For block b, reduction step i
+// combines rank b+i+1's own value with the partial sum of ranks b..b+i
+// received from rank b+i, so one column is the chain
+// acc = V_{b+d} (+) acc, d = 1 .. P-1, starting from V_b, and the P - 1
+// distribution steps hand acc to every rank.
+//
+// Both read every input once and write every output once (2 * P * n
+// elements), one 4-byte element per lane, 64 consecutive columns of one
+// block per wave, tiles laid on 256-byte boundaries of the block's root rank
+// buffer -- the layout of the cyclic column kernels (fused_col.hpp).
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "ar_internal.hpp"
+#include "device_common.hpp"
+
+namespace ar {
+
+namespace {
+
+// Halving levels f = F, F/2, ..., W: slot y (< f) keeps the pair {y, y|f}.
+template <int P, int W, int F, int OP, typename T>
+__device__ __forceinline__ void xor_halving(T (&X)[P], uint32_t b) {
+  if constexpr (F >= W && F >= 1) {
+    const bool upper = (b & uint32_t(F)) != 0;  // wave-uniform
+#pragma unroll
+    for (int y = 0; y < F; ++y) {
+      const T lo = X[y], hi = X[y + F];
+      const T own = upper ? hi : lo;
+      const T recv = upper ? lo : hi;
+      X[y] = comb<OP>(own, recv);
+    }
+    xor_halving<P, W, F / 2, OP, T>(X, b);
+  }
+}
+
+// Doubling levels f = F, F/2, ..., 1 over the W held slots.
+template <int P, int W, int F, int OP, typename T>
+__device__ __forceinline__ void xor_doubling(T (&X)[P]) {
+  if constexpr (F >= 1) {
+#pragma unroll
+    for (int y = 0; y < W; ++y) {
+      if ((y & F) == 0) {
+        const T u = X[y], v = X[y | F];
+        X[y] = comb<OP>(u, v);
+        X[y | F] = comb<OP>(v, u);
+      }
+    }
+    xor_doubling<P, W, F / 2, OP, T>(X);
+  }
+}
+
+template <int P, int R, typename T, int OP, bool NT>
+__global__ __launch_bounds__(kBlock) void fused_xor_kernel(const ColArgs a) {
+  constexpr int W = 1 << R;
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
+       t += gridDim.x * uint32_t(kWavesPerBlock)) {
+    const uint32_t seg = fdiv(t, a.tiles);  // seg = instance * P + block
+    const uint32_t tile = t - seg * a.tiles.d;
+    const uint32_t inst = fdiv(seg, a.pdiv);
+    const int32_t b = int32_t(seg - inst * a.pdiv.d);
+    const int64_t len = a.q + (b < a.m ? 1 : 0);
+    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+    const int64_t lo = ((reinterpret_cast<uintptr_t>(a.user[b]) >> 2) + e0) & (kWave - 1);
+    const int64_t c = int64_t(tile) * kWave - lo + lane;
+    if (c >= 0 && c < len) {
+      const int64_t e = e0 + c;
+      T X[P];
+#pragma unroll
+      for (int y = 0; y < P; ++y) X[y] = ld1<NT>(static_cast<const T*>(a.user[y]) + e);
+      xor_halving<P, W, P / 2, OP, T>(X, uint32_t(b));
+      xor_doubling<P, W, W / 2, OP, T>(X);
+#pragma unroll
+      for (int x = 0; x < P; ++x) st1<NT>(static_cast<T*>(a.user[x]) + e, X[x & (W - 1)]);
+    }
+  }
+}
+
+constexpr int kRingChunk = 16;  // loads in flight per lane along the chain
+
+template <typename T, int OP, bool NT>
+__global__ __launch_bounds__(kBlock) void fused_ring_kernel(const ColArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int32_t P = a.P;
+  for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
+       t += gridDim.x * uint32_t(kWavesPerBlock)) {
+    const uint32_t seg = fdiv(t, a.tiles);
+    const uint32_t tile = t - seg * a.tiles.d;
+    const uint32_t inst = fdiv(seg, a.pdiv);
+    const int32_t b = int32_t(seg - inst * a.pdiv.d);
+    const int64_t len = a.q + (b < a.m ? 1 : 0);
+    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+    void* const* rot = a.user + b;  // rot[d] is rank (b + d) mod P
+    const int64_t lo = ((reinterpret_cast<uintptr_t>(rot[0]) >> 2) + e0) & (kWave - 1);
+    const int64_t c = int64_t(tile) * kWave - lo + lane;
+    if (c >= 0 && c < len) {
+      const int64_t e = e0 + c;
+      T acc = ld1<NT>(static_cast<const T*>(rot[0]) + e);
+      for (int32_t d0 = 1; d0 < P; d0 += kRingChunk) {
+        T v[kRingChunk];
+#pragma unroll
+        for (int u = 0; u < kRingChunk; ++u)
+          if (d0 + u < P) v[u] = ld1<NT>(static_cast<const T*>(rot[d0 + u]) + e);
+#pragma unroll
+        for (int u = 0; u < kRingChunk; ++u)
+          if (d0 + u < P) acc = comb<OP>(v[u], acc);
+      }
+      for (int32_t d = 0; d < P; ++d) st1<NT>(static_cast<T*>(rot[d]) + e, acc);
+    }
+  }
+}
+
+template <int P, int R>
+int launch_xor_pr(const ColArgs& a, int dtype, int op, bool nt, int grid, hipStream_t s) {
+  const dim3 g(grid), blk(kBlock);
+  if (dtype == 0) {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 1, false>), g, blk, 0, s, a);
+    }
+  } else {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 1, false>), g, blk, 0, s, a);
+    }
+  }
+  return int(hipGetLastError());
+}
+
+template <int P, int R>
+int launch_xor_r(const ColArgs& a, int dtype, int op, bool nt, int grid, hipStream_t s) {
+  if constexpr ((1 << R) <= P) {
+    if (a.r == R) return launch_xor_pr<P, R>(a, dtype, op, nt, grid, s);
+    return launch_xor_r<P, R + 1>(a, dtype, op, nt, grid, s);
+  } else {
+    return int(hipErrorInvalidValue);
+  }
+}
+
+}  // namespace
+
+int launch_fused_xor(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  switch (P) {
+    case 2: return launch_xor_r<2, 0>(a, dtype, op, nt, grid, s);
+    case 4: return launch_xor_r<4, 0>(a, dtype, op, nt, grid, s);
+    case 8: return launch_xor_r<8, 0>(a, dtype, op, nt, grid, s);
+    case 16: return launch_xor_r<16, 0>(a, dtype, op, nt, grid, s);
+    case 32: return launch_xor_r<32, 0>(a, dtype, op, nt, grid, s);
+    case 64: return launch_xor_r<64, 0>(a, dtype, op, nt, grid, s);
+    case 128: return launch_xor_r<128, 0>(a, dtype, op, nt, grid, s);
+    default: return int(hipErrorInvalidValue);
+  }
+}
+
+int launch_fused_ring(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const dim3 g(grid), blk(kBlock);
+  if (dtype == 0) {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<int32_t, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<int32_t, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<int32_t, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<int32_t, 1, false>), g, blk, 0, s, a);
+    }
+  } else {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<float, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<float, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<float, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<float, 1, false>), g, blk, 0, s, a);
+    }
+  }
+  return int(hipGetLastError());
+}
+
+}  // namespace ar

@@ -3,10 +3,11 @@
 // Kolmakov & Zhang, "A Generalization of the Allreduce Operation"
 // (arXiv:2004.09362).  Two kernels:
 //
-//  step_kernel   one communication step of the schedule (Secs. 7-9): every
+//  step_kernel   one communication step of the schedule (Secs. 6-9): every
 //                rank x, for each of its placements p in the launch's ranges,
 //                combines (or copies) block b = (x - p) mod P of its own
-//                buffer with the same block of rank (x + delta) mod P.  The
+//                buffer with the same block of rank (x + delta) mod P (in the
+//                XOR group: block x XOR p, rank x XOR delta).  The
 //                work is pure streaming -- three (copy: two, dual: five)
 //                block-sized HBM accesses per item, one add per element --
 //                so the kernel is built for HBM bandwidth: 64-lane waves,
@@ -143,11 +144,17 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
     const DevRange& R = a.ranges[ri];
     int32_t p = R.p0 + (j - R.first);  // < 2P
     if (p >= P) p -= P;
-    int32_t b = x - p;
-    if (b < 0) b += P;
-    int32_t y = x + R.delta;            // |delta| < P
-    if (y >= P) y -= P;
-    if (y < 0) y += P;
+    int32_t b, y;
+    if (a.group == kGroupXor) {         // t_k(x) = x XOR k: block x XOR p, peer x XOR delta
+      b = x ^ p;
+      y = x ^ R.delta;
+    } else {                            // cyclic: block x - p, peer x + delta (|delta| < P)
+      b = x - p;
+      if (b < 0) b += P;
+      y = x + R.delta;
+      if (y >= P) y -= P;
+      if (y < 0) y += P;
+    }
     const int64_t len = a.q + (b < a.m ? 1 : 0);
     const int64_t off = int64_t(b) * a.q + (b < a.m ? b : a.m);
     const int64_t e0 = int64_t(inst) * a.stride + off;

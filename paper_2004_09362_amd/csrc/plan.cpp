@@ -27,6 +27,24 @@
 // Distribution phase (Sec. 7, reversed steps without combination): with
 // placements [0, h) held, the reversed step i fetches [max(c_i, h), N_i)
 // from rank x - f_i, only when N_i > h; exactly L - r steps remain.
+//
+// Group of Table 1b (power-of-two P, t_k(x) = x XOR k; every element is its
+// own inverse).  Placement p of rank x holds block x XOR p, and a step with
+// operator t_f pulls from rank x XOR f.  N_i = P / 2^i, f_i = c_i = N_i / 2.
+// The shifts s < w form a subgroup, so shifting the schedule by s only
+// permutes its vectors: while f_i >= w the w shifted schedules are one and
+// the same, and step i combines placements [0, f_i) with the received
+// [f_i, 2 f_i) in place (Recursive Halving, Sec. 7); once f_i < w every one
+// of the w held placements combines with its partner's (Recursive
+// Doubling, Sec. 9), ping-ponging through scratch since peers read what is
+// rewritten.  The last of those steps writes the caller's buffers.  The
+// distribution fetches [f_i, 2 f_i) from rank x XOR f_i for the L - r steps
+// with 2 f_i > w.
+//
+// Ring (Sec. 6, cyclic group): P - 1 reduction steps, each combining
+// placement i + 1 with placement i of rank x - 1 (one block, in place), then
+// P - 1 distribution steps copying placement j - 1 of rank x - 1 to
+// placement j.
 #include <algorithm>
 #include <cstdio>
 #include <set>
@@ -91,20 +109,101 @@ void emit_launch(std::vector<Launch>* out, int32_t phase, const std::vector<std:
 
 }  // namespace
 
+// Ring of Sec. 6: 2(P - 1) single-placement launches, all in place.
+static void ring_launches(Schedule* s) {
+  const int32_t P = s->P;
+  for (int32_t i = 0; i + 1 < P; ++i) {
+    std::vector<std::vector<POp>> per_p(P);
+    per_p[i + 1].push_back(POp{kReduce, -1, kBufU, kBufU, kBufNone, kBufNone, kBufU});
+    emit_launch(&s->launches, kPhaseReduce, per_p);
+  }
+  for (int32_t j = 0; j + 1 < P; ++j) {
+    std::vector<std::vector<POp>> per_p(P);
+    per_p[j].push_back(POp{kCopy, -1, kBufU, kBufNone, kBufNone, kBufNone, kBufU});
+    emit_launch(&s->launches, kPhaseDistribute, per_p);
+  }
+  s->rs_steps = P - 1;
+  s->ag_steps = P - 1;
+}
+
+// Butterfly schedules over the XOR group (power-of-two P).
+static void xor_launches(Schedule* s) {
+  const int32_t P = s->P, L = s->L, r = s->r, w = s->w;
+  // buffer written by reduction step i: U in place while f_i >= w (but X for
+  // the last such step when a single doubling step follows, which must not
+  // read and write U at once), then X / Y alternating so that the last step
+  // writes U.
+  auto rd_dst = [&](int32_t i) {
+    const int32_t back = L - 1 - i;
+    return back == 0 ? kBufU : (back % 2 == 1 ? kBufX : kBufY);
+  };
+  int32_t prim = kBufU;
+  bool local_copy = false;
+  for (int32_t i = 0; i < L; ++i) {
+    const int32_t f = P >> (i + 1);
+    std::vector<std::vector<POp>> per_p(P);
+    if (f >= w) {
+      const int32_t dst = (r == 1 && f == w) ? kBufX : kBufU;
+      for (int32_t p = 0; p < f; ++p) per_p[p].push_back(POp{kReduce, f, dst, kBufU, kBufNone, kBufNone, kBufU});
+      prim = dst;
+    } else {
+      int32_t dst = rd_dst(i);
+      if (dst == prim) {  // P = 2, k = 1: the only step reads U
+        dst = kBufX;
+        local_copy = true;
+      }
+      for (int32_t p = 0; p < w; ++p) per_p[p].push_back(POp{kReduce, f, dst, prim, kBufNone, kBufNone, prim});
+      prim = dst;
+    }
+    if (prim != kBufU) s->uses_scratch = true;
+    emit_launch(&s->launches, kPhaseReduce, per_p);
+  }
+  if (local_copy) {
+    std::vector<std::vector<POp>> cp_p(P);
+    for (int32_t p = 0; p < w; ++p) cp_p[p].push_back(POp{kCopy, 0, kBufU, kBufNone, kBufNone, kBufNone, kBufX});
+    emit_launch(&s->launches, kPhaseLocal, cp_p);
+  }
+  s->rs_steps = L;
+  for (int32_t i = L - 1; i >= 0; --i) {
+    const int32_t f = P >> (i + 1);
+    if (2 * f <= w) continue;
+    std::vector<std::vector<POp>> per_p(P);
+    for (int32_t p = f; p < 2 * f; ++p) per_p[p].push_back(POp{kCopy, f, kBufU, kBufNone, kBufNone, kBufNone, kBufU});
+    emit_launch(&s->launches, kPhaseDistribute, per_p);
+    ++s->ag_steps;
+  }
+}
+
 std::string build_schedule(int32_t P, int64_t n, int32_t k, Schedule* out) {
+  return build_schedule_ex(P, n, k, kGroupCyclic, kSchedButterfly, out);
+}
+
+std::string build_schedule_ex(int32_t P, int64_t n, int32_t k, int32_t group, int32_t sched, Schedule* out) {
   Schedule s;
   if (P < 1 || P > kMaxP) return "P must be in [1, 128]";
   if (n < 0) return "n must be >= 0";
+  if (group != kGroupCyclic && group != kGroupXor) return "unknown group";
+  if (sched != kSchedButterfly && sched != kSchedRing) return "unknown schedule";
+  if (group == kGroupXor && (P & (P - 1)) != 0) return "the XOR group needs a power-of-two P";
+  if (sched == kSchedRing && group != kGroupCyclic) return "the Ring schedule runs over the cyclic group";
   s.P = P;
   s.n = n;
   s.L = ceil_log2(P);
-  if (k < s.L || k > 2 * s.L) {
+  s.group = group;
+  s.sched = sched;
+  if (sched == kSchedRing) {
+    if (k != 2 * (P - 1)) {
+      char buf[96];
+      std::snprintf(buf, sizeof buf, "the Ring takes k_steps = 2(P-1) = %d for P=%d, got %d", 2 * (P - 1), P, k);
+      return buf;
+    }
+  } else if (k < s.L || k > 2 * s.L) {
     char buf[96];
     std::snprintf(buf, sizeof buf, "k_steps=%d outside [%d, %d] for P=%d", k, s.L, 2 * s.L, P);
     return buf;
   }
   s.k = k;
-  s.r = 2 * s.L - k;
+  s.r = sched == kSchedRing ? 0 : 2 * s.L - k;  // the Ring removes no distribution step
   s.w = int32_t(std::min<int64_t>(int64_t(1) << s.r, P));
   s.N.assign(s.L + 1, 0);
   s.f.assign(s.L, 0);
@@ -119,6 +218,11 @@ std::string build_schedule(int32_t P, int64_t n, int32_t k, Schedule* out) {
   const int32_t w = s.w;
   auto in_S = [&](int32_t p) { return p < w; };
 
+  if (sched == kSchedRing) {
+    ring_launches(&s);
+  } else if (group == kGroupXor) {
+    xor_launches(&s);
+  } else {
   // ---- reduction phase ----
   if (s.r == 0) {
     for (int32_t i = 0; i < s.L; ++i) {
@@ -189,6 +293,7 @@ std::string build_schedule(int32_t P, int64_t n, int32_t k, Schedule* out) {
     ++s.ag_steps;
     h = s.N[i];
   }
+  }  // cyclic butterfly
 
   // ---- sizes ----
   for (const Launch& l : s.launches) {
@@ -196,7 +301,7 @@ std::string build_schedule(int32_t P, int64_t n, int32_t k, Schedule* out) {
     for (const Range& rg : l.ranges) {
       for (int32_t j = 0; j < rg.count; ++j) {
         const int32_t p = pmod(rg.p0 + j, P);
-        if (rg.delta != 0) pulled.insert({rg.src, pmod(p + rg.delta, P)});
+        if (rg.delta != 0) pulled.insert({rg.src, group == kGroupXor ? (p ^ rg.delta) : pmod(p + rg.delta, P)});
         s.combines_per_rank += rg.kind == kReduce ? 1 : rg.kind == kReduce2 ? 2 : 0;
         s.hbm_blocks += rg.kind == kCopy ? 2 : rg.kind == kReduce ? 3 : 5;
       }
@@ -231,7 +336,7 @@ std::string check_hazards(const Schedule& s) {
     for (const Range& rg : l.ranges)
       for (int32_t j = 0; j < rg.count; ++j)
         for (int32_t x = 0; x < P; ++x, ++item) {
-          const int32_t p = pmod(rg.p0 + j, P), b = pmod(x - p, P);
+          const int32_t p = pmod(rg.p0 + j, P), b = group_block(s.group, x, p, P);
           for (int32_t d : {rg.dst, rg.dst2}) {
             if (d == kBufNone) continue;
             int64_t& wv = writer[key(d, x, b)];
@@ -244,8 +349,8 @@ std::string check_hazards(const Schedule& s) {
     for (const Range& rg : l.ranges)
       for (int32_t j = 0; j < rg.count; ++j)
         for (int32_t x = 0; x < P; ++x, ++item) {
-          const int32_t p = pmod(rg.p0 + j, P), b = pmod(x - p, P);
-          const int32_t y = pmod(x + rg.delta, P);
+          const int32_t p = pmod(rg.p0 + j, P), b = group_block(s.group, x, p, P);
+          const int32_t y = group_peer(s.group, x, rg.delta, P);
           const int64_t reads[3] = {rg.own == kBufNone ? -1 : key(rg.own, x, b),
                                     rg.own2 == kBufNone ? -1 : key(rg.own2, x, b),
                                     rg.src == kBufNone ? -1 : key(rg.src, y, b)};

@@ -158,6 +158,7 @@ def interpret(plan, x, op, order="forward"):
     tables' semantics as documented in include/ar.h)."""
     P, n = x.shape
     offs = part(n, P)
+    xor = plan.stats().group == ar.AR_GROUP_XOR
     bufs = {0: x.copy(), 1: np.zeros_like(x), 2: np.zeros_like(x)}
     for phase, ranges in plan.launches():
         items = []
@@ -169,9 +170,9 @@ def interpret(plan, x, op, order="forward"):
             items = items[::-1]
         src_bufs = {k: v.copy() for k, v in bufs.items()} if order == "snapshot" else bufs
         for r, p, rank in items:
-            b = (rank - p) % P
+            b = (rank ^ p) if xor else (rank - p) % P
             sl = slice(offs[b], offs[b + 1])
-            y = (rank + r["delta"]) % P
+            y = (rank ^ r["delta"]) if xor else (rank + r["delta"]) % P
             s = src_bufs[r["src"]][y, sl].copy()
             if r["kind"] == ar.AR_KIND_COPY:
                 bufs[r["dst"]][rank, sl] = s
