@@ -17,6 +17,11 @@ Workloads (seeded synthetic rank buffers, resident in HBM before timing):
   prime_sweep            P = 37, n = 2^22 fp32 U(-1,1), --k in 6..12 (default 12)
   large                  P = 127, n = 2^26 fp32 N(0,1e-2), --k 14 (default) or 10
   prime3                 P = 3, n = 1024 int32 U[-1000,1000], --k 2..4 (default 4)
+  gradsync32             P = 32, n = 2^24 fp32 N(0,1e-3), --k 5..10 (default 10)
+
+--group xor runs the butterfly schedules over the XOR group (power-of-two P:
+Recursive Halving at k = 2 log2 P, Recursive Doubling at k = log2 P);
+--schedule ring runs the Ring (k = 2(P-1)) on the workload's shape.
 
 Each step uses one of several input sets in turn, so that the sets together
 exceed the 256 MB Infinity Cache and every step reads HBM.
@@ -24,7 +29,6 @@ exceed the 256 MB Infinity Cache and every step reads HBM.
 Prints ONE JSON line.  Only one GPU is used: --gpus above 1 exits with an error.
 """
 import argparse
-import hashlib
 import json
 import os
 import sys
@@ -47,14 +51,18 @@ def ceil_log2(P):
     return max(0, (P - 1).bit_length())
 
 
-def jobs_for(name, k_arg):
+def jobs_for(name, k_arg, group="cyclic", schedule="butterfly"):
     from paper_2004_09362_amd import synth
     import numpy as np
 
     w = synth.WORKLOADS[name]
     jobs = []
     for P in w["P"]:
-        if w["ks"] == "lo":
+        if group == "xor" and P & (P - 1):
+            raise SystemExit("the XOR group needs a power-of-two P; the %s workload has P=%d" % (name, P))
+        if schedule == "ring":
+            k = 2 * (P - 1)
+        elif w["ks"] == "lo":
             k = ceil_log2(P)
         else:
             k = k_arg if k_arg is not None else DEFAULT_K[name]
@@ -65,26 +73,35 @@ def jobs_for(name, k_arg):
     return w, jobs
 
 
-DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4}
+DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4, "gradsync32": 10}
 
-DESCRIPTIONS = {
-    "small_batch": "small_batch: P in {5,6,7,12}, n=106 fp32 N(0,1), 65536 instances per launch, k=ceil(log2 P), sum",
-    "gradsync": "gradsync: P=24, n=16777216 fp32 N(0,1e-3), k=10 (bandwidth-optimal), sum",
-    "prime_sweep": "prime_sweep: P=37, n=4194304 fp32 U(-1,1), k=%d, sum",
-    "large": "large: P=127, n=67108864 fp32 N(0,1e-2), k=%d, sum",
-    "prime3": "prime3: P=3, n=1024 int32 U[-1000,1000], k=%d, sum",
+SHAPES = {
+    "small_batch": "small_batch: P in {5,6,7,12}, n=106 fp32 N(0,1), 65536 instances per launch",
+    "gradsync": "gradsync: P=24, n=16777216 fp32 N(0,1e-3)",
+    "prime_sweep": "prime_sweep: P=37, n=4194304 fp32 U(-1,1)",
+    "large": "large: P=127, n=67108864 fp32 N(0,1e-2)",
+    "prime3": "prime3: P=3, n=1024 int32 U[-1000,1000]",
+    "gradsync32": "gradsync32: P=32, n=16777216 fp32 N(0,1e-3)",
 }
 
 
+def describe(workload, jobs, group, schedule):
+    ks = sorted({j["k"] for j in jobs})
+    if schedule == "ring":
+        sched = "Ring k=2(P-1)" if len(ks) > 1 else "Ring k=%d" % ks[0]
+    else:
+        kk = "k=ceil(log2 P)" if len(ks) > 1 else "k=%d" % ks[0]
+        sched = ("XOR group " if group == "xor" else "") + kk
+    return "%s, %s, %s" % (SHAPES[workload], sched, jobs[0]["op"])
+
+
 def kernel_source_hash():
-    h = hashlib.sha256()
-    for f in ("kernels.hip", "capi.cpp", "plan.cpp", "ar_internal.hpp", "device_common.hpp", "fused_col.hpp"):
-        with open(os.path.join(ROOT, "paper_2004_09362_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
-    return h.hexdigest()[:16]
+    from paper_2004_09362_amd.build import source_hash
+
+    return source_hash()
 
 
-def traffic_from_profiles(workload, kernel, src_hash):
+def traffic_from_profiles(key, kernel, src_hash):
     """HBM bytes per launch from the committed counter summary, if it was
     taken on the current kernel sources; else None."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -93,7 +110,7 @@ def traffic_from_profiles(workload, kernel, src_hash):
     try:
         with open(path) as fh:
             data = json.load(fh)
-        ent = data.get(workload, {}).get(kernel)
+        ent = data.get(key, {}).get(kernel)
         if not ent or ent.get("source_hash") != src_hash:
             return None
         return ent.get("bytes_per_launch")
@@ -101,7 +118,12 @@ def traffic_from_profiles(workload, kernel, src_hash):
         return None
 
 
-def cpu_baseline(jobs, host_sets, budget_s=12.0):
+def traffic_key(workload, group, schedule):
+    """Entry of profiles/traffic.json for a workload run with a group and schedule."""
+    return workload + ("/xor" if group == "xor" else "") + ("/ring" if schedule == "ring" else "")
+
+
+def cpu_baseline(jobs, host_sets, budget_s=12.0, group="cyclic", schedule="butterfly"):
     """The CPU oracle (single thread, as it stands) on a bounded sample."""
     import numpy as np
 
@@ -120,7 +142,7 @@ def cpu_baseline(jobs, host_sets, budget_s=12.0):
                 xb = np.ascontiguousarray(x[:, :b])
                 t0 = time.perf_counter()
                 for _ in range(reps):
-                    oracle.allreduce_batched(xb, k, job["op"])
+                    oracle.allreduce_batched(xb, k, job["op"], group=group, schedule=schedule)
                 dt = time.perf_counter() - t0
                 if dt >= per_job_budget:
                     break
@@ -138,7 +160,7 @@ def cpu_baseline(jobs, host_sets, budget_s=12.0):
                 cols = np.unique(np.concatenate([np.arange(bb * q, bb * q + min(c, q)) for bb in range(P)]))
                 xs = np.ascontiguousarray(x[:, cols])
                 t0 = time.perf_counter()
-                oracle.allreduce(xs, k, job["op"], n=n, cols=cols)
+                oracle.allreduce(xs, k, job["op"], n=n, cols=cols, group=group, schedule=schedule)
                 dt = time.perf_counter() - t0
                 if dt >= per_job_budget or c >= q:
                     break
@@ -177,8 +199,10 @@ def main():
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="small_batch",
-                    choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3"])
+                    choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3", "gradsync32"])
     ap.add_argument("--k", type=int, default=None)
+    ap.add_argument("--group", choices=["cyclic", "xor"], default="cyclic")
+    ap.add_argument("--schedule", choices=["butterfly", "ring"], default="butterfly")
     ap.add_argument("--path", choices=["auto", "stepwise", "fused"], default="auto")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
@@ -204,7 +228,9 @@ def main():
     warmup = args.warmup if args.warmup is not None else (2 if args.workload == "large" else 5)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
-    w, jobs = jobs_for(args.workload, args.k)
+    if args.schedule == "ring" and args.group != "cyclic":
+        raise SystemExit("the Ring runs over the cyclic group")
+    w, jobs = jobs_for(args.workload, args.k, args.group, args.schedule)
     path = {"auto": ar.AR_PATH_AUTO, "stepwise": ar.AR_PATH_STEPWISE, "fused": ar.AR_PATH_FUSED}[args.path]
 
     # ---- plans and resident inputs ----
@@ -212,7 +238,8 @@ def main():
     n_sets = int(max(1, min(steps + warmup, -(-POOL_BYTES // set_bytes))))
     plans, sets = [], []
     for j in jobs:
-        p = ar.Plan(j["P"], j["n"], j["dtype"].name, j["op"], j["k"], path=path)
+        p = ar.Plan(j["P"], j["n"], j["dtype"].name, j["op"], j["k"], path=path, group=args.group,
+                    schedule=args.schedule)
         plans.append(p)
     log("workload %s: %d job(s), %d input set(s) of %.1f MB" % (args.workload, len(jobs), n_sets, set_bytes / 1e6))
     for s in range(n_sets):
@@ -279,7 +306,11 @@ def main():
     launch_ms = dom_ms / launches
     achieved = bytes_per_launch / (launch_ms * 1e-3) / 1e9
     if not fused:
-        kname = "step_kernel"
+        kname = "step_kernel<k=%d>" % dj["k"]
+    elif args.schedule == "ring":
+        kname = "fused_ring_kernel"
+    elif args.group == "xor":
+        kname = "fused_xor_kernel<P=%d,R=%d>" % (dj["P"], st.r)
     elif st.r == 0:
         kname = "fused_bo_kernel<P=%d>" % dj["P"]
     elif st.r == st.L and dj["P"] <= 16:
@@ -289,14 +320,12 @@ def main():
     src_hash = kernel_source_hash()
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic_from_profiles(args.workload, kname, src_hash),
+            "traffic": traffic_from_profiles(traffic_key(args.workload, args.group, args.schedule), kname, src_hash),
             "kernel": kname, "job_P": dj["P"], "bytes_per_launch": int(bytes_per_launch),
             "launch_ms": round(launch_ms, 5), "launches_per_step": launches}
     step_alg = sum(alg_bytes(j, p)[0] for j, p in zip(jobs, plans))
 
-    desc = DESCRIPTIONS[args.workload]
-    if "%d" in desc:
-        desc = desc % jobs[0]["k"]
+    desc = describe(args.workload, jobs, args.group, args.schedule)
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": steps,
         "warmup": warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
@@ -304,7 +333,8 @@ def main():
         "data": "synthetic (seeded; %d rotating input sets resident in HBM)" % n_sets,
         "config": {"workload": desc, "P": [j["P"] for j in jobs], "n": jobs[0]["n"], "batch": jobs[0]["batch"],
                    "k": [j["k"] for j in jobs], "op": jobs[0]["op"],
-                   "path": "fused" if fused else "stepwise", "parallelism": "1 GPU, P virtual ranks"},
+                   "path": "fused" if fused else "stepwise", "group": args.group, "schedule": args.schedule,
+                   "parallelism": "1 GPU, P virtual ranks"},
         "hbm_algorithmic_GBps_step": round(step_alg / (ms_per_step * 1e-3) / 1e9, 1),
         "wall_s_timed": round(wall, 4),
         "roofline": roof,
@@ -312,7 +342,7 @@ def main():
     }
     if host_sets is not None:
         log("timing the CPU oracle on a sample")
-        out["cpu_baseline"] = cpu_baseline(jobs, host_sets)
+        out["cpu_baseline"] = cpu_baseline(jobs, host_sets, group=args.group, schedule=args.schedule)
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)

@@ -72,6 +72,19 @@ def build(verbose: bool = False, incremental: bool = False) -> str:
     return LIB
 
 
+def source_hash() -> str:
+    """Short hash of every source and header of libar.so: profiles taken on
+    other sources are not reported as the current kernels' counters."""
+    import hashlib
+
+    h = hashlib.sha256()
+    for f in sorted(SOURCES + HEADERS, key=os.path.basename):
+        with open(f, "rb") as fh:
+            h.update(os.path.basename(f).encode())
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
 def stale() -> bool:
     if not os.path.exists(LIB):
         return True

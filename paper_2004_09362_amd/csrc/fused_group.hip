@@ -102,10 +102,14 @@ __global__ __launch_bounds__(kBlock) void fused_xor_kernel(const ColArgs a) {
   }
 }
 
-constexpr int kRingChunk = 16;  // loads in flight per lane along the chain
+constexpr int kRingChunk = 16;
 
-template <typename T, int OP, bool NT>
+// NC chunks of 16 ranks: the kernel serves 16 (NC - 1) + 1 < P <= 16 NC + 1,
+// so every load and store has a compile-time slot and a wave-uniform guard,
+// and all P loads of a column are in flight before the chain starts.
+template <int NC, typename T, int OP, bool NT>
 __global__ __launch_bounds__(kBlock) void fused_ring_kernel(const ColArgs a) {
+  constexpr int D = NC * kRingChunk;  // ranks after the root, upper bound
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int32_t P = a.P;
@@ -123,18 +127,41 @@ __global__ __launch_bounds__(kBlock) void fused_ring_kernel(const ColArgs a) {
     if (c >= 0 && c < len) {
       const int64_t e = e0 + c;
       T acc = ld1<NT>(static_cast<const T*>(rot[0]) + e);
-      for (int32_t d0 = 1; d0 < P; d0 += kRingChunk) {
-        T v[kRingChunk];
+      T v[D];
 #pragma unroll
-        for (int u = 0; u < kRingChunk; ++u)
-          if (d0 + u < P) v[u] = ld1<NT>(static_cast<const T*>(rot[d0 + u]) + e);
+      for (int d = 1; d <= D; ++d)
+        if (d < P) v[d - 1] = ld1<NT>(static_cast<const T*>(rot[d]) + e);
 #pragma unroll
-        for (int u = 0; u < kRingChunk; ++u)
-          if (d0 + u < P) acc = comb<OP>(v[u], acc);
-      }
-      for (int32_t d = 0; d < P; ++d) st1<NT>(static_cast<T*>(rot[d]) + e, acc);
+      for (int d = 1; d <= D; ++d)
+        if (d < P) acc = comb<OP>(v[d - 1], acc);
+#pragma unroll
+      for (int d = 0; d <= D; ++d)
+        if (d < P) st1<NT>(static_cast<T*>(rot[d]) + e, acc);
     }
   }
+}
+
+template <int NC>
+int launch_ring_nc(const ColArgs& a, int dtype, int op, bool nt, int grid, hipStream_t s) {
+  const dim3 g(grid), blk(kBlock);
+  if (dtype == 0) {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 1, false>), g, blk, 0, s, a);
+    }
+  } else {
+    if (op == 0) {
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, float, 0, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<NC, float, 0, false>), g, blk, 0, s, a);
+    } else {
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, float, 1, true>), g, blk, 0, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<NC, float, 1, false>), g, blk, 0, s, a);
+    }
+  }
+  return int(hipGetLastError());
 }
 
 template <int P, int R>
@@ -188,25 +215,17 @@ int launch_fused_xor(const ColArgs& a, int P, int dtype, int op, bool nt, int gr
 
 int launch_fused_ring(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const dim3 g(grid), blk(kBlock);
-  if (dtype == 0) {
-    if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_ring_kernel<int32_t, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_ring_kernel<int32_t, 0, false>), g, blk, 0, s, a);
-    } else {
-      if (nt) hipLaunchKernelGGL((fused_ring_kernel<int32_t, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_ring_kernel<int32_t, 1, false>), g, blk, 0, s, a);
-    }
-  } else {
-    if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_ring_kernel<float, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_ring_kernel<float, 0, false>), g, blk, 0, s, a);
-    } else {
-      if (nt) hipLaunchKernelGGL((fused_ring_kernel<float, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_ring_kernel<float, 1, false>), g, blk, 0, s, a);
-    }
+  switch ((a.P - 2) / kRingChunk) {  // P - 1 ranks after the root, in chunks of 16
+    case 0: return launch_ring_nc<1>(a, dtype, op, nt, grid, s);
+    case 1: return launch_ring_nc<2>(a, dtype, op, nt, grid, s);
+    case 2: return launch_ring_nc<3>(a, dtype, op, nt, grid, s);
+    case 3: return launch_ring_nc<4>(a, dtype, op, nt, grid, s);
+    case 4: return launch_ring_nc<5>(a, dtype, op, nt, grid, s);
+    case 5: return launch_ring_nc<6>(a, dtype, op, nt, grid, s);
+    case 6: return launch_ring_nc<7>(a, dtype, op, nt, grid, s);
+    case 7: return launch_ring_nc<8>(a, dtype, op, nt, grid, s);
+    default: return int(hipErrorInvalidValue);
   }
-  return int(hipGetLastError());
 }
 
 }  // namespace ar

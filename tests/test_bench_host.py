@@ -1,0 +1,117 @@
+"""Host-side checks of bench.py and of the rocprofv3 summary tool (no GPU)."""
+import csv
+import json
+import os
+import subprocess
+import sys
+
+import numpy as np
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+from paper_2004_09362_amd import profiling  # noqa: E402
+from paper_2004_09362_amd.build import source_hash  # noqa: E402
+
+
+def test_more_than_one_gpu_is_refused():
+    res = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                         text=True, timeout=120)
+    assert res.returncode == 2
+    assert "one GPU" in res.stderr
+
+
+@pytest.mark.parametrize("workload,k,group,schedule,want_P,want_k", [
+    ("small_batch", None, "cyclic", "butterfly", [5, 6, 7, 12], [3, 3, 3, 4]),
+    ("gradsync", None, "cyclic", "butterfly", [24], [10]),
+    ("gradsync", None, "cyclic", "ring", [24], [46]),
+    ("gradsync32", 7, "xor", "butterfly", [32], [7]),
+    ("prime_sweep", 9, "cyclic", "butterfly", [37], [9]),
+    ("large", None, "cyclic", "butterfly", [127], [14]),
+    ("prime3", None, "cyclic", "butterfly", [3], [4]),
+])
+def test_jobs(workload, k, group, schedule, want_P, want_k):
+    _, jobs = bench.jobs_for(workload, k, group, schedule)
+    assert [j["P"] for j in jobs] == want_P
+    assert [j["k"] for j in jobs] == want_k
+    desc = bench.describe(workload, jobs, group, schedule)
+    assert desc.startswith(workload + ":")
+    if schedule == "ring":
+        assert "Ring" in desc
+    if group == "xor":
+        assert "XOR" in desc
+
+
+def test_jobs_reject_bad_requests():
+    with pytest.raises(SystemExit):
+        bench.jobs_for("gradsync", None, "xor", "butterfly")     # P = 24 is not a power of two
+    with pytest.raises(SystemExit):
+        bench.jobs_for("prime_sweep", 13, "cyclic", "butterfly")  # k outside the workload's values
+
+
+def test_traffic_lookup_checks_the_source_hash(tmp_path, monkeypatch):
+    (tmp_path / "profiles").mkdir()
+    data = {"gradsync/ring": {"fused_ring_kernel": {"bytes_per_launch": 123, "source_hash": source_hash()}},
+            "gradsync": {"fused_bo_kernel<P=24>": {"bytes_per_launch": 456, "source_hash": "stale"}}}
+    (tmp_path / "profiles" / "traffic.json").write_text(json.dumps(data))
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    key = bench.traffic_key("gradsync", "cyclic", "ring")
+    assert bench.traffic_from_profiles(key, "fused_ring_kernel", source_hash()) == 123
+    assert bench.traffic_from_profiles("gradsync", "fused_bo_kernel<P=24>", source_hash()) is None
+    assert bench.traffic_from_profiles("gradsync", "missing", source_hash()) is None
+
+
+def test_cpu_baseline_runs_the_oracle_on_a_sample():
+    for workload, group, schedule in (("gradsync32", "xor", "butterfly"), ("gradsync", "cyclic", "ring")):
+        _, jobs = bench.jobs_for(workload, 10 if group == "xor" else None, group, schedule)
+        j = dict(jobs[0], n=64 * jobs[0]["P"])
+        x = np.random.default_rng(0).normal(size=(j["P"], j["n"])).astype(np.float32)
+        cb = bench.cpu_baseline([j], [x], budget_s=0.05, group=group, schedule=schedule)
+        assert cb["kind"] == "oracle" and cb["cores"] == 1 and cb["value"] > 0 and cb["unit"] == "GB/s"
+
+
+def _write_counters(d, counter, rows):
+    os.makedirs(d, exist_ok=True)
+    with open(os.path.join(d, "run_counter_collection.csv"), "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=["Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for name, val in rows:
+            w.writerow({"Kernel_Name": name, "Counter_Name": counter, "Counter_Value": val})
+
+
+def test_traffic_tool_scales_by_the_copy(tmp_path, monkeypatch):
+    """A counter that reads half of what the copy moved is scaled by 2."""
+    t = tmp_path
+    _write_counters(t / "cf", "FETCH_SIZE", [("__amd_rocclr_copyBuffer", 512.0)] * 3)
+    _write_counters(t / "cw", "WRITE_SIZE", [("__amd_rocclr_copyBuffer", 1024.0)] * 3)
+    _write_counters(t / "kf", "FETCH_SIZE", [("void ar::fused_bo_kernel<24, float, 0, true>(ar::ColArgs)", 100.0),
+                                             ("void ar::fused_bo_kernel<24, float, 0, true>(ar::ColArgs)", 102.0),
+                                             ("void ar::other_kernel()", 9e9)])
+    _write_counters(t / "kw", "WRITE_SIZE", [("void ar::fused_bo_kernel<24, float, 0, true>(ar::ColArgs)", 200.0)] * 2)
+    monkeypatch.setattr(profiling, "TRAFFIC", str(t / "traffic.json"))
+    ent = profiling.main(["traffic", "--key", "w", "--kernel", "k", "--match", "fused_bo_kernel<24,",
+                          "--fetch", str(t / "kf"), "--write", str(t / "kw"), "--copy-fetch", str(t / "cf"),
+                          "--copy-write", str(t / "cw"), "--copy-bytes", str(1024 * 1024), "--alg", "409600"])
+    assert ent is None
+    data = json.loads((t / "traffic.json").read_text())
+    e = data["w"]["k"]
+    assert e["fetch_scale"] == 2.0 and e["write_scale"] == 1.0
+    assert e["bytes_per_launch"] == int((101.0 * 2 + 200.0) * 1024)
+    assert e["launches_counted"] == 2 and e["source_hash"] == source_hash()
+
+
+def test_stats_tool_lists_library_kernels(tmp_path):
+    d = tmp_path / "tr"
+    d.mkdir()
+    with open(d / "run_kernel_stats.csv", "w", newline="") as fh:
+        w = csv.DictWriter(fh, fieldnames=["Name", "Calls", "AverageNs", "MinNs", "MaxNs"])
+        w.writeheader()
+        w.writerow({"Name": "void ar::(anonymous namespace)::fused_ring_kernel<2, float, 0, true>(ar::ColArgs)",
+                    "Calls": 25, "AverageNs": 536120.0, "MinNs": 527850.0, "MaxNs": 546930.0})
+        w.writerow({"Name": "__amd_rocclr_fillBufferAligned", "Calls": 3, "AverageNs": 1.0, "MinNs": 1.0,
+                    "MaxNs": 1.0})
+    out = profiling.stats(str(d))
+    assert "`fused_ring_kernel<2, float, 0, true>` | 25 | 536.12 | 527.85 | 546.93 |" in out
+    assert "fillBuffer" not in out
