@@ -95,10 +95,10 @@ def describe(workload, jobs, group, schedule):
     return "%s, %s, %s" % (SHAPES[workload], sched, jobs[0]["op"])
 
 
-def kernel_source_hash():
-    from paper_2004_09362_amd.build import source_hash
+def kernel_source_hash(kernel):
+    from paper_2004_09362_amd.build import kernel_family, source_hash
 
-    return source_hash()
+    return source_hash(kernel_family(kernel))
 
 
 def traffic_from_profiles(key, kernel, src_hash):
@@ -317,7 +317,7 @@ def main():
         kname = "fused_lo_kernel<P=%d>" % dj["P"]
     else:
         kname = "fused_mid_kernel<P=%d>" % dj["P"]
-    src_hash = kernel_source_hash()
+    src_hash = kernel_source_hash(kname)
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic_from_profiles(traffic_key(args.workload, args.group, args.schedule), kname, src_hash),

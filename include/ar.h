@@ -161,7 +161,10 @@ ar_status ar_plan_set_path(ar_plan* plan, ar_path path);
  * vectorised kernels.  With n = 0 nothing is touched and the pointers may be
  * NULL.  The first call on a plan that needs scratch (r > 0,
  * STEPWISE) allocates it on the current device; it is reused afterwards.
- * A plan must not run on two streams at once (shared scratch). */
+ * A plan must not run on two streams at once (shared scratch).  An execute
+ * only enqueues kernels (no memset, no synchronisation, no allocation once
+ * the scratch exists), so after one call with the same device, batch and
+ * stride it may be captured into a HIP graph. */
 ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t stream);
 
 /* `batch` independent Allreduce instances per rank: instance j of rank x is

@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libar.so")
-SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip", "fused_group.hip"] +
+SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip", "fused_lo.hip", "fused_group.hip"] +
            ["fused_col_g%d.hip" % i for i in range(8)]]
 HEADERS = [os.path.join(CSRC, f) for f in ("ar_internal.hpp", "device_common.hpp", "fused_col.hpp")] + [
     os.path.join(ROOT, "include", "ar.h")]
@@ -72,15 +72,35 @@ def build(verbose: bool = False, incremental: bool = False) -> str:
     return LIB
 
 
-def source_hash() -> str:
-    """Short hash of every source and header of libar.so: profiles taken on
-    other sources are not reported as the current kernels' counters."""
+# Sources of each kernel family (besides the common ones): a profile taken on
+# one family stays valid while only another family's sources change.
+COMMON = ["capi.cpp", "ar_internal.hpp", "device_common.hpp"]
+FAMILIES = {
+    "step": ["kernels.hip", "plan.cpp"],
+    "lo": ["fused_lo.hip"],
+    "col": ["fused_col.hpp"] + ["fused_col_g%d.hip" % i for i in range(8)],
+    "group": ["fused_group.hip"],
+}
+
+
+def kernel_family(kernel: str) -> str:
+    """Family of a kernel name as bench.py reports it."""
+    for prefix, fam in (("step_kernel", "step"), ("fused_lo_kernel", "lo"), ("fused_bo_kernel", "col"),
+                        ("fused_mid_kernel", "col"), ("fused_xor_kernel", "group"), ("fused_ring_kernel", "group")):
+        if kernel.startswith(prefix):
+            return fam
+    raise ValueError("unknown kernel %r" % kernel)
+
+
+def source_hash(family: str) -> str:
+    """Short hash of the sources that make up one kernel family: counter
+    profiles taken on other sources are not reported as current."""
     import hashlib
 
     h = hashlib.sha256()
-    for f in sorted(SOURCES + HEADERS, key=os.path.basename):
-        with open(f, "rb") as fh:
-            h.update(os.path.basename(f).encode())
+    for f in COMMON + FAMILIES[family]:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(f.encode())
             h.update(fh.read())
     return h.hexdigest()[:16]
 

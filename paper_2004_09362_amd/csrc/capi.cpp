@@ -46,6 +46,30 @@ struct ar_plan {
   bool ran = false;
 };
 
+namespace ar {
+
+// Column-fused kernels of the cyclic butterfly schedules: one instantiation
+// per P (fused_col_g*.hip), bandwidth-optimal (r = 0) or shifted (r >= 1).
+int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream) {
+  switch (P) {
+#define AR_BO_CASE(PP)                                                                                \
+  case PP:                                                                                            \
+    return a.r == 0 ? launch_fused_bo<PP>(a, dtype, op, nt, grid, stream)                             \
+                    : launch_fused_mid<PP>(a, dtype, op, nt, grid, stream);
+#define AR_BO_CASE8(B) AR_BO_CASE(B) AR_BO_CASE(B + 1) AR_BO_CASE(B + 2) AR_BO_CASE(B + 3) \
+  AR_BO_CASE(B + 4) AR_BO_CASE(B + 5) AR_BO_CASE(B + 6) AR_BO_CASE(B + 7)
+    AR_BO_CASE8(2) AR_BO_CASE8(10) AR_BO_CASE8(18) AR_BO_CASE8(26) AR_BO_CASE8(34) AR_BO_CASE8(42)
+    AR_BO_CASE8(50) AR_BO_CASE8(58) AR_BO_CASE8(66) AR_BO_CASE8(74) AR_BO_CASE8(82) AR_BO_CASE8(90)
+    AR_BO_CASE8(98) AR_BO_CASE8(106) AR_BO_CASE8(114) AR_BO_CASE(122) AR_BO_CASE(123) AR_BO_CASE(124)
+    AR_BO_CASE(125) AR_BO_CASE(126) AR_BO_CASE(127) AR_BO_CASE(128)
+#undef AR_BO_CASE8
+#undef AR_BO_CASE
+    default: return int(hipErrorInvalidValue);
+  }
+}
+
+}  // namespace ar
+
 namespace {
 
 thread_local std::string g_err;

@@ -1,29 +1,21 @@
-// kernels.hip -- HIP kernels of the generalized Allreduce for CDNA4 (gfx950).
+// kernels.hip -- the step kernel of the generalized Allreduce for CDNA4
+// (gfx950).
 //
 // Kolmakov & Zhang, "A Generalization of the Allreduce Operation"
-// (arXiv:2004.09362).  Two kernels:
+// (arXiv:2004.09362).  step_kernel runs one communication step of the
+// schedule (Secs. 6-9): every rank x, for each of its placements p in the
+// launch's ranges, combines (or copies) block b = (x - p) mod P of its own
+// buffer with the same block of rank (x + delta) mod P (in the XOR group:
+// block x XOR p, rank x XOR delta).  The work is pure streaming -- three
+// (copy: two, dual: five) block-sized HBM accesses per item, one add per
+// element -- so the kernel is built for HBM bandwidth: 64-lane waves,
+// 16-byte loads, several loads in flight per lane before the first store,
+// and no LDS (every byte is used exactly once, there is nothing to share
+// across lanes).
 //
-//  step_kernel   one communication step of the schedule (Secs. 6-9): every
-//                rank x, for each of its placements p in the launch's ranges,
-//                combines (or copies) block b = (x - p) mod P of its own
-//                buffer with the same block of rank (x + delta) mod P (in the
-//                XOR group: block x XOR p, rank x XOR delta).  The
-//                work is pure streaming -- three (copy: two, dual: five)
-//                block-sized HBM accesses per item, one add per element --
-//                so the kernel is built for HBM bandwidth: 64-lane waves,
-//                16-byte loads, several loads in flight per lane before the
-//                first store, and no LDS (every byte is used exactly once,
-//                there is nothing to share across lanes).
-//
-//  fused_lo_kernel  the whole latency-optimal schedule (Sec. 9) for one
-//                column of P values held in registers: the primed vector
-//                R[x] and the starred S[x] of every rank, updated as the
-//                reduction steps prescribe, then S[x] written to rank x.
-//                The pairs combined are exactly those of the step-by-step
-//                path, so the results are bit-identical, but each input is
-//                read once and each output written once (2*P*n elements).
-//
-// The column-fused kernels are in fused_col.hpp.
+// The fused kernels are in fused_lo.hip (latency-optimal, small P, no block
+// tiling), fused_col.hpp (column-fused, any P and k) and fused_group.hip
+// (XOR group and Ring).
 //
 // Compiled with packed-fp32 instructions disabled; only adds and compares,
 // so no contraction question arises.
@@ -125,7 +117,7 @@ __device__ __forceinline__ void seg_tile(T* __restrict__ dst, const T* __restric
 // divisions, short enough that a wave reaches its loads almost at once:
 // with one 16-byte vector per lane in flight, a long prologue would leave
 // the memory system idle.
-template <typename T, int OP, bool VEC, bool NT>
+template <typename T, int OP, bool VEC, bool NT, bool XOR>
 __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -145,7 +137,7 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
     int32_t p = R.p0 + (j - R.first);  // < 2P
     if (p >= P) p -= P;
     int32_t b, y;
-    if (a.group == kGroupXor) {         // t_k(x) = x XOR k: block x XOR p, peer x XOR delta
+    if constexpr (XOR) {                // t_k(x) = x XOR k: block x XOR p, peer x XOR delta
       b = x ^ p;
       y = x ^ R.delta;
     } else {                            // cyclic: block x - p, peer x + delta (|delta| < P)
@@ -174,135 +166,20 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   }
 }
 
-// ---------------------------------------------------------------------------
-// Fused latency-optimal kernel
-// ---------------------------------------------------------------------------
-
-constexpr int lo_L(int P) {
-  int L = 0;
-  while ((1 << L) < P) ++L;
-  return L;
-}
-constexpr int lo_N(int P, int i) {
-  int N = P;
-  for (int j = 0; j < i; ++j) N -= N / 2;
-  return N;
-}
-
-template <typename V, int OP>
-struct Comb;
-template <typename T, int OP>
-struct Comb<V4<T>, OP> {
-  __device__ __forceinline__ static V4<T> f(const V4<T>& a, const V4<T>& b) { return comb4<OP>(a, b); }
-};
-template <int OP>
-struct Comb<float, OP> {
-  __device__ __forceinline__ static float f(float a, float b) { return comb<OP>(a, b); }
-};
-template <int OP>
-struct Comb<int32_t, OP> {
-  __device__ __forceinline__ static int32_t f(int32_t a, int32_t b) { return comb<OP>(a, b); }
-};
-
-// Reduction step I of the latency-optimal schedule on one column: with
-// f = floor(N_I/2), every rank receives the primed vector of rank x + f;
-// starred sums take it on even N_I, primed sums on every step but the last.
-// Before the first odd step S and R hold the same values, and the compiler
-// computes their identical combinations once.
-template <int P, int I, int OP, typename V>
-__device__ __forceinline__ void lo_steps(V (&R)[P], V (&S)[P]) {
-  constexpr int L = lo_L(P);
-  if constexpr (I < L) {
-    constexpr int N = lo_N(P, I);
-    constexpr int f = N / 2;
-    constexpr bool even = (N % 2) == 0;
-    constexpr bool last = (I == L - 1);
-    V Rn[P];
-#pragma unroll
-    for (int x = 0; x < P; ++x) {
-      const V recv = R[(x + f) % P];
-      if constexpr (even) S[x] = Comb<V, OP>::f(S[x], recv);
-      if constexpr (!last) Rn[x] = Comb<V, OP>::f(R[x], recv);
-    }
-    if constexpr (!last) {
-#pragma unroll
-      for (int x = 0; x < P; ++x) R[x] = Rn[x];
-    }
-    lo_steps<P, I + 1, OP, V>(R, S);
-  }
-}
-
-// MODE 0: contiguous instances, column group g = elements [4g, 4g+4) of
-//         every rank (16-byte accesses);
-// MODE 1: contiguous instances, column g = element g (4-byte accesses);
-// MODE 2: any instance stride, column g = element g % n of instance g / n.
-template <int P, typename T, int OP, int MODE, bool NT>
-__global__ __launch_bounds__(kBlock) void fused_lo_kernel(const FusedArgs a) {
-  const int64_t nthreads = int64_t(gridDim.x) * kBlock;
-  for (int64_t g = int64_t(blockIdx.x) * kBlock + threadIdx.x; g < a.groups; g += nthreads) {
-    if constexpr (MODE == 0) {
-      V4<T> R[P], S[P];
-#pragma unroll
-      for (int x = 0; x < P; ++x) {
-        R[x] = ld4<NT>(reinterpret_cast<const V4<T>*>(a.user[x]) + g);
-        S[x] = R[x];
-      }
-      lo_steps<P, 0, OP, V4<T>>(R, S);
-#pragma unroll
-      for (int x = 0; x < P; ++x) st4<NT>(reinterpret_cast<V4<T>*>(a.user[x]) + g, S[x]);
-    } else {
-      int64_t e = g;
-      if constexpr (MODE == 2) {
-        const int64_t inst = g / a.n;
-        e = inst * a.stride + (g - inst * a.n);
-      }
-      T R[P], S[P];
-#pragma unroll
-      for (int x = 0; x < P; ++x) {
-        R[x] = ld1<NT>(reinterpret_cast<const T*>(a.user[x]) + e);
-        S[x] = R[x];
-      }
-      lo_steps<P, 0, OP, T>(R, S);
-#pragma unroll
-      for (int x = 0; x < P; ++x) st1<NT>(reinterpret_cast<T*>(a.user[x]) + e, S[x]);
-    }
-  }
-}
-
 template <typename T, int OP>
 int launch_step_t(const StepArgs& a, bool vec, bool nt, int grid, hipStream_t s) {
-  if (vec && nt) hipLaunchKernelGGL((step_kernel<T, OP, true, true>), dim3(grid), dim3(kBlock), 0, s, a);
-  else if (vec) hipLaunchKernelGGL((step_kernel<T, OP, true, false>), dim3(grid), dim3(kBlock), 0, s, a);
-  else hipLaunchKernelGGL((step_kernel<T, OP, false, false>), dim3(grid), dim3(kBlock), 0, s, a);
-  return int(hipGetLastError());
-}
-
-template <int P, typename T, int OP>
-int launch_fused_p(const FusedArgs& a, int mode, bool nt, int grid, hipStream_t s) {
-  const dim3 g(grid), blk(kBlock);
-  if (mode == 0) {
-    if (nt) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 0, true>), g, blk, 0, s, a);
-    else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 0, false>), g, blk, 0, s, a);
-  } else if (mode == 1) {
-    if (nt) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 1, true>), g, blk, 0, s, a);
-    else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 1, false>), g, blk, 0, s, a);
+  // the group is a template argument: the block / peer arithmetic sits in
+  // the prologue every wave runs before its first load
+  if (a.group == kGroupXor) {
+    if (vec && nt) hipLaunchKernelGGL((step_kernel<T, OP, true, true, true>), dim3(grid), dim3(kBlock), 0, s, a);
+    else if (vec) hipLaunchKernelGGL((step_kernel<T, OP, true, false, true>), dim3(grid), dim3(kBlock), 0, s, a);
+    else hipLaunchKernelGGL((step_kernel<T, OP, false, false, true>), dim3(grid), dim3(kBlock), 0, s, a);
   } else {
-    hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 2, false>), g, blk, 0, s, a);
+    if (vec && nt) hipLaunchKernelGGL((step_kernel<T, OP, true, true, false>), dim3(grid), dim3(kBlock), 0, s, a);
+    else if (vec) hipLaunchKernelGGL((step_kernel<T, OP, true, false, false>), dim3(grid), dim3(kBlock), 0, s, a);
+    else hipLaunchKernelGGL((step_kernel<T, OP, false, false, false>), dim3(grid), dim3(kBlock), 0, s, a);
   }
   return int(hipGetLastError());
-}
-
-template <typename T, int OP>
-int launch_fused_t(const FusedArgs& a, int P, int mode, bool nt, int grid, hipStream_t s) {
-  switch (P) {
-#define AR_LO_CASE(PP) \
-  case PP: return launch_fused_p<PP, T, OP>(a, mode, nt, grid, s);
-    AR_LO_CASE(2) AR_LO_CASE(3) AR_LO_CASE(4) AR_LO_CASE(5) AR_LO_CASE(6) AR_LO_CASE(7) AR_LO_CASE(8)
-    AR_LO_CASE(9) AR_LO_CASE(10) AR_LO_CASE(11) AR_LO_CASE(12) AR_LO_CASE(13) AR_LO_CASE(14)
-    AR_LO_CASE(15) AR_LO_CASE(16)
-#undef AR_LO_CASE
-    default: return int(hipErrorInvalidValue);
-  }
 }
 
 }  // namespace
@@ -321,31 +198,6 @@ int launch_step(const StepArgs& a, int dtype, int op, bool vec, bool nt, int gri
   if (dtype == 0)
     return op == 0 ? launch_step_t<int32_t, 0>(a, vec, nt, grid, s) : launch_step_t<int32_t, 1>(a, vec, nt, grid, s);
   return op == 0 ? launch_step_t<float, 0>(a, vec, nt, grid, s) : launch_step_t<float, 1>(a, vec, nt, grid, s);
-}
-
-int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, int mode, bool nt, int grid, void* stream) {
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (dtype == 0)
-    return op == 0 ? launch_fused_t<int32_t, 0>(a, P, mode, nt, grid, s) : launch_fused_t<int32_t, 1>(a, P, mode, nt, grid, s);
-  return op == 0 ? launch_fused_t<float, 0>(a, P, mode, nt, grid, s) : launch_fused_t<float, 1>(a, P, mode, nt, grid, s);
-}
-
-int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream) {
-  switch (P) {
-#define AR_BO_CASE(PP)                                                                                \
-  case PP:                                                                                            \
-    return a.r == 0 ? launch_fused_bo<PP>(a, dtype, op, nt, grid, stream)                             \
-                    : launch_fused_mid<PP>(a, dtype, op, nt, grid, stream);
-#define AR_BO_CASE8(B) AR_BO_CASE(B) AR_BO_CASE(B + 1) AR_BO_CASE(B + 2) AR_BO_CASE(B + 3) \
-  AR_BO_CASE(B + 4) AR_BO_CASE(B + 5) AR_BO_CASE(B + 6) AR_BO_CASE(B + 7)
-    AR_BO_CASE8(2) AR_BO_CASE8(10) AR_BO_CASE8(18) AR_BO_CASE8(26) AR_BO_CASE8(34) AR_BO_CASE8(42)
-    AR_BO_CASE8(50) AR_BO_CASE8(58) AR_BO_CASE8(66) AR_BO_CASE8(74) AR_BO_CASE8(82) AR_BO_CASE8(90)
-    AR_BO_CASE8(98) AR_BO_CASE8(106) AR_BO_CASE8(114) AR_BO_CASE(122) AR_BO_CASE(123) AR_BO_CASE(124)
-    AR_BO_CASE(125) AR_BO_CASE(126) AR_BO_CASE(127) AR_BO_CASE(128)
-#undef AR_BO_CASE8
-#undef AR_BO_CASE
-    default: return int(hipErrorInvalidValue);
-  }
 }
 
 }  // namespace ar

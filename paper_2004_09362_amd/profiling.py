@@ -13,8 +13,9 @@
       values in KiB per dispatch), each scaled by what the same counter read
       for a plain device copy of N bytes (`bench.py --copy-probe N`), so that
       a counter reading exactly what the copy moved scales by 1.  Stored in
-      profiles/traffic.json under KEY and NAME with the current kernel source
-      hash, which bench.py compares before it reports the figure.
+      profiles/traffic.json under KEY and NAME (a kernel name as bench.py
+      reports it) with the hash of that kernel family's current sources,
+      which bench.py compares before it reports the figure.
 
 Reads rocprofv3's CSV files only; runs nothing on the GPU.
 """
@@ -26,7 +27,7 @@ import json
 import os
 import sys
 
-from .build import source_hash
+from .build import kernel_family, source_hash
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
@@ -72,7 +73,7 @@ def traffic(a) -> dict:
     ent = {"bytes_per_launch": int(round(b)), "fetch_KiB_raw": round(mean(f), 1), "write_KiB_raw": round(mean(w), 1),
            "fetch_scale": round(sf, 4), "write_scale": round(sw, 4), "launches_counted": len(f),
            "algorithmic_bytes_per_launch": a.alg, "ratio_to_algorithmic": round(b / a.alg, 5) if a.alg else None,
-           "source_hash": source_hash()}
+           "source_hash": source_hash(kernel_family(a.kernel))}
     data = {}
     if os.path.exists(TRAFFIC):
         with open(TRAFFIC) as fh:

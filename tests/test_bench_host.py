@@ -53,14 +53,27 @@ def test_jobs_reject_bad_requests():
 
 def test_traffic_lookup_checks_the_source_hash(tmp_path, monkeypatch):
     (tmp_path / "profiles").mkdir()
-    data = {"gradsync/ring": {"fused_ring_kernel": {"bytes_per_launch": 123, "source_hash": source_hash()}},
+    h = source_hash("group")
+    data = {"gradsync/ring": {"fused_ring_kernel": {"bytes_per_launch": 123, "source_hash": h}},
             "gradsync": {"fused_bo_kernel<P=24>": {"bytes_per_launch": 456, "source_hash": "stale"}}}
     (tmp_path / "profiles" / "traffic.json").write_text(json.dumps(data))
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
     key = bench.traffic_key("gradsync", "cyclic", "ring")
-    assert bench.traffic_from_profiles(key, "fused_ring_kernel", source_hash()) == 123
-    assert bench.traffic_from_profiles("gradsync", "fused_bo_kernel<P=24>", source_hash()) is None
-    assert bench.traffic_from_profiles("gradsync", "missing", source_hash()) is None
+    assert bench.kernel_source_hash("fused_ring_kernel") == h
+    assert bench.traffic_from_profiles(key, "fused_ring_kernel", h) == 123
+    assert bench.traffic_from_profiles("gradsync", "fused_bo_kernel<P=24>", source_hash("col")) is None
+    assert bench.traffic_from_profiles("gradsync", "missing", h) is None
+
+
+def test_kernel_families_cover_every_source():
+    from paper_2004_09362_amd import build as b
+
+    listed = set(b.COMMON) | {f for fam in b.FAMILIES.values() for f in fam}
+    have = {os.path.basename(f) for f in b.SOURCES + b.HEADERS if "/csrc/" in f}
+    assert have == listed
+    assert {b.kernel_family(k) for k in ("step_kernel<k=10>", "fused_lo_kernel<P=12>", "fused_bo_kernel<P=24>",
+                                         "fused_mid_kernel<P=37>", "fused_xor_kernel<P=32,R=0>",
+                                         "fused_ring_kernel")} == {"step", "lo", "col", "group"}
 
 
 def test_cpu_baseline_runs_the_oracle_on_a_sample():
@@ -91,15 +104,15 @@ def test_traffic_tool_scales_by_the_copy(tmp_path, monkeypatch):
                                              ("void ar::other_kernel()", 9e9)])
     _write_counters(t / "kw", "WRITE_SIZE", [("void ar::fused_bo_kernel<24, float, 0, true>(ar::ColArgs)", 200.0)] * 2)
     monkeypatch.setattr(profiling, "TRAFFIC", str(t / "traffic.json"))
-    ent = profiling.main(["traffic", "--key", "w", "--kernel", "k", "--match", "fused_bo_kernel<24,",
+    ent = profiling.main(["traffic", "--key", "w", "--kernel", "fused_bo_kernel<P=24>", "--match", "fused_bo_kernel<24,",
                           "--fetch", str(t / "kf"), "--write", str(t / "kw"), "--copy-fetch", str(t / "cf"),
                           "--copy-write", str(t / "cw"), "--copy-bytes", str(1024 * 1024), "--alg", "409600"])
     assert ent is None
     data = json.loads((t / "traffic.json").read_text())
-    e = data["w"]["k"]
+    e = data["w"]["fused_bo_kernel<P=24>"]
     assert e["fetch_scale"] == 2.0 and e["write_scale"] == 1.0
     assert e["bytes_per_launch"] == int((101.0 * 2 + 200.0) * 1024)
-    assert e["launches_counted"] == 2 and e["source_hash"] == source_hash()
+    assert e["launches_counted"] == 2 and e["source_hash"] == source_hash("col")
 
 
 def test_stats_tool_lists_library_kernels(tmp_path):
