@@ -96,9 +96,9 @@ def describe(workload, jobs, group, schedule):
 
 
 def kernel_source_hash(kernel):
-    from paper_2004_09362_amd.build import kernel_family, source_hash
+    from paper_2004_09362_amd.build import kernel_families, source_hash
 
-    return source_hash(kernel_family(kernel))
+    return source_hash(kernel_families(kernel))
 
 
 def traffic_from_profiles(key, kernel, src_hash):
@@ -301,7 +301,7 @@ def main():
     # ---- roofline of the dominant kernel ----
     dj, dp = jobs[dom], plans[dom]
     alg, fused, st = alg_bytes(dj, dp)
-    launches = 1 if fused else st.launches
+    launches = st.fused_launches if fused else st.launches
     bytes_per_launch = alg / launches
     launch_ms = dom_ms / launches
     achieved = bytes_per_launch / (launch_ms * 1e-3) / 1e9
@@ -317,6 +317,8 @@ def main():
         kname = "fused_lo_kernel<P=%d>" % dj["P"]
     else:
         kname = "fused_mid_kernel<P=%d>" % dj["P"]
+    if fused and st.fused_launches == 2:
+        kname += "+broadcast"  # the pair: reducing launch, then the broadcast
     src_hash = kernel_source_hash(kname)
     roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),

@@ -72,6 +72,10 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *             XOR group and the Ring's chain; latency-optimal cyclic plans
  *             with P <= 16 take a kernel without block tiling (many
  *             independent small instances, Sec. 1's 425-byte average).
+ *             Where every rank receives the same result (bandwidth-optimal
+ *             plans, the Ring) and P >= 48, the launch stores each block's
+ *             result on one rank and a second launch broadcasts it: one more
+ *             block read and written per column, measured faster there.
  *   AUTO:     FUSED where it applies (P >= 2), STEPWISE otherwise.
  * Both paths combine exactly the same operand pairs in the same order, so
  * their results are bit-identical. */
@@ -105,9 +109,13 @@ typedef struct {
   int64_t bytes_pulled_total;        /* over all ranks = blocks_pulled_per_rank * n * e  */
   int64_t combines_per_rank;         /* block combinations                               */
   int64_t hbm_bytes_stepwise;        /* algorithmic HBM bytes of the STEPWISE path       */
-  int64_t hbm_bytes_fused;           /* 2 * P * n * e: read every input, write every output */
+  int64_t hbm_bytes_fused;           /* FUSED path: 2 * P * n * e (read every input, write
+                                        every output), (2P + 1) * n * e when split       */
   int64_t workspace_bytes;           /* device scratch per instance, STEPWISE path       */
   int32_t group, schedule;           /* ar_group and ar_schedule of the plan              */
+  int32_t fused_launches;            /* FUSED path: 1, or 2 when split into a reducing
+                                        launch and a broadcast (every rank receives the
+                                        same result and P >= 48)                          */
 } ar_stats;
 
 /* One launch of the STEPWISE path: a list of placement ranges.  In a range,

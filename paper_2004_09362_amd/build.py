@@ -16,7 +16,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libar.so")
-SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip", "fused_lo.hip", "fused_group.hip"] +
+SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip", "fused_lo.hip", "fused_group.hip",
+                                           "broadcast.hip"] +
            ["fused_col_g%d.hip" % i for i in range(8)]]
 HEADERS = [os.path.join(CSRC, f) for f in ("ar_internal.hpp", "device_common.hpp", "fused_col.hpp")] + [
     os.path.join(ROOT, "include", "ar.h")]
@@ -80,25 +81,36 @@ FAMILIES = {
     "lo": ["fused_lo.hip"],
     "col": ["fused_col.hpp"] + ["fused_col_g%d.hip" % i for i in range(8)],
     "group": ["fused_group.hip"],
+    "bcast": ["broadcast.hip"],
 }
 
 
-def kernel_family(kernel: str) -> str:
-    """Family of a kernel name as bench.py reports it."""
-    for prefix, fam in (("step_kernel", "step"), ("fused_lo_kernel", "lo"), ("fused_bo_kernel", "col"),
-                        ("fused_mid_kernel", "col"), ("fused_xor_kernel", "group"), ("fused_ring_kernel", "group")):
-        if kernel.startswith(prefix):
-            return fam
-    raise ValueError("unknown kernel %r" % kernel)
+def kernel_families(kernel: str) -> list[str]:
+    """Families of a kernel name as bench.py reports it; a split launch
+    ("<reducing kernel>+broadcast") has both kernels' families."""
+    out = []
+    for part in kernel.split("+"):
+        for prefix, fam in (("step_kernel", "step"), ("fused_lo_kernel", "lo"), ("fused_bo_kernel", "col"),
+                            ("fused_mid_kernel", "col"), ("fused_xor_kernel", "group"),
+                            ("fused_ring_kernel", "group"), ("broadcast", "bcast")):
+            if part.startswith(prefix):
+                out.append(fam)
+                break
+        else:
+            raise ValueError("unknown kernel %r" % kernel)
+    return out
 
 
-def source_hash(family: str) -> str:
-    """Short hash of the sources that make up one kernel family: counter
-    profiles taken on other sources are not reported as current."""
+def source_hash(families) -> str:
+    """Short hash of the sources that make up one kernel family (or a list
+    of families): counter profiles taken on other sources are not reported
+    as current."""
     import hashlib
 
+    if isinstance(families, str):
+        families = [families]
     h = hashlib.sha256()
-    for f in COMMON + FAMILIES[family]:
+    for f in COMMON + [f for fam in families for f in FAMILIES[fam]]:
         with open(os.path.join(CSRC, f), "rb") as fh:
             h.update(f.encode())
             h.update(fh.read())

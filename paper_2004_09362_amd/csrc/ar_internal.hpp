@@ -123,10 +123,13 @@ struct StepArgs {
   DevRange ranges[kMaxRanges];
 };
 
+// lds: dynamic LDS each workgroup reserves without using it, so that fewer
+// workgroups are resident per CU (0: no cap); read by the launchers.
 struct FusedArgs {
   void* user[kMaxP];
   int64_t n, stride, batch;
   int64_t groups;           // column groups (16-byte mode) or columns (other modes)
+  uint32_t lds;
 };
 
 // Column kernels: wave tile t -> (instance, block, 64 columns of the block).
@@ -138,6 +141,8 @@ struct ColArgs {
   uint32_t total_tiles;     // batch * P * tiles (< 2^31)
   FastDiv tiles, pdiv;      // column tiles per block, P
   int32_t P, r;             // r: distribution steps removed (kept shifts w = min(2^r, P))
+  int32_t split;            // 1: store the block's result to its root rank only (a broadcast follows)
+  uint32_t lds;             // as in FusedArgs
 };
 
 // dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.
@@ -158,6 +163,9 @@ int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, in
 // power of two and any r, and the Ring for any P in 2..128.
 int launch_fused_xor(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream);
 int launch_fused_ring(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream);
+// Second half of a split fused launch (broadcast.hip): block b's result,
+// stored on rank b by the reducing kernel, copied to the other P - 1 ranks.
+int launch_broadcast(const ColArgs& a, int dtype, int grid, void* stream);
 // Workgroups of a step launch over `total_tiles` wave tiles, and the tile size.
 int step_grid(int64_t total_tiles);
 int64_t step_tile_elems();

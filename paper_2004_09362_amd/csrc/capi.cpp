@@ -22,6 +22,28 @@
 // smaller sizes, switch at a lower mark.
 constexpr int64_t kNtThresholdBytes = int64_t(512) << 20;
 constexpr int64_t kFusedNtThresholdBytes = int64_t(128) << 20;
+// Plans whose ranks all receive the same result (bandwidth-optimal in either
+// group, the Ring) run fused as a reducing launch plus a broadcast from this
+// many ranks up (broadcast.hip): measured faster at P = 64 and 127, slower
+// at P = 24.
+constexpr int32_t kSplitMinP = 48;
+
+// Occupancy caps of the fused kernels.  Every fused launch streams P rank
+// buffers in and out at once, and HBM serves that pattern faster when fewer
+// waves are resident: fewer DRAM rows are open at a time.  A launch caps the
+// workgroups resident per CU (one wave per SIMD each) by reserving LDS it
+// does not use.  The caps below are the best points measured on MI355X
+// (gfx950) at the benchmark shapes, against no cap:
+//   latency-optimal, 65536 instances of 106 elements: P = 5 and 7 at 5,
+//     P = 6 at 4, P = 12 at 3-4 (2-4%);
+//   bandwidth-optimal, P = 24 and 32 at 3-4, P = 37 at 3 (3-4%);
+//   shifted, P = 37 at 2-3 (2%); at P = 127 its registers already allow only
+//     one wave per SIMD, and a cap changes nothing;
+//   the Ring at P = 24: 4 (2%);
+//   split launches (P = 127): the reducing launch at 3-6, the broadcast at 2.
+// AR_FUSED_CAP = N (both launches) or N,M (fused launch, broadcast) overrides
+// them; 0 is no cap.
+static int32_t lo_cap(int32_t P) { return P <= 4 ? 0 : P == 6 ? 4 : P <= 7 ? 5 : P <= 11 ? 4 : 3; }
 
 // Which single-launch kernel runs a plan on the FUSED path: the flat
 // latency-optimal kernel (small P; its columns need no block index), the
@@ -34,8 +56,14 @@ struct ar_plan {
   int32_t dtype = 0, op = 0;
   // Tuning overrides read from the environment at plan creation:
   // AR_STEP_NT / AR_FUSED_NT = 0|1 (nontemporal never / always; default by
-  // launch size), AR_FUSED_MODE = 0|1 (16-byte or 4-byte columns).
-  int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1;
+  // launch size), AR_FUSED_MODE = 0|1 (16-byte or 4-byte columns),
+  // AR_FUSED_SPLIT = 0|1 (single fused launch / reduce plus broadcast, where
+  // every rank receives the same result; default by P).
+  int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1, split_mode = -1;
+  bool fused_split = false;
+  // Occupancy caps (resident workgroups per CU; 0: none) of the fused launch
+  // and of the broadcast that follows a split one.  AR_FUSED_CAP = N forces N.
+  int32_t fused_cap = 0, bcast_cap = 0;
   int32_t path = AR_PATH_AUTO;
   int32_t fused_kind = kFusedNone;
   bool fused_ok = false;
@@ -133,6 +161,27 @@ ar_status ensure_scratch(ar_plan* pl, size_t need, int device) {
   return AR_OK;
 }
 
+// LDS a workgroup reserves so that at most `cap` workgroups fit on a CU of
+// `device` (0 for no cap).  Cached per device.
+uint32_t cap_lds(int32_t cap, int device) {
+  static int64_t per_cu[64] = {}, per_block[64] = {};
+  if (cap <= 0 || device < 0 || device >= 64) return 0;
+  if (per_cu[device] == 0) {
+    int a = 0, b = 0;
+    if (hipDeviceGetAttribute(&a, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) != hipSuccess ||
+        hipDeviceGetAttribute(&b, hipDeviceAttributeMaxSharedMemoryPerBlock, device) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    per_cu[device] = a;
+    per_block[device] = b;
+  }
+  // cap workgroups fit, cap + 1 do not (1 KB margin, 512-byte allocation steps)
+  int64_t bytes = (per_cu[device] / cap - 1024) / 512 * 512;
+  if (bytes <= 0 || per_cu[device] / (cap + 1) >= bytes) return 0;
+  return uint32_t(std::min(bytes, per_block[device]));
+}
+
 bool use_nt(int32_t mode, int64_t bytes, int64_t threshold = kNtThresholdBytes) {
   return mode == 1 || (mode < 0 && bytes >= threshold);
 }
@@ -193,7 +242,8 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   return AR_OK;
 }
 
-ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool all16, hipStream_t stream) {
+ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool all16, hipStream_t stream,
+                       int device) {
   const ar::Schedule& s = pl->s;
   ar::FusedArgs a;
   std::memset(&a, 0, sizeof a);
@@ -209,12 +259,14 @@ ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   int64_t blocks = (a.groups + 255) / 256;
   blocks = std::min<int64_t>(std::max<int64_t>(blocks, 1), int64_t(1) << 22);
   const bool nt = mode != 2 && use_nt(pl->fused_nt_mode, int64_t(2) * s.P * cols * 4, kFusedNtThresholdBytes);
+  a.lds = cap_lds(pl->fused_cap, device);
   const int e = ar::launch_fused_lo(a, s.P, pl->dtype, pl->op, mode, nt, int(blocks), stream);
   if (e != 0) return hip_fail(hipError_t(e), "fused latency-optimal kernel launch");
   return AR_OK;
 }
 
-ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, hipStream_t stream) {
+ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, hipStream_t stream,
+                        int device) {
   // one ColArgs layout for every column kernel; the XOR kernel reads the
   // first P entries of the rank table, the others a rotation of it
   const ar::Schedule& s = pl->s;
@@ -223,6 +275,7 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   for (int32_t x = 0; x < 2 * s.P; ++x) a.user[x] = bufs[x % s.P];
   a.P = s.P;
   a.r = s.r;
+  a.split = pl->fused_split ? 1 : 0;
   a.stride = stride;
   a.q = s.n / s.P;
   a.m = s.n % s.P;
@@ -237,11 +290,17 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   a.pdiv = ar::make_fastdiv(uint32_t(s.P));
   const bool nt = use_nt(pl->fused_nt_mode, int64_t(2) * s.P * s.n * batch * 4, kFusedNtThresholdBytes);
   const int grid = ar::step_grid(total);
+  a.lds = cap_lds(pl->fused_cap, device);
   int e;
   if (pl->fused_kind == kFusedXor) e = ar::launch_fused_xor(a, s.P, pl->dtype, pl->op, nt, grid, stream);
   else if (pl->fused_kind == kFusedRing) e = ar::launch_fused_ring(a, pl->dtype, pl->op, nt, grid, stream);
   else e = ar::launch_fused_col_any(a, s.P, pl->dtype, pl->op, nt, grid, stream);
   if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");
+  if (pl->fused_split) {
+    a.lds = cap_lds(pl->bcast_cap, device);
+    e = ar::launch_broadcast(a, pl->dtype, grid, stream);
+    if (e != 0) return hip_fail(hipError_t(e), "broadcast kernel launch");
+  }
   return AR_OK;
 }
 
@@ -274,12 +333,33 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
   pl->nt_mode = env_mode("AR_STEP_NT");
   pl->fused_nt_mode = env_mode("AR_FUSED_NT");
   pl->fused_mode = env_mode("AR_FUSED_MODE");
+  pl->split_mode = env_mode("AR_FUSED_SPLIT");
   if (pl->s.P < 2) pl->fused_kind = kFusedNone;
   else if (pl->s.sched == ar::kSchedRing) pl->fused_kind = kFusedRing;
   else if (pl->s.group == ar::kGroupXor) pl->fused_kind = kFusedXor;
   else if (pl->s.P <= ar::kFusedMaxP && pl->s.r == pl->s.L) pl->fused_kind = kFusedLo;
   else pl->fused_kind = kFusedCol;
   pl->fused_ok = pl->fused_kind != kFusedNone;
+  // one result for every rank: the Ring, and r = 0 outside the flat LO kernel
+  const bool one_result = pl->fused_kind == kFusedRing ||
+                          ((pl->fused_kind == kFusedCol || pl->fused_kind == kFusedXor) && pl->s.r == 0);
+  pl->fused_split = one_result && (pl->split_mode == 1 || (pl->split_mode < 0 && pl->s.P >= kSplitMinP));
+  {
+    const int32_t P = pl->s.P;
+    if (pl->fused_split) pl->fused_cap = 6;
+    else if (pl->fused_kind == kFusedLo) pl->fused_cap = lo_cap(P);
+    else if (pl->fused_kind == kFusedRing) pl->fused_cap = 4;
+    else if (pl->s.r == 0) pl->fused_cap = P <= 32 ? 4 : 3;
+    else pl->fused_cap = P >= 64 ? 0 : 3;
+    pl->bcast_cap = 2;
+    // AR_FUSED_CAP = N caps both launches, "N,M" the fused one and the broadcast
+    const char* ce = std::getenv("AR_FUSED_CAP");
+    if (ce != nullptr && ce[0] >= '0' && ce[0] <= '9') {
+      pl->fused_cap = pl->bcast_cap = std::atoi(ce);
+      const char* comma = std::strchr(ce, ',');
+      if (comma != nullptr && comma[1] >= '0' && comma[1] <= '9') pl->bcast_cap = std::atoi(comma + 1);
+    }
+  }
   *out_plan = pl;
   g_err.clear();
   return AR_OK;
@@ -321,9 +401,9 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
   if (elems / batch / plan->s.P != plan->s.n) return fail(AR_ERR_INVALID_ARG, "size overflow");
   const bool fused = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok);
   if (fused && plan->fused_kind != kFusedLo) {
-    st = run_fused_col(plan, rank_buffers, batch, instance_stride, stream);
+    st = run_fused_col(plan, rank_buffers, batch, instance_stride, stream, device);
   } else if (fused) {
-    st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream);
+    st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream, device);
   } else {
     const bool vec = all16 && (batch == 1 || instance_stride % 4 == 0);
     st = run_stepwise(plan, rank_buffers, batch, instance_stride, vec, stream, device);
@@ -382,7 +462,8 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
   out->bytes_pulled_total = total;
   out->combines_per_rank = s.combines_per_rank;
   out->hbm_bytes_stepwise = s.hbm_blocks * s.n * 4;
-  out->hbm_bytes_fused = s.P > 1 ? int64_t(2) * s.P * s.n * 4 : 0;
+  out->hbm_bytes_fused = s.P > 1 ? (int64_t(2) * s.P + (plan->fused_split ? 1 : 0)) * s.n * 4 : 0;
+  out->fused_launches = s.P > 1 ? (plan->fused_split ? 2 : 1) : 0;
   out->workspace_bytes = s.uses_scratch ? int64_t(2) * s.P * round_up(s.n, 64) * 4 : 0;
   out->group = s.group;
   out->schedule = s.sched;

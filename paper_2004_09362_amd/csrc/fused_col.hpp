@@ -15,6 +15,11 @@
 // is read once and every output written once (2 * P * n elements of HBM
 // traffic instead of 5 * (P - 1) * n).
 //
+// With a.split set, only the root rank b receives the result and a second
+// launch (broadcast.hip) copies it to the other ranks: the same bits, one
+// more read and write of a block per column, but the reading and the writing
+// of the P streams no longer interleave (see the broadcast kernel).
+//
 // One wave covers 64 consecutive columns of one block of one instance, one
 // 4-byte element per lane: the block, hence the rotation of the rank
 // pointers, is uniform across the wave and every access is a coalesced
@@ -103,8 +108,12 @@ __global__ __launch_bounds__(kBlock) void fused_bo_kernel(const ColArgs a) {
 #pragma unroll
       for (int d = 0; d < P; ++d) w[d] = ld1<NT>(static_cast<const T*>(rot[d]) + e);
       bo_fold<P, OP, T, P>(w);
+      if (a.split) {
+        st1<NT>(static_cast<T*>(rot[0]) + e, w[0]);
+      } else {
 #pragma unroll
-      for (int d = 0; d < P; ++d) st1<NT>(static_cast<T*>(rot[d]) + e, w[0]);
+        for (int d = 0; d < P; ++d) st1<NT>(static_cast<T*>(rot[d]) + e, w[0]);
+      }
     }
   }
 }
@@ -199,19 +208,19 @@ int launch_fused_bo(const ColArgs& a, int dtype, int op, bool nt, int grid, void
   const dim3 g(grid), blk(kBlock);
   if (dtype == 0) {
     if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 0, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 0, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 0, false>), g, blk, a.lds, s, a);
     } else {
-      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 1, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 1, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_bo_kernel<P, int32_t, 1, false>), g, blk, a.lds, s, a);
     }
   } else {
     if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, float, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_bo_kernel<P, float, 0, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, float, 0, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_bo_kernel<P, float, 0, false>), g, blk, a.lds, s, a);
     } else {
-      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, float, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_bo_kernel<P, float, 1, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_bo_kernel<P, float, 1, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_bo_kernel<P, float, 1, false>), g, blk, a.lds, s, a);
     }
   }
   return int(hipGetLastError());
@@ -227,19 +236,19 @@ int launch_fused_mid(const ColArgs& a, int dtype, int op, bool nt, int grid, voi
   const dim3 g(grid), blk(kBlock);
   if (dtype == 0) {
     if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 0, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 0, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 0, false>), g, blk, a.lds, s, a);
     } else {
-      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 1, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 1, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_mid_kernel<P, int32_t, 1, false>), g, blk, a.lds, s, a);
     }
   } else {
     if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, float, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_mid_kernel<P, float, 0, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, float, 0, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_mid_kernel<P, float, 0, false>), g, blk, a.lds, s, a);
     } else {
-      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, float, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_mid_kernel<P, float, 1, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_mid_kernel<P, float, 1, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_mid_kernel<P, float, 1, false>), g, blk, a.lds, s, a);
     }
   }
   return int(hipGetLastError());

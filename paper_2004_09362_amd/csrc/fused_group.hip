@@ -30,7 +30,9 @@
 // Both read every input once and write every output once (2 * P * n
 // elements), one 4-byte element per lane, 64 consecutive columns of one
 // block per wave, tiles laid on 256-byte boundaries of the block's root rank
-// buffer -- the layout of the cyclic column kernels (fused_col.hpp).
+// buffer -- the layout of the cyclic column kernels (fused_col.hpp).  Where
+// every rank receives the same result (the Ring, Recursive Halving) a split
+// launch stores it to the root rank b only and broadcast.hip copies it on.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -43,16 +45,17 @@ namespace ar {
 namespace {
 
 // Halving levels f = F, F/2, ..., W: slot y (< f) keeps the pair {y, y|f}.
+// The operand order is a wave-uniform branch, so each level updates its
+// slots in place (a per-pair select had doubled the live registers).
 template <int P, int W, int F, int OP, typename T>
 __device__ __forceinline__ void xor_halving(T (&X)[P], uint32_t b) {
   if constexpr (F >= W && F >= 1) {
-    const bool upper = (b & uint32_t(F)) != 0;  // wave-uniform
+    if (b & uint32_t(F)) {  // the kept operand is slot y|f
 #pragma unroll
-    for (int y = 0; y < F; ++y) {
-      const T lo = X[y], hi = X[y + F];
-      const T own = upper ? hi : lo;
-      const T recv = upper ? lo : hi;
-      X[y] = comb<OP>(own, recv);
+      for (int y = 0; y < F; ++y) X[y] = comb<OP>(X[y + F], X[y]);
+    } else {
+#pragma unroll
+      for (int y = 0; y < F; ++y) X[y] = comb<OP>(X[y], X[y + F]);
     }
     xor_halving<P, W, F / 2, OP, T>(X, b);
   }
@@ -87,17 +90,26 @@ __global__ __launch_bounds__(kBlock) void fused_xor_kernel(const ColArgs a) {
     const int32_t b = int32_t(seg - inst * a.pdiv.d);
     const int64_t len = a.q + (b < a.m ? 1 : 0);
     const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
-    const int64_t lo = ((reinterpret_cast<uintptr_t>(a.user[b]) >> 2) + e0) & (kWave - 1);
+    // The rank table is the same for every tile.  t < 2^31, so tbl is
+    // a.user; indexing by t >> 31 keeps the compiler from hoisting the P
+    // pointer loads out of the loop, which would keep them live across
+    // iterations (spilling SGPRs into VGPRs and costing occupancy).
+    void* const* tbl = a.user + (t >> 31);
+    const int64_t lo = ((reinterpret_cast<uintptr_t>(tbl[b]) >> 2) + e0) & (kWave - 1);
     const int64_t c = int64_t(tile) * kWave - lo + lane;
     if (c >= 0 && c < len) {
       const int64_t e = e0 + c;
       T X[P];
 #pragma unroll
-      for (int y = 0; y < P; ++y) X[y] = ld1<NT>(static_cast<const T*>(a.user[y]) + e);
+      for (int y = 0; y < P; ++y) X[y] = ld1<NT>(static_cast<const T*>(tbl[y]) + e);
       xor_halving<P, W, P / 2, OP, T>(X, uint32_t(b));
       xor_doubling<P, W, W / 2, OP, T>(X);
+      if (W == 1 && a.split) {  // Recursive Halving: one result, rank b holds it first
+        st1<NT>(static_cast<T*>(tbl[b]) + e, X[0]);
+      } else {
 #pragma unroll
-      for (int x = 0; x < P; ++x) st1<NT>(static_cast<T*>(a.user[x]) + e, X[x & (W - 1)]);
+        for (int x = 0; x < P; ++x) st1<NT>(static_cast<T*>(tbl[x]) + e, X[x & (W - 1)]);
+      }
     }
   }
 }
@@ -134,9 +146,13 @@ __global__ __launch_bounds__(kBlock) void fused_ring_kernel(const ColArgs a) {
 #pragma unroll
       for (int d = 1; d <= D; ++d)
         if (d < P) acc = comb<OP>(v[d - 1], acc);
+      if (a.split) {
+        st1<NT>(static_cast<T*>(rot[0]) + e, acc);
+      } else {
 #pragma unroll
-      for (int d = 0; d <= D; ++d)
-        if (d < P) st1<NT>(static_cast<T*>(rot[d]) + e, acc);
+        for (int d = 0; d <= D; ++d)
+          if (d < P) st1<NT>(static_cast<T*>(rot[d]) + e, acc);
+      }
     }
   }
 }
@@ -146,19 +162,19 @@ int launch_ring_nc(const ColArgs& a, int dtype, int op, bool nt, int grid, hipSt
   const dim3 g(grid), blk(kBlock);
   if (dtype == 0) {
     if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 0, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 0, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 0, false>), g, blk, a.lds, s, a);
     } else {
-      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 1, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 1, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<NC, int32_t, 1, false>), g, blk, a.lds, s, a);
     }
   } else {
     if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, float, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_ring_kernel<NC, float, 0, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, float, 0, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<NC, float, 0, false>), g, blk, a.lds, s, a);
     } else {
-      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, float, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_ring_kernel<NC, float, 1, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_ring_kernel<NC, float, 1, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_ring_kernel<NC, float, 1, false>), g, blk, a.lds, s, a);
     }
   }
   return int(hipGetLastError());
@@ -169,19 +185,19 @@ int launch_xor_pr(const ColArgs& a, int dtype, int op, bool nt, int grid, hipStr
   const dim3 g(grid), blk(kBlock);
   if (dtype == 0) {
     if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 0, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 0, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 0, false>), g, blk, a.lds, s, a);
     } else {
-      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 1, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 1, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_xor_kernel<P, R, int32_t, 1, false>), g, blk, a.lds, s, a);
     }
   } else {
     if (op == 0) {
-      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 0, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 0, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 0, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 0, false>), g, blk, a.lds, s, a);
     } else {
-      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 1, true>), g, blk, 0, s, a);
-      else hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 1, false>), g, blk, 0, s, a);
+      if (nt) hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 1, true>), g, blk, a.lds, s, a);
+      else hipLaunchKernelGGL((fused_xor_kernel<P, R, float, 1, false>), g, blk, a.lds, s, a);
     }
   }
   return int(hipGetLastError());

@@ -119,13 +119,13 @@ template <int P, typename T, int OP>
 int launch_fused_p(const FusedArgs& a, int mode, bool nt, int grid, hipStream_t s) {
   const dim3 g(grid), blk(kBlock);
   if (mode == 0) {
-    if (nt) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 0, true>), g, blk, 0, s, a);
-    else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 0, false>), g, blk, 0, s, a);
+    if (nt) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 0, true>), g, blk, a.lds, s, a);
+    else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 0, false>), g, blk, a.lds, s, a);
   } else if (mode == 1) {
-    if (nt) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 1, true>), g, blk, 0, s, a);
-    else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 1, false>), g, blk, 0, s, a);
+    if (nt) hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 1, true>), g, blk, a.lds, s, a);
+    else hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 1, false>), g, blk, a.lds, s, a);
   } else {
-    hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 2, false>), g, blk, 0, s, a);
+    hipLaunchKernelGGL((fused_lo_kernel<P, T, OP, 2, false>), g, blk, a.lds, s, a);
   }
   return int(hipGetLastError());
 }

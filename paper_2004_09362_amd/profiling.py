@@ -27,7 +27,7 @@ import json
 import os
 import sys
 
-from .build import kernel_family, source_hash
+from .build import kernel_families, source_hash
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
@@ -73,7 +73,7 @@ def traffic(a) -> dict:
     ent = {"bytes_per_launch": int(round(b)), "fetch_KiB_raw": round(mean(f), 1), "write_KiB_raw": round(mean(w), 1),
            "fetch_scale": round(sf, 4), "write_scale": round(sw, 4), "launches_counted": len(f),
            "algorithmic_bytes_per_launch": a.alg, "ratio_to_algorithmic": round(b / a.alg, 5) if a.alg else None,
-           "source_hash": source_hash(kernel_family(a.kernel))}
+           "source_hash": source_hash(kernel_families(a.kernel))}
     data = {}
     if os.path.exists(TRAFFIC):
         with open(TRAFFIC) as fh:

@@ -71,9 +71,11 @@ def test_kernel_families_cover_every_source():
     listed = set(b.COMMON) | {f for fam in b.FAMILIES.values() for f in fam}
     have = {os.path.basename(f) for f in b.SOURCES + b.HEADERS if "/csrc/" in f}
     assert have == listed
-    assert {b.kernel_family(k) for k in ("step_kernel<k=10>", "fused_lo_kernel<P=12>", "fused_bo_kernel<P=24>",
-                                         "fused_mid_kernel<P=37>", "fused_xor_kernel<P=32,R=0>",
-                                         "fused_ring_kernel")} == {"step", "lo", "col", "group"}
+    assert {b.kernel_families(k)[0] for k in ("step_kernel<k=10>", "fused_lo_kernel<P=12>", "fused_bo_kernel<P=24>",
+                                              "fused_mid_kernel<P=37>", "fused_xor_kernel<P=32,R=0>",
+                                              "fused_ring_kernel")} == {"step", "lo", "col", "group"}
+    assert b.kernel_families("fused_bo_kernel<P=127>+broadcast") == ["col", "bcast"]
+    assert b.source_hash(["col", "bcast"]) != b.source_hash("col")
 
 
 def test_cpu_baseline_runs_the_oracle_on_a_sample():

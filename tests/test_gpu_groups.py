@@ -218,3 +218,53 @@ def test_ring_gradsync_shape():
     """The gradient-sync shape itself: P = 24, n = 16,777,216 fp32, k = 46."""
     w = synth.WORKLOADS["gradsync"]
     full_size("ring gradsync", 24, w["n"], 46, "cyclic", "ring", w["seed"], w["dist"])
+
+
+# ---------------------------------------------------------------------------
+# Split fused launch (reduce, then broadcast) against the single launch
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("P,k,group,schedule", [(5, 6, "cyclic", "butterfly"), (24, 10, "cyclic", "butterfly"),
+                                                (64, 12, "cyclic", "butterfly"), (127, 14, "cyclic", "butterfly"),
+                                                (8, 6, "xor", "butterfly"), (64, 12, "xor", "butterfly"),
+                                                (7, 12, "cyclic", "ring"), (64, 126, "cyclic", "ring")])
+def test_split_and_single_fused_launch_agree(P, k, group, schedule, monkeypatch):
+    """AR_FUSED_SPLIT forces either form; both must give the oracle's bits,
+    on a ragged batch with gaps between instances."""
+    rng = np.random.default_rng(P * 3 + k)
+    n, B, stride = 5 * P + 3, 3, 5 * P + 11
+    x = rng.normal(size=(P, B, stride)).astype(np.float32)
+    want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, "sum", group=group, schedule=schedule)
+    for split in ("0", "1"):
+        monkeypatch.setenv("AR_FUSED_SPLIT", split)
+        plan = ar.Plan(P, n, "float32", "sum", k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
+        assert plan.stats().fused_launches == (2 if split == "1" else 1)
+        note("split=%s %s/%s P=%d k=%d" % (split, group, schedule, P, k))
+        X = torch.from_numpy(x).to(DEV)
+        plan.batched([X[i] for i in range(P)], B, stride)
+        torch.cuda.synchronize()
+        got = X.cpu().numpy()
+        assert np.array_equal(bits(got[:, :, :n]), bits(want)), split
+        assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), split
+        plan.close()
+
+
+@pytest.mark.parametrize("P,k,group,schedule,B", [(12, 4, "cyclic", "butterfly", 40), (24, 10, "cyclic", "butterfly", 1),
+                                                  (37, 8, "cyclic", "butterfly", 1), (64, 12, "cyclic", "butterfly", 1),
+                                                  (32, 7, "xor", "butterfly", 1), (24, 46, "cyclic", "ring", 1)])
+def test_occupancy_cap_does_not_change_bits(P, k, group, schedule, B, monkeypatch):
+    """AR_FUSED_CAP = 0 (no cap), 1 and 5 resident workgroups per CU: the
+    launch shape changes, the results must not."""
+    rng = np.random.default_rng(P + 17 * k)
+    n = 4 * P + 9 if B > 1 else 3000 + P
+    x = rng.normal(size=(P, B, n)).astype(np.float32)
+    want = oracle.allreduce_batched(x, k, "sum", group=group, schedule=schedule)
+    for cap in ("0", "1", "5"):
+        monkeypatch.setenv("AR_FUSED_CAP", cap)
+        note("cap=%s %s/%s P=%d k=%d" % (cap, group, schedule, P, k))
+        X = torch.from_numpy(x).to(DEV)
+        plan = ar.Plan(P, n, "float32", "sum", k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
+        plan.batched([X[i] for i in range(P)], B, n)
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(X.cpu().numpy()), bits(want)), cap
+        plan.close()

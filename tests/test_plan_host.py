@@ -198,7 +198,10 @@ def test_plan_sizes_match_oracle_counts(P):
         assert st.blocks_pulled_per_rank == sum(tr.pulls[:k])
         assert st.combines_per_rank == sum(tr.combines[:tr.rs_steps])
         assert st.bytes_pulled_total == st.blocks_pulled_per_rank * st.n * 4
-        assert st.hbm_bytes_fused == (2 * P * st.n * 4 if P > 1 else 0)
+        split = st.fused_launches == 2
+        assert st.fused_launches == (0 if P == 1 else 2 if split else 1)
+        assert split == (P >= 48 and k == 2 * ceil_log2(P))
+        assert st.hbm_bytes_fused == ((2 * P + split) * st.n * 4 if P > 1 else 0)
         # per-launch pulls equal the oracle's per-step pulls
         launches = [l for l in plan.launches() if l[0] != 2]
         assert len(launches) == k
