@@ -6,9 +6,10 @@
       of this library only; times in microseconds).
 
   python -m paper_2004_09362_amd.profiling traffic --key KEY --kernel NAME
-          --match SUBSTR --fetch DIR --write DIR --copy-fetch DIR
-          --copy-write DIR --copy-bytes N --alg BYTES
-      HBM bytes per launch of the kernels whose name contains SUBSTR, from a
+          --match SUBSTR [--match SUBSTR2] --fetch DIR --write DIR
+          --copy-fetch DIR --copy-write DIR --copy-bytes N --alg BYTES
+      HBM bytes per launch of the kernels whose name contains SUBSTR (any of
+      the --match strings: a split launch counts its two kernels), from a
       `rocprofv3 --pmc FETCH_SIZE` and a `--pmc WRITE_SIZE` run (counter
       values in KiB per dispatch), each scaled by what the same counter read
       for a plain device copy of N bytes (`bench.py --copy-probe N`), so that
@@ -33,10 +34,11 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic.json")
 
 
-def counter_values(d: str, counter: str, match: str) -> list[float]:
+def counter_values(d: str, counter: str, match) -> list[float]:
+    pats = [match] if isinstance(match, str) else list(match)
     with open(os.path.join(d, "run_counter_collection.csv")) as fh:
         return [float(r["Counter_Value"]) for r in csv.DictReader(fh)
-                if match in r["Kernel_Name"] and r["Counter_Name"] == counter]
+                if any(p in r["Kernel_Name"] for p in pats) and r["Counter_Name"] == counter]
 
 
 def mean(v: list[float]) -> float:
@@ -93,8 +95,9 @@ def main(argv=None):
     s = sub.add_parser("stats")
     s.add_argument("dir")
     t = sub.add_parser("traffic")
-    for name in ("--key", "--kernel", "--match", "--fetch", "--write", "--copy-fetch", "--copy-write"):
+    for name in ("--key", "--kernel", "--fetch", "--write", "--copy-fetch", "--copy-write"):
         t.add_argument(name, required=True)
+    t.add_argument("--match", action="append", required=True)
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--alg", type=int, required=True)
     a = ap.parse_args(argv)
