@@ -78,7 +78,20 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *             block read and written per column, measured faster there.
  *   AUTO:     FUSED where it applies (P >= 2), STEPWISE otherwise.
  * Both paths combine exactly the same operand pairs in the same order, so
- * their results are bit-identical. */
+ * their results are bit-identical.
+ *
+ * Tuning overrides, read from the environment when a plan is created (they
+ * change launch shapes and speed, never results):
+ *   AR_STEP_NT, AR_FUSED_NT = 0|1   nontemporal loads and stores never /
+ *                                   always (default: by bytes per launch);
+ *   AR_FUSED_MODE = 0|1             latency-optimal kernel with P <= 16:
+ *                                   16-byte or 4-byte columns (default 1);
+ *   AR_FUSED_SPLIT = 0|1            single fused launch, or reduce plus
+ *                                   broadcast where every rank receives the
+ *                                   same result (default: split for P >= 48);
+ *   AR_FUSED_CAP = N or N,M         resident workgroups per CU of the fused
+ *                                   launch (and of the broadcast); 0 is no
+ *                                   cap (default: per kernel and P). */
 typedef enum { AR_PATH_AUTO = 0, AR_PATH_STEPWISE = 1, AR_PATH_FUSED = 2 } ar_path;
 
 typedef struct ar_plan ar_plan; /* opaque; owned by the caller between create and destroy */

@@ -62,7 +62,7 @@ struct ar_plan {
   int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1, split_mode = -1;
   bool fused_split = false;
   // Occupancy caps (resident workgroups per CU; 0: none) of the fused launch
-  // and of the broadcast that follows a split one.  AR_FUSED_CAP = N forces N.
+  // and of the broadcast that follows a split one (AR_FUSED_CAP overrides).
   int32_t fused_cap = 0, bcast_cap = 0;
   int32_t path = AR_PATH_AUTO;
   int32_t fused_kind = kFusedNone;
