@@ -101,9 +101,19 @@ def kernel_families(kernel: str) -> list[str]:
     return out
 
 
+def code_text(text: str) -> str:
+    """C++ source without comments and with whitespace collapsed: what the
+    compiler sees, so that editing a comment does not count as a change."""
+    import re
+
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_hash(families) -> str:
-    """Short hash of the sources that make up one kernel family (or a list
-    of families): counter profiles taken on other sources are not reported
+    """Short hash of the code (comments removed) of one kernel family, or a
+    list of families: counter profiles taken on other code are not reported
     as current."""
     import hashlib
 
@@ -111,9 +121,9 @@ def source_hash(families) -> str:
         families = [families]
     h = hashlib.sha256()
     for f in COMMON + [f for fam in families for f in FAMILIES[fam]]:
-        with open(os.path.join(CSRC, f), "rb") as fh:
+        with open(os.path.join(CSRC, f), encoding="utf-8") as fh:
             h.update(f.encode())
-            h.update(fh.read())
+            h.update(code_text(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

@@ -130,3 +130,13 @@ def test_stats_tool_lists_library_kernels(tmp_path):
     out = profiling.stats(str(d))
     assert "`fused_ring_kernel<2, float, 0, true>` | 25 | 536.12 | 527.85 | 546.93 |" in out
     assert "fillBuffer" not in out
+
+
+def test_source_hash_ignores_comments():
+    from paper_2004_09362_amd.build import code_text
+
+    a = "int f(int x) { // add one\n  return x + 1; /* the\n value */ }\n"
+    b = "int f(int x) {\n    return x + 1;  }"
+    c = "int f(int x) { return x + 2; }"
+    assert code_text(a) == code_text(b)
+    assert code_text(a) != code_text(c)
