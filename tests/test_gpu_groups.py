@@ -268,3 +268,32 @@ def test_occupancy_cap_does_not_change_bits(P, k, group, schedule, B, monkeypatc
         torch.cuda.synchronize()
         assert np.array_equal(bits(X.cpu().numpy()), bits(want)), cap
         plan.close()
+
+
+@pytest.mark.parametrize("group,schedule,P", [("xor", "butterfly", 2), ("xor", "butterfly", 8), ("xor", "butterfly", 64),
+                                              ("cyclic", "ring", 2), ("cyclic", "ring", 5), ("cyclic", "ring", 64)])
+def test_degenerate_sizes_other_schedules(group, schedule, P):
+    """n = 0 (nothing touched), n = 1 and n < P (empty blocks), n = P, on
+    every k of the schedule and both paths."""
+    kk = [2 * (P - 1)] if schedule == "ring" else ks(P)
+    for n in (0, 1, P - 1, P):
+        x = np.random.default_rng(n + P).integers(-1000, 1000, size=(P, n)).astype(np.int32)
+        for k in kk:
+            want = oracle.allreduce(x, k, "sum", group=group, schedule=schedule)
+            for path in BOTH:
+                note("degenerate %s/%s P=%d n=%d k=%d path=%d" % (group, schedule, P, n, k, path))
+                X = torch.from_numpy(x).to(DEV)
+                run(P, n, "int32", "sum", k, X, path, group, schedule)
+                assert np.array_equal(X.cpu().numpy(), want), (n, k, path)
+
+
+def test_single_rank_other_schedules():
+    """P = 1: both schedules are the identity (k = 0)."""
+    x = np.arange(17, dtype=np.float32)[None, :]
+    for group, schedule in (("xor", "butterfly"), ("cyclic", "ring")):
+        X = torch.from_numpy(x).to(DEV)
+        plan = ar.Plan(1, 17, "float32", "sum", 0, group=group, schedule=schedule)
+        assert plan.stats().launches == 0 and plan.stats().fused_ok == 0
+        plan([X[0]])
+        torch.cuda.synchronize()
+        assert np.array_equal(X.cpu().numpy(), x)
