@@ -140,3 +140,39 @@ def test_xor_hybrid_costs_no_more_than_cyclic():
             assert x <= c
             if 0 < r < L:
                 assert x < c, (P, k)
+
+
+# ---------------------------------------------------------------------------
+# Randomised: any group, schedule, P, k and ragged n
+# ---------------------------------------------------------------------------
+
+from hypothesis import HealthCheck, given, settings, strategies as st  # noqa: E402
+
+
+@st.composite
+def plan_case(draw):
+    sched = draw(st.sampled_from(["butterfly", "butterfly", "ring"]))
+    if sched == "ring":
+        P = draw(st.integers(1, 40))
+        group, k = "cyclic", 2 * (P - 1)
+    else:
+        group = draw(st.sampled_from(["cyclic", "xor"]))
+        P = draw(st.sampled_from(POW2)) if group == "xor" else draw(st.integers(1, 128))
+        k = draw(st.sampled_from(ks(P)))
+    n = draw(st.integers(0, 3 * P + 7))
+    seed = draw(st.integers(0, 2**31 - 1))
+    return group, sched, P, k, n, seed
+
+
+@settings(max_examples=60, deadline=None, suppress_health_check=[HealthCheck.too_slow])
+@given(plan_case())
+def test_random_plans_reproduce_oracle(case):
+    group, sched, P, k, n, seed = case
+    x = np.random.default_rng(seed).integers(-2**31, 2**31, size=(P, n), dtype=np.int64).astype(np.int32)
+    plan = ar.Plan(P, n, "int32", "sum", k, group=group, schedule=sched)
+    want = oracle.allreduce(x, k, "sum", group=group, schedule=sched)
+    got = interpret(plan, x, "sum", "reverse")
+    assert np.array_equal(got, want), case
+    st_ = plan.stats()
+    assert st_.rs_steps + st_.ag_steps == k
+    assert st_.bytes_pulled_total == st_.blocks_pulled_per_rank * n * 4
