@@ -18,6 +18,7 @@ Workloads (seeded synthetic rank buffers, resident in HBM before timing):
   large                  P = 127, n = 2^26 fp32 N(0,1e-2), --k 14 (default) or 10
   prime3                 P = 3, n = 1024 int32 U[-1000,1000], --k 2..4 (default 4)
   gradsync32             P = 32, n = 2^24 fp32 N(0,1e-3), --k 5..10 (default 10)
+  small_batch127         P = 127, n = 106 fp32 N(0,1), 65536 instances, k = 7
 
 --group xor runs the butterfly schedules over the XOR group (power-of-two P:
 Recursive Halving at k = 2 log2 P, Recursive Doubling at k = log2 P);
@@ -82,6 +83,7 @@ SHAPES = {
     "large": "large: P=127, n=67108864 fp32 N(0,1e-2)",
     "prime3": "prime3: P=3, n=1024 int32 U[-1000,1000]",
     "gradsync32": "gradsync32: P=32, n=16777216 fp32 N(0,1e-3)",
+    "small_batch127": "small_batch127: P=127, n=106 fp32 N(0,1), 65536 instances per launch",
 }
 
 
@@ -199,7 +201,8 @@ def main():
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="small_batch",
-                    choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3", "gradsync32"])
+                    choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3", "gradsync32",
+                             "small_batch127"])
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--group", choices=["cyclic", "xor"], default="cyclic")
     ap.add_argument("--schedule", choices=["butterfly", "ring"], default="butterfly")

@@ -143,6 +143,13 @@ struct ColArgs {
   int32_t P, r;             // r: distribution steps removed (kept shifts w = min(2^r, P))
   int32_t split;            // 1: store the block's result to its root rank only (a broadcast follows)
   uint32_t lds;             // as in FusedArgs
+  // Latency-optimal plans (r = L): the tree of every rank is the same for
+  // every block, so the kernels may tile the batch * n columns as one flat
+  // space (64 per wave, no block index): flat = 1, flat_cols = batch * n
+  // (< 2^32 - 64), ndiv = n.
+  int32_t flat;
+  uint32_t flat_cols;
+  FastDiv ndiv;
 };
 
 // dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.

@@ -282,14 +282,24 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   const int64_t max_len = a.q + (a.m ? 1 : 0);
   // +63: the tile grid of a block is shifted onto 256-byte boundaries
   const int64_t tiles = std::max<int64_t>(1, (max_len + 63 + 63) / 64);
-  const int64_t total = batch * s.P * tiles;
-  if (total >= (int64_t(1) << 31))
-    return fail(AR_ERR_UNSUPPORTED, "the fused kernel would need 2^31 or more tiles; split the batch");
-  a.total_tiles = uint32_t(total);
-  a.tiles = ar::make_fastdiv(uint32_t(tiles));
+  a.tiles = ar::make_fastdiv(uint32_t(std::min<int64_t>(tiles, INT32_MAX)));
   a.pdiv = ar::make_fastdiv(uint32_t(s.P));
+  // Latency-optimal plans: one flat column space (every block has the same
+  // trees), so small instances fill whole waves.
+  const int64_t cols = batch * s.n;
+  if (s.r == s.L && pl->fused_kind != kFusedRing && cols < (int64_t(1) << 32) - 64) {
+    a.flat = 1;
+    a.flat_cols = uint32_t(cols);
+    a.ndiv = ar::make_fastdiv(uint32_t(s.n));
+    a.total_tiles = uint32_t((cols + 63) / 64);
+  } else {
+    const int64_t total = batch * s.P * tiles;
+    if (total >= (int64_t(1) << 31))
+      return fail(AR_ERR_UNSUPPORTED, "the fused kernel would need 2^31 or more tiles; split the batch");
+    a.total_tiles = uint32_t(total);
+  }
   const bool nt = use_nt(pl->fused_nt_mode, int64_t(2) * s.P * s.n * batch * 4, kFusedNtThresholdBytes);
-  const int grid = ar::step_grid(total);
+  const int grid = ar::step_grid(a.total_tiles);
   a.lds = cap_lds(pl->fused_cap, device);
   int e;
   if (pl->fused_kind == kFusedXor) e = ar::launch_fused_xor(a, s.P, pl->dtype, pl->op, nt, grid, stream);

@@ -118,6 +118,11 @@ __global__ __launch_bounds__(kBlock) void fused_bo_kernel(const ColArgs a) {
   }
 }
 
+// With a.flat (latency-optimal plans) the tile loop runs over the flat
+// columns of all instances with b = 0: rank q then stores S[q], the tree
+// rooted at itself, which is the same for every block.  Many small
+// instances (blocks of a few elements, or none) then fill whole waves.
+//
 // fused_mid_kernel: shifted (intermediate) and latency-optimal schedules,
 // 1 <= r <= ceil(log2 P).  For block b the column is V[d] = V_{b+d}[e].  The
 // primed sums R[d] and starred sums S[d] of every offset d follow the
@@ -179,17 +184,29 @@ __global__ __launch_bounds__(kBlock) void fused_mid_kernel(const ColArgs a) {
   const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
        t += gridDim.x * uint32_t(kWavesPerBlock)) {
-    const uint32_t seg = fdiv(t, a.tiles);
-    const uint32_t tile = t - seg * a.tiles.d;
-    const uint32_t inst = fdiv(seg, a.pdiv);
-    const int32_t b = int32_t(seg - inst * a.pdiv.d);
-    const int64_t len = a.q + (b < a.m ? 1 : 0);
-    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+    int32_t b;
+    int64_t e;
+    bool live;
+    if (a.flat) {  // r = L: flat columns, every rank's tree rooted at itself (b = 0)
+      const uint32_t g = t * uint32_t(kWave) + uint32_t(lane);
+      const uint32_t inst = fdiv(g, a.ndiv);
+      b = 0;
+      e = int64_t(inst) * a.stride + int64_t(g - inst * a.ndiv.d);
+      live = g < a.flat_cols;
+    } else {
+      const uint32_t seg = fdiv(t, a.tiles);
+      const uint32_t tile = t - seg * a.tiles.d;
+      const uint32_t inst = fdiv(seg, a.pdiv);
+      b = int32_t(seg - inst * a.pdiv.d);
+      const int64_t len = a.q + (b < a.m ? 1 : 0);
+      const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+      const int64_t lo = ((reinterpret_cast<uintptr_t>(a.user[b]) >> 2) + e0) & (kWave - 1);
+      const int64_t c = int64_t(tile) * kWave - lo + lane;
+      e = e0 + c;
+      live = c >= 0 && c < len;
+    }
     void* const* rot = a.user + b;
-    const int64_t lo = ((reinterpret_cast<uintptr_t>(rot[0]) >> 2) + e0) & (kWave - 1);
-    const int64_t c = int64_t(tile) * kWave - lo + lane;
-    if (c >= 0 && c < len) {
-      const int64_t e = e0 + c;
+    if (live) {
       T R[P], S[P];
 #pragma unroll
       for (int d = 0; d < P; ++d) {

@@ -44,6 +44,12 @@ namespace ar {
 
 namespace {
 
+constexpr int xor_L(int P) {
+  int L = 0;
+  while ((1 << L) < P) ++L;
+  return L;
+}
+
 // Halving levels f = F, F/2, ..., W: slot y (< f) keeps the pair {y, y|f}.
 // The operand order is a wave-uniform branch, so each level updates its
 // slots in place (a per-pair select had doubled the live registers).
@@ -84,21 +90,33 @@ __global__ __launch_bounds__(kBlock) void fused_xor_kernel(const ColArgs a) {
   const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
        t += gridDim.x * uint32_t(kWavesPerBlock)) {
-    const uint32_t seg = fdiv(t, a.tiles);  // seg = instance * P + block
-    const uint32_t tile = t - seg * a.tiles.d;
-    const uint32_t inst = fdiv(seg, a.pdiv);
-    const int32_t b = int32_t(seg - inst * a.pdiv.d);
-    const int64_t len = a.q + (b < a.m ? 1 : 0);
-    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
     // The rank table is the same for every tile.  t < 2^31, so tbl is
     // a.user; indexing by t >> 31 keeps the compiler from hoisting the P
     // pointer loads out of the loop, which would keep them live across
     // iterations (spilling SGPRs into VGPRs and costing occupancy).
     void* const* tbl = a.user + (t >> 31);
-    const int64_t lo = ((reinterpret_cast<uintptr_t>(tbl[b]) >> 2) + e0) & (kWave - 1);
-    const int64_t c = int64_t(tile) * kWave - lo + lane;
-    if (c >= 0 && c < len) {
-      const int64_t e = e0 + c;
+    int32_t b;
+    int64_t e;
+    bool live;
+    if (R == xor_L(P) && a.flat) {  // Recursive Doubling: no block dependence, flat columns
+      const uint32_t g = t * uint32_t(kWave) + uint32_t(lane);
+      const uint32_t inst = fdiv(g, a.ndiv);
+      b = 0;
+      e = int64_t(inst) * a.stride + int64_t(g - inst * a.ndiv.d);
+      live = g < a.flat_cols;
+    } else {
+      const uint32_t seg = fdiv(t, a.tiles);  // seg = instance * P + block
+      const uint32_t tile = t - seg * a.tiles.d;
+      const uint32_t inst = fdiv(seg, a.pdiv);
+      b = int32_t(seg - inst * a.pdiv.d);
+      const int64_t len = a.q + (b < a.m ? 1 : 0);
+      const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+      const int64_t lo = ((reinterpret_cast<uintptr_t>(tbl[b]) >> 2) + e0) & (kWave - 1);
+      const int64_t c = int64_t(tile) * kWave - lo + lane;
+      e = e0 + c;
+      live = c >= 0 && c < len;
+    }
+    if (live) {
       T X[P];
 #pragma unroll
       for (int y = 0; y < P; ++y) X[y] = ld1<NT>(static_cast<const T*>(tbl[y]) + e);

@@ -97,6 +97,9 @@ WORKLOADS = {
                         ks=[6, 7, 8, 9, 10, 11, 12], ops=["sum", "max"], batch=1, seed=BASE_SEED + 3),
     "large": dict(P=[127], n=67108864, dtype=np.float32, dist=Dist("normal", 0.0, 1e-2), ks=[14, 10],
                   ops=["sum"], batch=1, seed=BASE_SEED + 4),
+    # the 425-byte message at the paper's P = 127, many instances per launch
+    "small_batch127": dict(P=[127], n=106, dtype=np.float32, dist=Dist("normal", 0.0, 1.0), ks="lo",
+                           ops=["sum"], batch=65536, seed=BASE_SEED + 6),
     # the gradient-sync shape at a power of two, where the XOR group applies
     "gradsync32": dict(P=[32], n=16777216, dtype=np.float32, dist=Dist("normal", 0.0, 1e-3),
                        ks=[5, 6, 7, 8, 9, 10], ops=["sum"], batch=1, seed=BASE_SEED + 5),

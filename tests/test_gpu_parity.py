@@ -405,3 +405,26 @@ def test_prime_sweep_workload(k, op):
 def test_large_workload(k):
     w = synth.WORKLOADS["large"]
     check_full_size("large", 127, w["n"], k, "sum", w["seed"], w["dist"])
+
+
+@pytest.mark.parametrize("P,group", [(17, "cyclic"), (24, "cyclic"), (37, "cyclic"), (64, "cyclic"), (127, "cyclic"),
+                                     (32, "xor"), (128, "xor")])
+def test_latency_optimal_flat_columns_with_gaps(P, group):
+    """Latency-optimal plans above P = 16 tile the flat columns of all
+    instances (blocks of a 106-element message hold at most one element at
+    P = 127): many small instances with gaps between them, and a ragged n."""
+    L = ceil_log2(P)
+    rng = np.random.default_rng(P * 13)
+    for n, B, stride in ((106, 37, 113), (P + 3, 5, P + 9), (1, 70, 2)):
+        x = rng.normal(size=(P, B, stride)).astype(np.float32)
+        want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), L, "sum", group=group)
+        for path in (ar.AR_PATH_FUSED, ar.AR_PATH_STEPWISE):
+            note("flat LO P=%d %s n=%d B=%d path=%d" % (P, group, n, B, path))
+            X = torch.from_numpy(x).to(DEV)
+            plan = ar.Plan(P, n, "float32", "sum", L, path=path, group=group)
+            plan.batched([X[i] for i in range(P)], B, stride)
+            torch.cuda.synchronize()
+            got = X.cpu().numpy()
+            assert np.array_equal(bits(got[:, :, :n]), bits(want)), (n, path)
+            assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), (n, path)
+            plan.close()
