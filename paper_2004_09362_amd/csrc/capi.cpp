@@ -1,8 +1,9 @@
 // capi.cpp -- the C ABI of libar.so (declared in include/ar.h).
 //
 // Argument checking, workspace management and launch orchestration.  The
-// schedule comes from plan.cpp, the kernels from kernels.hip; nothing here
-// computes on the host.
+// schedule comes from plan.cpp, the kernels from kernels.hip (step),
+// fused_lo.hip, fused_col.hpp / fused_col_g*.hip, fused_group.hip and
+// broadcast.hip; nothing here computes on the host.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -45,10 +46,11 @@ constexpr int32_t kSplitMinP = 48;
 // them; 0 is no cap.
 static int32_t lo_cap(int32_t P) { return P <= 4 ? 0 : P == 6 ? 4 : P <= 7 ? 5 : P <= 11 ? 4 : 3; }
 
-// Which single-launch kernel runs a plan on the FUSED path: the flat
-// latency-optimal kernel (small P; its columns need no block index), the
-// block-tiled column kernels (every other cyclic butterfly plan), or the
-// column kernels of the XOR group and of the Ring.
+// Which kernel runs a plan on the FUSED path: the latency-optimal kernel for
+// P <= 16 (flat columns, no block index), the column kernels of the cyclic
+// butterfly schedules (tiled by block; flat columns when r = L), or the
+// column kernels of the XOR group and of the Ring.  Where every rank
+// receives the same result a broadcast launch may follow (fused_split).
 enum FusedKind { kFusedNone = 0, kFusedLo = 1, kFusedCol = 2, kFusedXor = 3, kFusedRing = 4 };
 
 struct ar_plan {
