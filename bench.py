@@ -282,20 +282,23 @@ def main():
         run_step(s)
     torch.cuda.synchronize()
 
-    # ---- timed region: exactly `steps` steps; HIP events bracket the
-    # dominant job's launch(es) on the launch stream ----
+    # ---- timed region: exactly `steps` steps on the launch stream.  With
+    # several jobs per step, HIP events bracket the dominant job's launch(es)
+    # in every step; with one job, the events around the whole region time it
+    # (no event packets between its back-to-back launches) ----
+    per_launch = len(jobs) > 1
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
     for s in range(steps):
-        run_step(warmup + s, ev[s])
+        run_step(warmup + s, ev[s] if per_launch else None)
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     total_ms = start.elapsed_time(stop)
-    dom_ms = sum(a.elapsed_time(b) for a, b in ev) / steps
+    dom_ms = sum(a.elapsed_time(b) for a, b in ev) / steps if per_launch else total_ms / steps
 
     eff_bytes = sum(j["P"] * j["n"] * j["batch"] * j["dtype"].itemsize for j in jobs)
     ms_per_step = total_ms / steps
@@ -327,7 +330,8 @@ def main():
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": traffic_from_profiles(traffic_key(args.workload, args.group, args.schedule), kname, src_hash),
             "kernel": kname, "job_P": dj["P"], "bytes_per_launch": int(bytes_per_launch),
-            "launch_ms": round(launch_ms, 5), "launches_per_step": launches}
+            "launch_ms": round(launch_ms, 5), "launches_per_step": launches,
+            "timed_by": "HIP events around each launch" if per_launch else "HIP events around the timed region"}
     step_alg = sum(alg_bytes(j, p)[0] for j, p in zip(jobs, plans))
 
     desc = describe(args.workload, jobs, args.group, args.schedule)

@@ -73,7 +73,7 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *             with P <= 16 take a kernel without block tiling (many
  *             independent small instances, Sec. 1's 425-byte average).
  *             Where every rank receives the same result (bandwidth-optimal
- *             plans, the Ring) and P >= 48, the launch stores each block's
+ *             plans, the Ring) and P >= 64, the launch stores each block's
  *             result on one rank and a second launch broadcasts it: one more
  *             block read and written per column, measured faster there.
  *   AUTO:     FUSED where it applies (P >= 2), STEPWISE otherwise.
@@ -88,7 +88,10 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   16-byte or 4-byte columns (default 1);
  *   AR_FUSED_SPLIT = 0|1            single fused launch, or reduce plus
  *                                   broadcast where every rank receives the
- *                                   same result (default: split for P >= 48);
+ *                                   same result (default: split for P >= 64);
+ *   AR_BCAST_NT = 0|1               nontemporal loads and stores in that
+ *                                   broadcast (default: for P >= 96 and
+ *                                   large launches);
  *   AR_FUSED_CAP = N or N,M         resident workgroups per CU of the fused
  *                                   launch (and of the broadcast); 0 is no
  *                                   cap (default: per kernel and P). */
@@ -128,7 +131,7 @@ typedef struct {
   int32_t group, schedule;           /* ar_group and ar_schedule of the plan              */
   int32_t fused_launches;            /* FUSED path: 1, or 2 when split into a reducing
                                         launch and a broadcast (every rank receives the
-                                        same result and P >= 48)                          */
+                                        same result and P >= 64)                          */
 } ar_stats;
 
 /* One launch of the STEPWISE path: a list of placement ranges.  In a range,

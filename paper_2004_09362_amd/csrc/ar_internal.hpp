@@ -172,7 +172,7 @@ int launch_fused_xor(const ColArgs& a, int P, int dtype, int op, bool nt, int gr
 int launch_fused_ring(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream);
 // Second half of a split fused launch (broadcast.hip): block b's result,
 // stored on rank b by the reducing kernel, copied to the other P - 1 ranks.
-int launch_broadcast(const ColArgs& a, int dtype, int grid, void* stream);
+int launch_broadcast(const ColArgs& a, int dtype, bool nt, int grid, void* stream);
 // Workgroups of a step launch over `total_tiles` wave tiles, and the tile size.
 int step_grid(int64_t total_tiles);
 int64_t step_tile_elems();

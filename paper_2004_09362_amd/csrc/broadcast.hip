@@ -28,7 +28,7 @@ namespace ar {
 
 namespace {
 
-template <typename T>
+template <typename T, bool NT>
 __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -46,19 +46,25 @@ __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
     const int64_t c = int64_t(tile) * kWave - lo + lane;
     if (c >= 0 && c < len) {
       const int64_t e = e0 + c;
-      const T v = ld1<false>(static_cast<const T*>(rot[0]) + e);
+      const T v = ld1<NT>(static_cast<const T*>(rot[0]) + e);
 #pragma unroll 8
-      for (int32_t d = 1; d < P; ++d) st1<false>(static_cast<T*>(rot[d]) + e, v);
+      for (int32_t d = 1; d < P; ++d) st1<NT>(static_cast<T*>(rot[d]) + e, v);
     }
   }
 }
 
 }  // namespace
 
-int launch_broadcast(const ColArgs& a, int dtype, int grid, void* stream) {
+int launch_broadcast(const ColArgs& a, int dtype, bool nt, int grid, void* stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (dtype == 0) hipLaunchKernelGGL((broadcast_kernel<int32_t>), dim3(grid), dim3(kBlock), a.lds, s, a);
-  else hipLaunchKernelGGL((broadcast_kernel<float>), dim3(grid), dim3(kBlock), a.lds, s, a);
+  const dim3 g(grid), blk(kBlock);
+  if (dtype == 0) {
+    if (nt) hipLaunchKernelGGL((broadcast_kernel<int32_t, true>), g, blk, a.lds, s, a);
+    else hipLaunchKernelGGL((broadcast_kernel<int32_t, false>), g, blk, a.lds, s, a);
+  } else {
+    if (nt) hipLaunchKernelGGL((broadcast_kernel<float, true>), g, blk, a.lds, s, a);
+    else hipLaunchKernelGGL((broadcast_kernel<float, false>), g, blk, a.lds, s, a);
+  }
   return int(hipGetLastError());
 }
 

@@ -26,8 +26,13 @@ constexpr int64_t kFusedNtThresholdBytes = int64_t(128) << 20;
 // Plans whose ranks all receive the same result (bandwidth-optimal in either
 // group, the Ring) run fused as a reducing launch plus a broadcast from this
 // many ranks up (broadcast.hip): measured faster at P = 64 and 127, slower
-// at P = 24.
-constexpr int32_t kSplitMinP = 48;
+// at P = 24 and 48.
+constexpr int32_t kSplitMinP = 64;
+// From this many ranks up the broadcast streams its P - 1 stores
+// nontemporally (at kFusedNtThresholdBytes and above) with one workgroup per
+// CU: 3-4% faster at P = 100-128 than cached stores at two workgroups per CU,
+// the same at P = 64, and 13% slower at P = 48.  Neither change helps alone.
+constexpr int32_t kBcastStreamMinP = 96;
 
 // Occupancy caps of the fused kernels.  Every fused launch streams P rank
 // buffers in and out at once, and HBM serves that pattern faster when fewer
@@ -41,7 +46,8 @@ constexpr int32_t kSplitMinP = 48;
 //   shifted, P = 37 at 2-3 (2%); at P = 127 its registers already allow only
 //     one wave per SIMD, and a cap changes nothing;
 //   the Ring at P = 24: 4 (2%);
-//   split launches (P = 127): the reducing launch at 3-6, the broadcast at 2.
+//   split launches (P = 127): the reducing launch at 3-6, the broadcast at 2
+//     (1 with nontemporal stores, from kBcastStreamMinP ranks up).
 // AR_FUSED_CAP = N (both launches) or N,M (fused launch, broadcast) overrides
 // them; 0 is no cap.
 static int32_t lo_cap(int32_t P) { return P <= 4 ? 0 : P == 6 ? 4 : P <= 7 ? 5 : P <= 11 ? 4 : 3; }
@@ -60,8 +66,9 @@ struct ar_plan {
   // AR_STEP_NT / AR_FUSED_NT = 0|1 (nontemporal never / always; default by
   // launch size), AR_FUSED_MODE = 0|1 (16-byte or 4-byte columns),
   // AR_FUSED_SPLIT = 0|1 (single fused launch / reduce plus broadcast, where
-  // every rank receives the same result; default by P).
-  int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1, split_mode = -1;
+  // every rank receives the same result; default by P), AR_BCAST_NT = 0|1
+  // (the broadcast's loads and stores; default by P and launch size).
+  int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1, split_mode = -1, bcast_nt_mode = -1;
   bool fused_split = false;
   // Occupancy caps (resident workgroups per CU; 0: none) of the fused launch
   // and of the broadcast that follows a split one (AR_FUSED_CAP overrides).
@@ -310,7 +317,10 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");
   if (pl->fused_split) {
     a.lds = cap_lds(pl->bcast_cap, device);
-    e = ar::launch_broadcast(a, pl->dtype, grid, stream);
+    const bool bnt = pl->bcast_nt_mode == 1 ||
+                     (pl->bcast_nt_mode < 0 && s.P >= kBcastStreamMinP &&
+                      int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes);
+    e = ar::launch_broadcast(a, pl->dtype, bnt, grid, stream);
     if (e != 0) return hip_fail(hipError_t(e), "broadcast kernel launch");
   }
   return AR_OK;
@@ -346,6 +356,7 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
   pl->fused_nt_mode = env_mode("AR_FUSED_NT");
   pl->fused_mode = env_mode("AR_FUSED_MODE");
   pl->split_mode = env_mode("AR_FUSED_SPLIT");
+  pl->bcast_nt_mode = env_mode("AR_BCAST_NT");
   if (pl->s.P < 2) pl->fused_kind = kFusedNone;
   else if (pl->s.sched == ar::kSchedRing) pl->fused_kind = kFusedRing;
   else if (pl->s.group == ar::kGroupXor) pl->fused_kind = kFusedXor;
@@ -363,7 +374,7 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
     else if (pl->fused_kind == kFusedRing) pl->fused_cap = 4;
     else if (pl->s.r == 0) pl->fused_cap = P <= 32 ? 4 : 3;
     else pl->fused_cap = P >= 64 ? 0 : 3;
-    pl->bcast_cap = 2;
+    pl->bcast_cap = P >= kBcastStreamMinP ? 1 : 2;
     // AR_FUSED_CAP = N caps both launches, "N,M" the fused one and the broadcast
     const char* ce = std::getenv("AR_FUSED_CAP");
     if (ce != nullptr && ce[0] >= '0' && ce[0] <= '9') {

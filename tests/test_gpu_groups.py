@@ -229,17 +229,19 @@ def test_ring_gradsync_shape():
                                                 (8, 6, "xor", "butterfly"), (64, 12, "xor", "butterfly"),
                                                 (7, 12, "cyclic", "ring"), (64, 126, "cyclic", "ring")])
 def test_split_and_single_fused_launch_agree(P, k, group, schedule, monkeypatch):
-    """AR_FUSED_SPLIT forces either form; both must give the oracle's bits,
-    on a ragged batch with gaps between instances."""
+    """AR_FUSED_SPLIT forces either form, and AR_BCAST_NT either kind of
+    broadcast store; all must give the oracle's bits, on a ragged batch with
+    gaps between instances."""
     rng = np.random.default_rng(P * 3 + k)
     n, B, stride = 5 * P + 3, 3, 5 * P + 11
     x = rng.normal(size=(P, B, stride)).astype(np.float32)
     want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, "sum", group=group, schedule=schedule)
-    for split in ("0", "1"):
+    for split, bnt in (("0", "0"), ("1", "0"), ("1", "1")):
         monkeypatch.setenv("AR_FUSED_SPLIT", split)
+        monkeypatch.setenv("AR_BCAST_NT", bnt)
         plan = ar.Plan(P, n, "float32", "sum", k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
         assert plan.stats().fused_launches == (2 if split == "1" else 1)
-        note("split=%s %s/%s P=%d k=%d" % (split, group, schedule, P, k))
+        note("split=%s broadcast nt=%s %s/%s P=%d k=%d" % (split, bnt, group, schedule, P, k))
         X = torch.from_numpy(x).to(DEV)
         plan.batched([X[i] for i in range(P)], B, stride)
         torch.cuda.synchronize()
