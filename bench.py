@@ -175,6 +175,53 @@ def cpu_baseline(jobs, host_sets, budget_s=12.0, group="cyclic", schedule="butte
             "sample": "; ".join(parts) + " (single-threaded C replay, %.1f s)" % total_t}
 
 
+class HipEvent:
+    """A timing event of the HIP runtime torch runs on, created with
+    hipEventDisableSystemFence: recording it then skips the system-scope
+    cache writeback and invalidation that a default event performs, which
+    HIP documents as the way to time device work accurately (a default event
+    added about 2 us to a 109 us launch here, and slowed the work after it)."""
+
+    _hip = None
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    @classmethod
+    def runtime(cls):
+        import ctypes
+
+        if cls._hip is None:
+            paths = sorted({ln.split()[-1] for ln in open("/proc/self/maps") if "libamdhip64" in ln})
+            if not paths:
+                raise RuntimeError("the HIP runtime is not loaded in this process")
+            cls._hip = ctypes.CDLL(paths[0])  # the library torch loaded (same handle)
+        return cls._hip
+
+    def __init__(self):
+        import ctypes
+
+        self._ct = ctypes
+        self.h = ctypes.c_void_p()
+        e = self.runtime().hipEventCreateWithFlags(ctypes.byref(self.h), ctypes.c_uint(self.DISABLE_SYSTEM_FENCE))
+        if e != 0:
+            raise RuntimeError("hipEventCreateWithFlags failed (%d)" % e)
+
+    def record(self, stream):
+        e = self.runtime().hipEventRecord(self.h, self._ct.c_void_p(stream.cuda_stream))
+        if e != 0:
+            raise RuntimeError("hipEventRecord failed (%d)" % e)
+
+    def elapsed_time(self, end):
+        ms = self._ct.c_float()
+        e = self.runtime().hipEventElapsedTime(self._ct.byref(ms), self.h, end.h)
+        if e != 0:
+            raise RuntimeError("hipEventElapsedTime failed (%d)" % e)
+        return ms.value
+
+    def __del__(self):
+        if self._hip is not None and self.h:
+            self._hip.hipEventDestroy(self.h)
+
+
 def copy_probe(nbytes, reps):
     """A plain copy kernel of known size: reads and writes nbytes per launch.
     Its FETCH_SIZE / WRITE_SIZE readings calibrate the HBM counters."""
@@ -285,10 +332,11 @@ def main():
     # ---- timed region: exactly `steps` steps on the launch stream.  With
     # several jobs per step, HIP events bracket the dominant job's launch(es)
     # in every step; with one job, the events around the whole region time it
-    # (no event packets between its back-to-back launches) ----
+    # (no event packets between its back-to-back launches).  The events carry
+    # no system-scope fence (HipEvent) ----
     per_launch = len(jobs) > 1
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ev = [(HipEvent(), HipEvent()) for _ in range(steps)] if per_launch else []
+    start, stop = HipEvent(), HipEvent()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
