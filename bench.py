@@ -14,7 +14,8 @@ Workloads (seeded synthetic rank buffers, resident in HBM before timing):
                          425-byte average message the paper quotes), 65536
                          instances per launch, latency-optimal k = ceil(log2 P)
   gradsync               P = 24, n = 2^24 fp32 N(0,1e-3), k = 10
-  prime_sweep            P = 37, n = 2^22 fp32 U(-1,1), --k in 6..12 (default 12)
+  prime_sweep            P = 37, n = 2^22 fp32 U(-1,1), --k in 6..12 (default 12),
+                         --op sum (default) or max
   large                  P = 127, n = 2^26 fp32 N(0,1e-2), --k 14 (default) or 10
   prime3                 P = 3, n = 1024 int32 U[-1000,1000], --k 2..4 (default 4)
   gradsync32             P = 32, n = 2^24 fp32 N(0,1e-3), --k 5..10 (default 10)
@@ -52,11 +53,13 @@ def ceil_log2(P):
     return max(0, (P - 1).bit_length())
 
 
-def jobs_for(name, k_arg, group="cyclic", schedule="butterfly"):
+def jobs_for(name, k_arg, group="cyclic", schedule="butterfly", op=None):
     from paper_2004_09362_amd import synth
     import numpy as np
 
     w = synth.WORKLOADS[name]
+    if op is not None and op not in w["ops"]:
+        raise SystemExit("op %s is not one of the %s workload's ops %s" % (op, name, w["ops"]))
     jobs = []
     for P in w["P"]:
         if group == "xor" and P & (P - 1):
@@ -69,7 +72,7 @@ def jobs_for(name, k_arg, group="cyclic", schedule="butterfly"):
             k = k_arg if k_arg is not None else DEFAULT_K[name]
             if k not in w["ks"]:
                 raise SystemExit("k=%d is not one of the %s workload's k values %s" % (k, name, w["ks"]))
-        jobs.append(dict(P=P, n=w["n"], batch=w["batch"], k=k, op=w["ops"][0],
+        jobs.append(dict(P=P, n=w["n"], batch=w["batch"], k=k, op=op or w["ops"][0],
                          dtype=np.dtype(w["dtype"]), dist=w["dist"], seed=w["seed"]))
     return w, jobs
 
@@ -251,6 +254,8 @@ def main():
                     choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3", "gradsync32",
                              "small_batch127"])
     ap.add_argument("--k", type=int, default=None)
+    ap.add_argument("--op", choices=["sum", "max"], default=None,
+                    help="the reduction (default: the workload's first; prime_sweep also runs max)")
     ap.add_argument("--group", choices=["cyclic", "xor"], default="cyclic")
     ap.add_argument("--schedule", choices=["butterfly", "ring"], default="butterfly")
     ap.add_argument("--path", choices=["auto", "stepwise", "fused"], default="auto")
@@ -280,7 +285,7 @@ def main():
     torch.cuda.set_device(dev)
     if args.schedule == "ring" and args.group != "cyclic":
         raise SystemExit("the Ring runs over the cyclic group")
-    w, jobs = jobs_for(args.workload, args.k, args.group, args.schedule)
+    w, jobs = jobs_for(args.workload, args.k, args.group, args.schedule, args.op)
     path = {"auto": ar.AR_PATH_AUTO, "stepwise": ar.AR_PATH_STEPWISE, "fused": ar.AR_PATH_FUSED}[args.path]
 
     # ---- plans and resident inputs ----

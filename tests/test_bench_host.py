@@ -49,6 +49,10 @@ def test_jobs_reject_bad_requests():
         bench.jobs_for("gradsync", None, "xor", "butterfly")     # P = 24 is not a power of two
     with pytest.raises(SystemExit):
         bench.jobs_for("prime_sweep", 13, "cyclic", "butterfly")  # k outside the workload's values
+    with pytest.raises(SystemExit):
+        bench.jobs_for("gradsync", None, "cyclic", "butterfly", "max")  # gradsync sums only
+    _, jobs = bench.jobs_for("prime_sweep", 9, "cyclic", "butterfly", "max")
+    assert [(j["P"], j["k"], j["op"]) for j in jobs] == [(37, 9, "max")]
 
 
 def test_traffic_lookup_checks_the_source_hash(tmp_path, monkeypatch):
