@@ -92,6 +92,12 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *   AR_BCAST_NT = 0|1               nontemporal loads and stores in that
  *                                   broadcast (default: for P >= 96 and
  *                                   large launches);
+ *   AR_FUSED_PACKED = 0|1           column launches other than the latency-
+ *                                   optimal ones: a wave takes 64 columns of
+ *                                   one block of one instance, or one block
+ *                                   of several instances when blocks hold at
+ *                                   most 64 elements (default: the latter
+ *                                   for batches with blocks that short);
  *   AR_FUSED_CAP = N or N,M         resident workgroups per CU of the fused
  *                                   launch (and of the broadcast); 0 is no
  *                                   cap (default: per kernel and P). */

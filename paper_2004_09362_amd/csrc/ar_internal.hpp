@@ -150,6 +150,14 @@ struct ColArgs {
   int32_t flat;
   uint32_t flat_cols;
   FastDiv ndiv;
+  // Short blocks (every other plan): with packed = 1 a wave tile covers the
+  // same block of ipw instances, lane = j * maxlen + c for column c of
+  // instance j of the tile's group; lendiv = maxlen (the longest block),
+  // ipw = 64 / maxlen, batch = the number of instances.  Otherwise a tile
+  // covers 64 columns of one block of one instance.
+  int32_t packed;
+  uint32_t ipw, batch;
+  FastDiv lendiv;
 };
 
 // dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.

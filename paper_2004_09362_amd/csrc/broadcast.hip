@@ -13,10 +13,13 @@
 // launch (probes: reducing 6.4 TB/s, broadcasting 5.3 TB/s, fused 5.35
 // TB/s).
 //
-// Layout and tiles as in fused_col.hpp: one wave per 64 columns of one
-// block of one instance, tiles laid on 256-byte boundaries of rank b's
-// buffer, ordinary (cached) stores, which streamed faster here than
-// nontemporal ones.
+// Layout and tiles as in the reducing launch (col_tile_column,
+// device_common.hpp): one wave per 64 columns of one block of one instance,
+// tiles laid on 256-byte boundaries of rank b's buffer, or one short block
+// of several instances per wave.  Loads and stores are nontemporal (NT) or
+// ordinary: from P = 96 ranks, streaming the P - 1 stores nontemporally at
+// one resident workgroup per CU was 3-4% faster; below, ordinary stores
+// streamed as fast or faster.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -35,17 +38,11 @@ __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
   const int32_t P = a.P;
   for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
        t += gridDim.x * uint32_t(kWavesPerBlock)) {
-    const uint32_t seg = fdiv(t, a.tiles);  // seg = instance * P + block
-    const uint32_t tile = t - seg * a.tiles.d;
-    const uint32_t inst = fdiv(seg, a.pdiv);
-    const int32_t b = int32_t(seg - inst * a.pdiv.d);
-    const int64_t len = a.q + (b < a.m ? 1 : 0);
-    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+    int32_t b;
+    int64_t e;
+    const bool live = col_tile_column(a, t, lane, b, e);
     void* const* rot = a.user + b;  // rot[d] is rank (b + d) mod P
-    const int64_t lo = ((reinterpret_cast<uintptr_t>(rot[0]) >> 2) + e0) & (kWave - 1);
-    const int64_t c = int64_t(tile) * kWave - lo + lane;
-    if (c >= 0 && c < len) {
-      const int64_t e = e0 + c;
+    if (live) {
       const T v = ld1<NT>(static_cast<const T*>(rot[0]) + e);
 #pragma unroll 8
       for (int32_t d = 1; d < P; ++d) st1<NT>(static_cast<T*>(rot[d]) + e, v);

@@ -7,6 +7,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdint>
 #include <cstdio>
@@ -33,6 +34,14 @@ constexpr int32_t kSplitMinP = 64;
 // CU: 3-4% faster at P = 100-128 than cached stores at two workgroups per CU,
 // the same at P = 64, and 13% slower at P = 48.  Neither change helps alone.
 constexpr int32_t kBcastStreamMinP = 96;
+// Blocks of at most this many elements (many small instances) are packed:
+// a column-fused wave takes one block of 64 / max_len instances instead of 64
+// columns of one block of one instance, laid on 256-byte boundaries (which
+// split a short block over two waves).  Measured against blocked tiles:
+// 1.5-1.9x at P = 127 and 12 with blocks of 8-19 elements, 1.3x with
+// blocks of 33, 1.6x for the Ring at P = 24; within 4% of them for
+// bandwidth-optimal P = 24 and shifted P = 37 with blocks of 4-9.
+constexpr int64_t kPackMaxLen = 64;
 
 // Occupancy caps of the fused kernels.  Every fused launch streams P rank
 // buffers in and out at once, and HBM serves that pattern faster when fewer
@@ -67,8 +76,12 @@ struct ar_plan {
   // launch size), AR_FUSED_MODE = 0|1 (16-byte or 4-byte columns),
   // AR_FUSED_SPLIT = 0|1 (single fused launch / reduce plus broadcast, where
   // every rank receives the same result; default by P), AR_BCAST_NT = 0|1
-  // (the broadcast's loads and stores; default by P and launch size).
+  // (the broadcast's loads and stores; default by P and launch size),
+  // AR_FUSED_PACKED = 0|1 (column tiles of one block of one instance / of
+  // several instances, for blocks of up to 64 elements; default: packed for
+  // batches whose blocks hold up to kPackMaxLen elements).
   int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1, split_mode = -1, bcast_nt_mode = -1;
+  int32_t packed_mode = -1;
   bool fused_split = false;
   // Occupancy caps (resident workgroups per CU; 0: none) of the fused launch
   // and of the broadcast that follows a split one (AR_FUSED_CAP overrides).
@@ -171,24 +184,31 @@ ar_status ensure_scratch(ar_plan* pl, size_t need, int device) {
 }
 
 // LDS a workgroup reserves so that at most `cap` workgroups fit on a CU of
-// `device` (0 for no cap).  Cached per device.
+// `device` (0 for no cap, or when the device allows no such reservation).
+// The device's LDS sizes are cached per device; threads that query the same
+// device at once store the same values.
 uint32_t cap_lds(int32_t cap, int device) {
-  static int64_t per_cu[64] = {}, per_block[64] = {};
+  static std::atomic<int64_t> per_cu[64], per_block[64];
   if (cap <= 0 || device < 0 || device >= 64) return 0;
-  if (per_cu[device] == 0) {
+  int64_t cu = per_cu[device].load(std::memory_order_acquire);
+  int64_t blk = per_block[device].load(std::memory_order_acquire);
+  if (cu == 0 || blk == 0) {
     int a = 0, b = 0;
     if (hipDeviceGetAttribute(&a, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, device) != hipSuccess ||
         hipDeviceGetAttribute(&b, hipDeviceAttributeMaxSharedMemoryPerBlock, device) != hipSuccess) {
       (void)hipGetLastError();
       return 0;
     }
-    per_cu[device] = a;
-    per_block[device] = b;
+    cu = a;
+    blk = b;
+    per_block[device].store(blk, std::memory_order_release);
+    per_cu[device].store(cu, std::memory_order_release);
   }
-  // cap workgroups fit, cap + 1 do not (1 KB margin, 512-byte allocation steps)
-  int64_t bytes = (per_cu[device] / cap - 1024) / 512 * 512;
-  if (bytes <= 0 || per_cu[device] / (cap + 1) >= bytes) return 0;
-  return uint32_t(std::min(bytes, per_block[device]));
+  // cap workgroups fit, cap + 1 do not (1 KB margin, 512-byte allocation
+  // steps); a reservation above the per-workgroup limit cannot enforce it
+  const int64_t bytes = (cu / cap - 1024) / 512 * 512;
+  if (bytes <= 0 || cu / (cap + 1) >= bytes || bytes > blk) return 0;
+  return uint32_t(bytes);
 }
 
 bool use_nt(int32_t mode, int64_t bytes, int64_t threshold = kNtThresholdBytes) {
@@ -301,6 +321,18 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
     a.flat_cols = uint32_t(cols);
     a.ndiv = ar::make_fastdiv(uint32_t(s.n));
     a.total_tiles = uint32_t((cols + 63) / 64);
+  } else if (max_len >= 1 && batch < INT32_MAX &&
+             (pl->packed_mode == 1 ? max_len <= int64_t(64)
+                                   : pl->packed_mode < 0 && batch > 1 && max_len <= kPackMaxLen)) {
+    // Short blocks: one block of 64 / max_len instances per wave tile.
+    a.packed = 1;
+    a.ipw = uint32_t(64 / max_len);
+    a.batch = uint32_t(batch);
+    a.lendiv = ar::make_fastdiv(uint32_t(max_len));
+    const int64_t total = (batch + a.ipw - 1) / a.ipw * s.P;
+    if (total >= (int64_t(1) << 31))
+      return fail(AR_ERR_UNSUPPORTED, "the fused kernel would need 2^31 or more tiles; split the batch");
+    a.total_tiles = uint32_t(total);
   } else {
     const int64_t total = batch * s.P * tiles;
     if (total >= (int64_t(1) << 31))
@@ -357,6 +389,7 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
   pl->fused_mode = env_mode("AR_FUSED_MODE");
   pl->split_mode = env_mode("AR_FUSED_SPLIT");
   pl->bcast_nt_mode = env_mode("AR_BCAST_NT");
+  pl->packed_mode = env_mode("AR_FUSED_PACKED");
   if (pl->s.P < 2) pl->fused_kind = kFusedNone;
   else if (pl->s.sched == ar::kSchedRing) pl->fused_kind = kFusedRing;
   else if (pl->s.group == ar::kGroupXor) pl->fused_kind = kFusedXor;

@@ -94,4 +94,39 @@ __device__ __forceinline__ uint32_t fdiv(uint32_t n, const FastDiv& f) {
   return (t + ((n - t) >> 1)) >> (f.l - 1);
 }
 
+// The column that one lane of wave tile t works on in a block-tiled column
+// launch: sets the block b (the same for the whole wave, so the rank
+// rotation and its pointers stay uniform) and the element index e of the
+// column in every rank buffer; returns whether the lane holds a column.
+//
+// Blocked tiles (a.packed = 0): t = (instance * P + block) * tiles + tile,
+// 64 columns of one block per tile, the tiles of a block laid on 256-byte
+// boundaries of its root rank's buffer (its first and last tile partial).
+// Packed tiles (a.packed = 1, blocks of at most 64 elements): t = group * P
+// + block, and the tile covers that block in a.ipw consecutive instances,
+// lane j * maxlen + c holding column c of instance group * ipw + j, so short
+// blocks fill the wave; the four waves of a workgroup take neighbouring
+// blocks of the same instances.
+__device__ __forceinline__ bool col_tile_column(const ColArgs& a, uint32_t t, int lane, int32_t& b, int64_t& e) {
+  if (a.packed) {
+    const uint32_t g = fdiv(t, a.pdiv);
+    b = int32_t(t - g * a.pdiv.d);
+    const uint32_t j = fdiv(uint32_t(lane), a.lendiv);
+    const int64_t c = int64_t(lane) - int64_t(j) * a.lendiv.d;
+    const uint32_t inst = g * a.ipw + j;
+    e = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m) + c;
+    return j < a.ipw && inst < a.batch && c < a.q + (b < a.m ? 1 : 0);
+  }
+  const uint32_t seg = fdiv(t, a.tiles);  // seg = instance * P + block
+  const uint32_t tile = t - seg * a.tiles.d;
+  const uint32_t inst = fdiv(seg, a.pdiv);
+  b = int32_t(seg - inst * a.pdiv.d);
+  const int64_t len = a.q + (b < a.m ? 1 : 0);
+  const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+  const int64_t lo = ((reinterpret_cast<uintptr_t>(a.user[b]) >> 2) + e0) & (kWave - 1);
+  const int64_t c = int64_t(tile) * kWave - lo + lane;
+  e = e0 + c;
+  return c >= 0 && c < len;
+}
+
 }  // namespace ar

@@ -27,8 +27,11 @@
 // the tiles of a block are laid on 256-byte boundaries of the buffer (the
 // first and last tile of a block are partial): rows that straddled cache
 // lines cost a third more line transfers, and much more when streamed
-// nontemporally.  P is a template parameter so that W stays in registers
-// with static indices.
+// nontemporally.  Blocks of at most 64 elements (many small instances) are
+// packed instead: a wave takes the same block of several instances, so the
+// rotation stays uniform while the lanes fill (col_tile_column in
+// device_common.hpp).  P is a template parameter so that W stays in
+// registers with static indices.
 #pragma once
 
 #include <type_traits>
@@ -92,18 +95,11 @@ __global__ __launch_bounds__(kBlock) void fused_bo_kernel(const ColArgs a) {
   const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
        t += gridDim.x * uint32_t(kWavesPerBlock)) {
-    const uint32_t seg = fdiv(t, a.tiles);  // seg = instance * P + block
-    const uint32_t tile = t - seg * a.tiles.d;
-    const uint32_t inst = fdiv(seg, a.pdiv);
-    const int32_t b = int32_t(seg - inst * a.pdiv.d);
-    const int64_t len = a.q + (b < a.m ? 1 : 0);
-    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+    int32_t b;
+    int64_t e;
+    const bool live = col_tile_column(a, t, lane, b, e);
     void* const* rot = a.user + b;  // rot[d] is rank (b + d) mod P
-    // columns before the first 256-byte boundary of the root rank's row
-    const int64_t lo = ((reinterpret_cast<uintptr_t>(rot[0]) >> 2) + e0) & (kWave - 1);
-    const int64_t c = int64_t(tile) * kWave - lo + lane;
-    if (c >= 0 && c < len) {
-      const int64_t e = e0 + c;
+    if (live) {
       T w[P];
 #pragma unroll
       for (int d = 0; d < P; ++d) w[d] = ld1<NT>(static_cast<const T*>(rot[d]) + e);
@@ -194,16 +190,7 @@ __global__ __launch_bounds__(kBlock) void fused_mid_kernel(const ColArgs a) {
       e = int64_t(inst) * a.stride + int64_t(g - inst * a.ndiv.d);
       live = g < a.flat_cols;
     } else {
-      const uint32_t seg = fdiv(t, a.tiles);
-      const uint32_t tile = t - seg * a.tiles.d;
-      const uint32_t inst = fdiv(seg, a.pdiv);
-      b = int32_t(seg - inst * a.pdiv.d);
-      const int64_t len = a.q + (b < a.m ? 1 : 0);
-      const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
-      const int64_t lo = ((reinterpret_cast<uintptr_t>(a.user[b]) >> 2) + e0) & (kWave - 1);
-      const int64_t c = int64_t(tile) * kWave - lo + lane;
-      e = e0 + c;
-      live = c >= 0 && c < len;
+      live = col_tile_column(a, t, lane, b, e);
     }
     void* const* rot = a.user + b;
     if (live) {

@@ -30,7 +30,8 @@
 // Both read every input once and write every output once (2 * P * n
 // elements), one 4-byte element per lane, 64 consecutive columns of one
 // block per wave, tiles laid on 256-byte boundaries of the block's root rank
-// buffer -- the layout of the cyclic column kernels (fused_col.hpp).  Where
+// buffer, or one short block of several instances per wave -- the tiling of
+// the cyclic column kernels (col_tile_column, device_common.hpp).  Where
 // every rank receives the same result (the Ring, Recursive Halving) a split
 // launch stores it to the root rank b only and broadcast.hip copies it on.
 #include <hip/hip_runtime.h>
@@ -105,16 +106,7 @@ __global__ __launch_bounds__(kBlock) void fused_xor_kernel(const ColArgs a) {
       e = int64_t(inst) * a.stride + int64_t(g - inst * a.ndiv.d);
       live = g < a.flat_cols;
     } else {
-      const uint32_t seg = fdiv(t, a.tiles);  // seg = instance * P + block
-      const uint32_t tile = t - seg * a.tiles.d;
-      const uint32_t inst = fdiv(seg, a.pdiv);
-      b = int32_t(seg - inst * a.pdiv.d);
-      const int64_t len = a.q + (b < a.m ? 1 : 0);
-      const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
-      const int64_t lo = ((reinterpret_cast<uintptr_t>(tbl[b]) >> 2) + e0) & (kWave - 1);
-      const int64_t c = int64_t(tile) * kWave - lo + lane;
-      e = e0 + c;
-      live = c >= 0 && c < len;
+      live = col_tile_column(a, t, lane, b, e);
     }
     if (live) {
       T X[P];
@@ -145,17 +137,11 @@ __global__ __launch_bounds__(kBlock) void fused_ring_kernel(const ColArgs a) {
   const int32_t P = a.P;
   for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
        t += gridDim.x * uint32_t(kWavesPerBlock)) {
-    const uint32_t seg = fdiv(t, a.tiles);
-    const uint32_t tile = t - seg * a.tiles.d;
-    const uint32_t inst = fdiv(seg, a.pdiv);
-    const int32_t b = int32_t(seg - inst * a.pdiv.d);
-    const int64_t len = a.q + (b < a.m ? 1 : 0);
-    const int64_t e0 = int64_t(inst) * a.stride + int64_t(b) * a.q + (b < a.m ? b : a.m);
+    int32_t b;
+    int64_t e;
+    const bool live = col_tile_column(a, t, lane, b, e);
     void* const* rot = a.user + b;  // rot[d] is rank (b + d) mod P
-    const int64_t lo = ((reinterpret_cast<uintptr_t>(rot[0]) >> 2) + e0) & (kWave - 1);
-    const int64_t c = int64_t(tile) * kWave - lo + lane;
-    if (c >= 0 && c < len) {
-      const int64_t e = e0 + c;
+    if (live) {
       T acc = ld1<NT>(static_cast<const T*>(rot[0]) + e);
       T v[D];
 #pragma unroll

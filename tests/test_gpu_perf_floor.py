@@ -49,6 +49,8 @@ def achieved(P, n, B, k, group, schedule, reps=10):
     ("XOR Recursive Halving P=128, split", 128, 1 << 23, 1, 14, "xor", "butterfly", 0.50),
     ("XOR hybrid P=128", 128, 1 << 23, 1, 10, "xor", "butterfly", 0.50),
     ("Ring P=24", 24, 1 << 23, 1, 46, "cyclic", "ring", 0.55),
+    # packed tiles: 8192 messages of 9 KB at P = 127, k = 11 (blocks of 18 elements); measured 23%
+    ("shifted P=127, 8192 x 2304, packed", 127, 2304, 8192, 11, "cyclic", "butterfly", 0.15),
 ])
 def test_fused_kernels_stay_near_their_roofline(name, P, n, B, k, group, schedule, floor):
     if not torch.cuda.is_available():
