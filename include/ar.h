@@ -72,10 +72,17 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *             XOR group and the Ring's chain; latency-optimal cyclic plans
  *             with P <= 16 take a kernel without block tiling (many
  *             independent small instances, Sec. 1's 425-byte average).
- *             Where every rank receives the same result (bandwidth-optimal
- *             plans, the Ring) and P >= 64, the launch stores each block's
- *             result on one rank and a second launch broadcasts it: one more
- *             block read and written per column, measured faster there.
+ *             Sums whose blocks hold at most 64 elements (many small
+ *             instances) run on flat columns, every rank's row loaded whole:
+ *             cyclic plans with r < L and the Ring rotate each lane's column
+ *             by its block before the same fold, recursion or chain; the
+ *             XOR group's plans leave the block out (it only orders the
+ *             operands of a halving pair, which a sum does not see).
+ *             Otherwise, where every rank receives the same result
+ *             (bandwidth-optimal plans, the Ring) and P >= 64, the launch
+ *             stores each block's result on one rank and a second launch
+ *             broadcasts it: one more block read and written per column,
+ *             measured faster there.
  *   AUTO:     FUSED where it applies (P >= 2), STEPWISE otherwise.
  * Both paths combine exactly the same operand pairs in the same order, so
  * their results are bit-identical.
@@ -86,9 +93,10 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   always (default: by bytes per launch);
  *   AR_FUSED_MODE = 0|1             latency-optimal kernel with P <= 16:
  *                                   16-byte or 4-byte columns (default 1);
- *   AR_FUSED_SPLIT = 0|1            single fused launch, or reduce plus
- *                                   broadcast where every rank receives the
- *                                   same result (default: split for P >= 64);
+ *   AR_FUSED_SPLIT = 0|1            block-tiled launches: single fused
+ *                                   launch, or reduce plus broadcast where
+ *                                   every rank receives the same result
+ *                                   (default: split for P >= 64);
  *   AR_BCAST_NT = 0|1               nontemporal loads and stores in that
  *                                   broadcast (default: for P >= 96 and
  *                                   large launches);
@@ -98,6 +106,10 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   of several instances when blocks hold at
  *                                   most 64 elements (default: the latter
  *                                   for batches with blocks that short);
+ *   AR_FUSED_ROTATE = 0|1           sums (other than latency-optimal):
+ *                                   never / always on flat columns as above
+ *                                   (default: when blocks hold at most 64
+ *                                   elements);
  *   AR_FUSED_CAP = N or N,M         resident workgroups per CU of the fused
  *                                   launch (and of the broadcast); 0 is no
  *                                   cap (default: per kernel and P). */
@@ -137,7 +149,8 @@ typedef struct {
   int32_t group, schedule;           /* ar_group and ar_schedule of the plan              */
   int32_t fused_launches;            /* FUSED path: 1, or 2 when split into a reducing
                                         launch and a broadcast (every rank receives the
-                                        same result and P >= 64)                          */
+                                        same result, P >= 64 and, for sums, blocks
+                                        longer than 64 elements)                          */
 } ar_stats;
 
 /* One launch of the STEPWISE path: a list of placement ranges.  In a range,

@@ -158,6 +158,10 @@ struct ColArgs {
   int32_t packed;
   uint32_t ipw, batch;
   FastDiv lendiv;
+  // Rank-slot kernel of the cyclic butterfly plans (flat columns, block of
+  // each lane from its index i in the instance): the first m blocks hold
+  // q + 1 elements (q1div = q + 1), the others q (qdiv = max(q, 1)).
+  FastDiv q1div, qdiv;
 };
 
 // dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.
@@ -173,6 +177,12 @@ int launch_fused_bo(const ColArgs& a, int dtype, int op, bool nt, int grid, void
 template <int P>
 int launch_fused_mid(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream);
 int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream);
+// Rank-slot kernel on flat columns (batches of short blocks, sums): the
+// cyclic butterfly plans with r < L, or the Ring (ring = true); and its
+// dispatcher over P = 2..128.
+template <int P>
+int launch_fused_rot(const ColArgs& a, int dtype, int op, bool ring, int grid, void* stream);
+int launch_fused_rot_any(const ColArgs& a, int P, int dtype, int op, bool ring, int grid, void* stream);
 // Column-fused kernels of the other schedules (fused_group.hip): the XOR
 // group's Recursive Halving / hybrid / Recursive Doubling for P = 2..128 a
 // power of two and any r, and the Ring for any P in 2..128.

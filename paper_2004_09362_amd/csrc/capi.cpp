@@ -56,7 +56,9 @@ constexpr int64_t kPackMaxLen = 64;
 //     one wave per SIMD, and a cap changes nothing;
 //   the Ring at P = 24: 4 (2%);
 //   split launches (P = 127): the reducing launch at 3-6, the broadcast at 2
-//     (1 with nontemporal stores, from kBcastStreamMinP ranks up).
+//     (1 with nontemporal stores, from kBcastStreamMinP ranks up);
+//   flat columns for short blocks (fused_flat): P = 12 at 3-4, P = 24, 32 and
+//     37 at 2 (3-7%); at P = 127 registers allow one wave per SIMD.
 // AR_FUSED_CAP = N (both launches) or N,M (fused launch, broadcast) overrides
 // them; 0 is no cap.
 static int32_t lo_cap(int32_t P) { return P <= 4 ? 0 : P == 6 ? 4 : P <= 7 ? 5 : P <= 11 ? 4 : 3; }
@@ -79,10 +81,18 @@ struct ar_plan {
   // (the broadcast's loads and stores; default by P and launch size),
   // AR_FUSED_PACKED = 0|1 (column tiles of one block of one instance / of
   // several instances, for blocks of up to 64 elements; default: packed for
-  // batches whose blocks hold up to kPackMaxLen elements).
+  // batches whose blocks hold up to kPackMaxLen elements), AR_FUSED_ROTATE =
+  // 0|1 (flat columns for sums other than the latency-optimal ones -- the
+  // rank-slot kernel, or the XOR kernel without the block: never / always;
+  // default: for blocks of up to kPackMaxLen elements).
   int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1, split_mode = -1, bcast_nt_mode = -1;
-  int32_t packed_mode = -1;
+  int32_t packed_mode = -1, rotate_mode = -1;
   bool fused_split = false;
+  // Sums whose blocks hold at most kPackMaxLen elements run on flat columns
+  // (one launch, no split) whenever the batch's columns fit in 32 bits: the
+  // cyclic butterfly plans with r < L and the Ring in the rank-slot kernel,
+  // the XOR group's plans in its own kernel with the block left out.
+  bool fused_flat = false;
   // Occupancy caps (resident workgroups per CU; 0: none) of the fused launch
   // and of the broadcast that follows a split one (AR_FUSED_CAP overrides).
   int32_t fused_cap = 0, bcast_cap = 0;
@@ -114,6 +124,22 @@ int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, in
     AR_BO_CASE(125) AR_BO_CASE(126) AR_BO_CASE(127) AR_BO_CASE(128)
 #undef AR_BO_CASE8
 #undef AR_BO_CASE
+    default: return int(hipErrorInvalidValue);
+  }
+}
+
+int launch_fused_rot_any(const ColArgs& a, int P, int dtype, int op, bool ring, int grid, void* stream) {
+  switch (P) {
+#define AR_ROT_CASE(PP) \
+  case PP: return launch_fused_rot<PP>(a, dtype, op, ring, grid, stream);
+#define AR_ROT_CASE8(B) AR_ROT_CASE(B) AR_ROT_CASE(B + 1) AR_ROT_CASE(B + 2) AR_ROT_CASE(B + 3) \
+  AR_ROT_CASE(B + 4) AR_ROT_CASE(B + 5) AR_ROT_CASE(B + 6) AR_ROT_CASE(B + 7)
+    AR_ROT_CASE8(2) AR_ROT_CASE8(10) AR_ROT_CASE8(18) AR_ROT_CASE8(26) AR_ROT_CASE8(34) AR_ROT_CASE8(42)
+    AR_ROT_CASE8(50) AR_ROT_CASE8(58) AR_ROT_CASE8(66) AR_ROT_CASE8(74) AR_ROT_CASE8(82) AR_ROT_CASE8(90)
+    AR_ROT_CASE8(98) AR_ROT_CASE8(106) AR_ROT_CASE8(114) AR_ROT_CASE(122) AR_ROT_CASE(123) AR_ROT_CASE(124)
+    AR_ROT_CASE(125) AR_ROT_CASE(126) AR_ROT_CASE(127) AR_ROT_CASE(128)
+#undef AR_ROT_CASE8
+#undef AR_ROT_CASE
     default: return int(hipErrorInvalidValue);
   }
 }
@@ -316,10 +342,16 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   // Latency-optimal plans: one flat column space (every block has the same
   // trees), so small instances fill whole waves.
   const int64_t cols = batch * s.n;
-  if (s.r == s.L && pl->fused_kind != kFusedRing && cols < (int64_t(1) << 32) - 64) {
+  const bool flat_fits = cols < (int64_t(1) << 32) - 64;
+  // The cyclic butterfly plans with r < L on batches of short blocks: rank
+  // slots on flat columns, each lane's column rotated by its block.
+  const bool rotate = pl->fused_flat && flat_fits;
+  if ((s.r == s.L && pl->fused_kind != kFusedRing && flat_fits) || rotate) {
     a.flat = 1;
     a.flat_cols = uint32_t(cols);
     a.ndiv = ar::make_fastdiv(uint32_t(s.n));
+    a.q1div = ar::make_fastdiv(uint32_t(a.q + 1));
+    a.qdiv = ar::make_fastdiv(uint32_t(a.q > 0 ? a.q : 1));
     a.total_tiles = uint32_t((cols + 63) / 64);
   } else if (max_len >= 1 && batch < INT32_MAX &&
              (pl->packed_mode == 1 ? max_len <= int64_t(64)
@@ -344,6 +376,7 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   a.lds = cap_lds(pl->fused_cap, device);
   int e;
   if (pl->fused_kind == kFusedXor) e = ar::launch_fused_xor(a, s.P, pl->dtype, pl->op, nt, grid, stream);
+  else if (rotate) e = ar::launch_fused_rot_any(a, s.P, pl->dtype, pl->op, pl->fused_kind == kFusedRing, grid, stream);
   else if (pl->fused_kind == kFusedRing) e = ar::launch_fused_ring(a, pl->dtype, pl->op, nt, grid, stream);
   else e = ar::launch_fused_col_any(a, s.P, pl->dtype, pl->op, nt, grid, stream);
   if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");
@@ -390,6 +423,7 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
   pl->split_mode = env_mode("AR_FUSED_SPLIT");
   pl->bcast_nt_mode = env_mode("AR_BCAST_NT");
   pl->packed_mode = env_mode("AR_FUSED_PACKED");
+  pl->rotate_mode = env_mode("AR_FUSED_ROTATE");
   if (pl->s.P < 2) pl->fused_kind = kFusedNone;
   else if (pl->s.sched == ar::kSchedRing) pl->fused_kind = kFusedRing;
   else if (pl->s.group == ar::kGroupXor) pl->fused_kind = kFusedXor;
@@ -399,10 +433,19 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
   // one result for every rank: the Ring, and r = 0 outside the flat LO kernel
   const bool one_result = pl->fused_kind == kFusedRing ||
                           ((pl->fused_kind == kFusedCol || pl->fused_kind == kFusedXor) && pl->s.r == 0);
-  pl->fused_split = one_result && (pl->split_mode == 1 || (pl->split_mode < 0 && pl->s.P >= kSplitMinP));
+  {
+    const int64_t max_len = pl->s.P > 0 ? pl->s.n / pl->s.P + (pl->s.n % pl->s.P ? 1 : 0) : 0;
+    const bool kind = pl->fused_kind == kFusedRing || pl->fused_kind == kFusedXor ||
+                      (pl->fused_kind == kFusedCol && pl->s.r < pl->s.L);
+    pl->fused_flat = kind && pl->op == AR_SUM &&
+                     (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && max_len <= kPackMaxLen));
+  }
+  pl->fused_split = one_result && !pl->fused_flat &&
+                    (pl->split_mode == 1 || (pl->split_mode < 0 && pl->s.P >= kSplitMinP));
   {
     const int32_t P = pl->s.P;
     if (pl->fused_split) pl->fused_cap = 6;
+    else if (pl->fused_flat) pl->fused_cap = P <= 16 ? 4 : P < 64 ? 2 : 0;
     else if (pl->fused_kind == kFusedLo) pl->fused_cap = lo_cap(P);
     else if (pl->fused_kind == kFusedRing) pl->fused_cap = 4;
     else if (pl->s.r == 0) pl->fused_cap = P <= 32 ? 4 : 3;

@@ -206,6 +206,139 @@ __global__ __launch_bounds__(kBlock) void fused_mid_kernel(const ColArgs a) {
   }
 }
 
+// fused_rot_kernel: the cyclic butterfly plans with r < L (the
+// bandwidth-optimal fold and the shifted recursion above) for batches of
+// short blocks, in rank slots over flat columns (sums).  Lane g holds element i of
+// instance g / n; its block b follows from i.  It loads X[y] = V_y[e] for
+// every rank y -- each load a whole 256-byte row of one rank buffer,
+// whatever the blocks -- and rotates the column by b, X[p] <- X[b + p], so
+// that X[p] is placement p's value, V_{b+p}, exactly as the block-tiled
+// kernels read it through rotated pointers.  The fold or the recursion then
+// combines the same operand pairs in the same order (the same bits).  The
+// bandwidth-optimal result goes to every rank; in the shifted plan rank
+// b + q receives S[col_src(q)], so the column of results is rotated back by
+// b and rank y stores slot y.  A rotation by a per-lane amount is a
+// log-depth network of static rotations by 2^j, each applied on the lanes
+// whose amount has bit j set (P selects per stage; a stage no lane needs is
+// skipped).
+
+// Lanes whose bit in m is set take b, the others a: one v_cndmask_b32.  The
+// instruction is written out because the compiler otherwise turned the
+// selects of a rotation network into selects of array indices and rebuilt
+// the network as duplicated select trees behind divergent branches (2761
+// selects instead of 120 at P = 24, six times slower).
+template <typename T>
+__device__ __forceinline__ T lane_select(uint64_t m, T a, T b) {
+  static_assert(sizeof(T) == 4, "4-byte elements");
+  uint32_t r;
+  asm("v_cndmask_b32 %0, %1, %2, %3"
+      : "=v"(r)
+      : "v"(__builtin_bit_cast(uint32_t, a)), "v"(__builtin_bit_cast(uint32_t, b)), "s"(m));
+  return __builtin_bit_cast(T, r);
+}
+
+// X[p] <- X[(p + s) mod P] for the lane's s in [0, P).
+template <int P, int K, typename T>
+__device__ __forceinline__ void rotate_lanes(T (&X)[P], uint32_t s) {
+  if constexpr ((1 << K) < P) {
+    constexpr int sh = 1 << K;
+    const uint64_t m = __builtin_amdgcn_ballot_w64(((s >> K) & 1u) != 0);
+    if (m != 0) {
+      T Y[P];
+#pragma unroll
+      for (int p = 0; p < P; ++p) Y[p] = lane_select(m, X[p], X[(p + sh) % P]);
+#pragma unroll
+      for (int p = 0; p < P; ++p) X[p] = Y[p];
+    }
+    rotate_lanes<P, K + 1, T>(X, s);
+  }
+}
+
+// Shifted plan with RR removed distribution steps: slot q takes
+// S[col_src(q)], the result that reaches placement q (compile-time indices).
+template <int P, int RR, typename T, int... Qs>
+__device__ __forceinline__ void rot_gather(T (&Z)[P], const T (&S)[P], std::integer_sequence<int, Qs...>) {
+  ((Z[Qs] = S[std::integral_constant<int, col_src(P, RR, Qs)>::value]), ...);
+}
+
+// RR = 0: the bandwidth-optimal fold; RR >= 1: the shifted recursion with
+// RR distribution steps removed; RR = -1: the Ring of Sec. 6, whose column
+// is the chain acc = V_{b+d} (+) acc, d = 1 .. P-1, from V_b (the order of
+// fused_ring_kernel), its result going to every rank.  RR is a template parameter so that the
+// compiler drops the starred sums that no rank receives (all but 2^RR of
+// them) and the primed sums that only feed those: at P = 127, RR = 4 that
+// is 306 combinations of 1524 and a third of the registers.  Loads and
+// stores are always nontemporal: these launches stream short blocks of many
+// instances once.
+template <int P, int RR, typename T, int OP>
+__global__ __launch_bounds__(kBlock) void fused_rot_kernel(const ColArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
+       t += gridDim.x * uint32_t(kWavesPerBlock)) {
+    const uint32_t g = t * uint32_t(kWave) + uint32_t(lane);
+    if (g < a.flat_cols) {
+      const uint32_t inst = fdiv(g, a.ndiv);
+      const uint32_t i = g - inst * a.ndiv.d;
+      const uint32_t longer = uint32_t(a.m) * (uint32_t(a.q) + 1);  // elements in the blocks of q + 1
+      const uint32_t b = i < longer ? fdiv(i, a.q1div) : uint32_t(a.m) + fdiv(i - longer, a.qdiv);
+      const int64_t e = int64_t(inst) * a.stride + i;
+      T X[P];
+#pragma unroll
+      for (int y = 0; y < P; ++y) X[y] = ld1<true>(static_cast<const T*>(a.user[y]) + e);
+      rotate_lanes<P, 0, T>(X, b);
+      if constexpr (RR < 0) {
+        T acc = X[0];
+#pragma unroll
+        for (int d = 1; d < P; ++d) acc = comb<OP>(X[d], acc);
+#pragma unroll
+        for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(a.user[y]) + e, acc);
+      } else if constexpr (RR == 0) {
+        bo_fold<P, OP, T, P>(X);
+#pragma unroll
+        for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(a.user[y]) + e, X[0]);
+      } else {
+        T S[P];
+#pragma unroll
+        for (int d = 0; d < P; ++d) S[d] = X[d];
+        mid_steps<P, 0, OP, T>(X, S);
+        // rank b + q receives slot q: rotate the slots back by b, rank y stores slot y
+        rot_gather<P, RR, T>(X, S, std::make_integer_sequence<int, P>{});
+        rotate_lanes<P, 0, T>(X, b == 0 ? 0u : uint32_t(P) - b);
+#pragma unroll
+        for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(a.user[y]) + e, X[y]);
+      }
+    }
+  }
+}
+
+template <int P, int RR, typename T, int OP>
+int launch_rot_rr(const ColArgs& a, int grid, hipStream_t s) {
+  if constexpr (RR < col_L(P)) {
+    if (a.r == RR) {
+      hipLaunchKernelGGL((fused_rot_kernel<P, RR, T, OP>), dim3(grid), dim3(kBlock), a.lds, s, a);
+      return int(hipGetLastError());
+    }
+    return launch_rot_rr<P, RR + 1, T, OP>(a, grid, s);
+  } else {
+    return int(hipErrorInvalidValue);
+  }
+}
+
+// Sums only (op 0): max plans with short blocks keep the packed tiles, which
+// halves the instantiations of these kernels.
+template <int P>
+int launch_fused_rot(const ColArgs& a, int dtype, int op, bool ring, int grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (op != 0) return int(hipErrorInvalidValue);
+  if (ring) {
+    if (dtype == 0) hipLaunchKernelGGL((fused_rot_kernel<P, -1, int32_t, 0>), dim3(grid), dim3(kBlock), a.lds, s, a);
+    else hipLaunchKernelGGL((fused_rot_kernel<P, -1, float, 0>), dim3(grid), dim3(kBlock), a.lds, s, a);
+    return int(hipGetLastError());
+  }
+  return dtype == 0 ? launch_rot_rr<P, 0, int32_t, 0>(a, grid, s) : launch_rot_rr<P, 0, float, 0>(a, grid, s);
+}
+
 template <int P>
 int launch_fused_bo(const ColArgs& a, int dtype, int op, bool nt, int grid, void* stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);

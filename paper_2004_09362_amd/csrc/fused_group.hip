@@ -99,7 +99,10 @@ __global__ __launch_bounds__(kBlock) void fused_xor_kernel(const ColArgs a) {
     int32_t b;
     int64_t e;
     bool live;
-    if (R == xor_L(P) && a.flat) {  // Recursive Doubling: no block dependence, flat columns
+    // Flat columns where no result depends on the block: Recursive
+    // Doubling, and sums at any R (the block only orders the operands of a
+    // halving pair, and a sum is the same either way).
+    if ((R == xor_L(P) || OP == 0) && a.flat) {
       const uint32_t g = t * uint32_t(kWave) + uint32_t(lane);
       const uint32_t inst = fdiv(g, a.ndiv);
       b = 0;

@@ -236,6 +236,7 @@ def test_split_and_single_fused_launch_agree(P, k, group, schedule, monkeypatch)
     n, B, stride = 5 * P + 3, 3, 5 * P + 11
     x = rng.normal(size=(P, B, stride)).astype(np.float32)
     want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, "sum", group=group, schedule=schedule)
+    monkeypatch.setenv("AR_FUSED_ROTATE", "0")  # short blocks: keep the block-tiled launches that split
     for split, bnt in (("0", "0"), ("1", "0"), ("1", "1")):
         monkeypatch.setenv("AR_FUSED_SPLIT", split)
         monkeypatch.setenv("AR_BCAST_NT", bnt)

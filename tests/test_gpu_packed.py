@@ -9,6 +9,14 @@ halving and hybrid schedules, the Ring -- must give the oracle's bits with
 packed tiles (AR_FUSED_PACKED=1), with blocked tiles (=0) and by default,
 on batches with gaps between instances, ragged last tile groups and blocks
 of zero, one or a few elements, and must leave the gaps untouched.
+
+Sums also run such batches on flat columns (AR_FUSED_ROTATE), every rank's
+row loaded whole: the cyclic butterfly plans with r < L and the Ring in a
+rank-slot kernel that rotates each lane's column by its block, the XOR
+group's plans with the block left out (it only orders the operands of a
+halving pair, which a sum does not see).  It is checked forced on and off, with
+either tiling, on blocks of every length up to 70 elements (longer blocks
+leave most stages of the rotation network unused by a whole wave).
 """
 import numpy as np
 import pytest
@@ -20,7 +28,7 @@ from test_gpu_parity import DEV, bits, note
 
 pytestmark = pytest.mark.gpu
 
-# P, n, batch, instance stride, k, group, schedule, op
+# P, n, batch, instance stride, k, group, schedule, op ("isum": int32 sum)
 CASES = [
     (5, 23, 37, 29, 6, "cyclic", "butterfly", "sum"),        # bandwidth-optimal, blocks of 4-5, 12 per wave
     (24, 100, 50, 104, 10, "cyclic", "butterfly", "sum"),    # bandwidth-optimal, blocks of 4-5
@@ -38,6 +46,21 @@ CASES = [
     (127, 500, 7, 500, 252, "cyclic", "ring", "sum"),        # Ring, split
     (24, 1200, 6, 1200, 10, "cyclic", "butterfly", "sum"),   # blocks of 50: one instance per packed wave
     (24, 1700, 4, 1700, 10, "cyclic", "butterfly", "sum"),   # blocks of 70: blocked tiles even when forced
+    (24, 1700, 4, 1703, 7, "cyclic", "butterfly", "max"),    # shifted, blocks of 70
+    (2, 9, 50, 11, 2, "cyclic", "butterfly", "sum"),         # P = 2: one step each way
+    (3, 50, 40, 53, 3, "cyclic", "butterfly", "sum"),        # P = 3, r = 1
+    (127, 1000, 9, 1003, 8, "cyclic", "butterfly", "sum"),   # shifted at P = 127, r = 6 = L - 1
+    (127, 1000, 9, 1003, 13, "cyclic", "butterfly", "sum"),  # shifted at P = 127, r = 1
+    (100, 6400, 3, 6400, 12, "cyclic", "butterfly", "sum"),  # blocks of exactly 64
+    (37, 300, 20, 301, 9, "cyclic", "butterfly", "isum"),    # int32, shifted
+    (127, 1000, 9, 1003, 14, "cyclic", "butterfly", "isum"), # int32, bandwidth-optimal
+    (16, 100, 9, 103, 5, "xor", "butterfly", "isum"),        # int32, XOR hybrid
+    (64, 300, 6, 300, 12, "xor", "butterfly", "sum"),        # Recursive Halving at P = 64
+    (24, 100, 17, 100, 46, "cyclic", "ring", "isum"),        # int32, Ring
+]
+
+SETTINGS = [  # AR_FUSED_ROTATE, AR_FUSED_PACKED (None: unset, the default)
+    ("0", "0"), ("0", "1"), ("1", None), (None, None),
 ]
 
 
@@ -46,17 +69,27 @@ def test_packed_and_blocked_tiles_agree_with_oracle(P, n, B, stride, k, group, s
     if not torch.cuda.is_available():
         pytest.fail("GPU tests need a GPU")
     rng = np.random.default_rng(P * 1000 + n + k)
-    x = rng.normal(size=(P, B, stride)).astype(np.float32)
+    dtype = "int32" if op == "isum" else "float32"
+    if op == "isum":
+        op = "sum"
+        x = rng.integers(-2**31, 2**31, size=(P, B, stride), dtype=np.int64).astype(np.int32)
+    else:
+        x = rng.normal(size=(P, B, stride)).astype(np.float32)
     want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, op, group=group, schedule=schedule)
+    if dtype == "int32":  # wrapping sum, exact whatever the order
+        s64 = x[:, :, :n].astype(np.int64).sum(axis=0)
+        assert np.array_equal(want, np.broadcast_to(((s64 + 2**31) % 2**32 - 2**31).astype(np.int32), want.shape))
     if op == "max":
         assert np.array_equal(want, np.broadcast_to(x[:, :, :n].max(axis=0), want.shape))
-    for mode in ("0", "1", None):
-        if mode is None:
-            monkeypatch.delenv("AR_FUSED_PACKED", raising=False)
-        else:
-            monkeypatch.setenv("AR_FUSED_PACKED", mode)
-        note("packed=%s %s/%s P=%d n=%d B=%d k=%d op=%s" % (mode, group, schedule, P, n, B, k, op))
-        plan = ar.Plan(P, n, "float32", op, k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
+    for rotate, packed in SETTINGS:
+        for var, val in (("AR_FUSED_ROTATE", rotate), ("AR_FUSED_PACKED", packed)):
+            if val is None:
+                monkeypatch.delenv(var, raising=False)
+            else:
+                monkeypatch.setenv(var, val)
+        mode = "rotate=%s packed=%s" % (rotate, packed)
+        note("%s %s/%s P=%d n=%d B=%d k=%d op=%s" % (mode, group, schedule, P, n, B, k, op))
+        plan = ar.Plan(P, n, dtype, op, k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
         X = torch.from_numpy(x).to(DEV)
         plan.batched([X[i] for i in range(P)], B, stride)
         torch.cuda.synchronize()
