@@ -20,6 +20,8 @@ Workloads (seeded synthetic rank buffers, resident in HBM before timing):
   prime3                 P = 3, n = 1024 int32 U[-1000,1000], --k 2..4 (default 4)
   gradsync32             P = 32, n = 2^24 fp32 N(0,1e-3), --k 5..10 (default 10)
   small_batch127         P = 127, n = 106 fp32 N(0,1), 65536 instances, k = 7
+  medium127              P = 127, n = 2304 fp32 N(0,1) (9 KB), 8192 instances,
+                         --k 7..14 (default 11)
 
 --group xor runs the butterfly schedules over the XOR group (power-of-two P:
 Recursive Halving at k = 2 log2 P, Recursive Doubling at k = log2 P);
@@ -77,7 +79,7 @@ def jobs_for(name, k_arg, group="cyclic", schedule="butterfly", op=None):
     return w, jobs
 
 
-DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4, "gradsync32": 10}
+DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4, "gradsync32": 10, "medium127": 11}
 
 SHAPES = {
     "small_batch": "small_batch: P in {5,6,7,12}, n=106 fp32 N(0,1), 65536 instances per launch",
@@ -87,6 +89,7 @@ SHAPES = {
     "prime3": "prime3: P=3, n=1024 int32 U[-1000,1000]",
     "gradsync32": "gradsync32: P=32, n=16777216 fp32 N(0,1e-3)",
     "small_batch127": "small_batch127: P=127, n=106 fp32 N(0,1), 65536 instances per launch",
+    "medium127": "medium127: P=127, n=2304 fp32 N(0,1), 8192 instances per launch",
 }
 
 
@@ -252,7 +255,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="small_batch",
                     choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3", "gradsync32",
-                             "small_batch127"])
+                             "small_batch127", "medium127"])
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--op", choices=["sum", "max"], default=None,
                     help="the reduction (default: the workload's first; prime_sweep also runs max)")
@@ -366,6 +369,8 @@ def main():
     achieved = bytes_per_launch / (launch_ms * 1e-3) / 1e9
     if not fused:
         kname = "step_kernel<k=%d>" % dj["k"]
+    elif st.fused_flat and args.group != "xor":
+        kname = "fused_rot_kernel<P=%d,%s>" % (dj["P"], "ring" if args.schedule == "ring" else "r=%d" % st.r)
     elif args.schedule == "ring":
         kname = "fused_ring_kernel"
     elif args.group == "xor":

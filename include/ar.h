@@ -151,6 +151,10 @@ typedef struct {
                                         launch and a broadcast (every rank receives the
                                         same result, P >= 64 and, for sums, blocks
                                         longer than 64 elements)                          */
+  int32_t fused_flat;                /* FUSED path of a sum with short blocks: 1 when it
+                                        runs on flat columns (the rank-slot kernel, or
+                                        the XOR group's kernel without the block) for
+                                        batches of fewer than 2^32 - 64 columns           */
 } ar_stats;
 
 /* One launch of the STEPWISE path: a list of placement ranges.  In a range,

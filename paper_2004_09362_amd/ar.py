@@ -52,6 +52,7 @@ class Stats(ctypes.Structure):
         ("hbm_bytes_stepwise", ctypes.c_int64), ("hbm_bytes_fused", ctypes.c_int64),
         ("workspace_bytes", ctypes.c_int64),
         ("group", ctypes.c_int32), ("schedule", ctypes.c_int32), ("fused_launches", ctypes.c_int32),
+        ("fused_flat", ctypes.c_int32),
     ]
 
     def as_dict(self):

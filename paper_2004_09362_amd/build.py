@@ -91,7 +91,7 @@ def kernel_families(kernel: str) -> list[str]:
     out = []
     for part in kernel.split("+"):
         for prefix, fam in (("step_kernel", "step"), ("fused_lo_kernel", "lo"), ("fused_bo_kernel", "col"),
-                            ("fused_mid_kernel", "col"), ("fused_xor_kernel", "group"),
+                            ("fused_mid_kernel", "col"), ("fused_rot_kernel", "col"), ("fused_xor_kernel", "group"),
                             ("fused_ring_kernel", "group"), ("broadcast", "bcast")):
             if part.startswith(prefix):
                 out.append(fam)

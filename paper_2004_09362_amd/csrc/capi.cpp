@@ -563,6 +563,7 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
   out->hbm_bytes_stepwise = s.hbm_blocks * s.n * 4;
   out->hbm_bytes_fused = s.P > 1 ? (int64_t(2) * s.P + (plan->fused_split ? 1 : 0)) * s.n * 4 : 0;
   out->fused_launches = s.P > 1 ? (plan->fused_split ? 2 : 1) : 0;
+  out->fused_flat = s.P > 1 && plan->fused_flat ? 1 : 0;
   out->workspace_bytes = s.uses_scratch ? int64_t(2) * s.P * round_up(s.n, 64) * 4 : 0;
   out->group = s.group;
   out->schedule = s.sched;

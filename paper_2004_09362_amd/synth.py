@@ -100,6 +100,10 @@ WORKLOADS = {
     # the 425-byte message at the paper's P = 127, many instances per launch
     "small_batch127": dict(P=[127], n=106, dtype=np.float32, dist=Dist("normal", 0.0, 1.0), ks="lo",
                            ops=["sum"], batch=65536, seed=BASE_SEED + 6),
+    # a 9 KB message at the paper's P = 127, many instances per launch: the medium size at which the cost
+    # model with the measured cluster parameters picks k = 11 (blocks of 18-19 elements)
+    "medium127": dict(P=[127], n=2304, dtype=np.float32, dist=Dist("normal", 0.0, 1.0),
+                      ks=[7, 8, 9, 10, 11, 12, 13, 14], ops=["sum"], batch=8192, seed=BASE_SEED + 7),
     # the gradient-sync shape at a power of two, where the XOR group applies
     "gradsync32": dict(P=[32], n=16777216, dtype=np.float32, dist=Dist("normal", 0.0, 1e-3),
                        ks=[5, 6, 7, 8, 9, 10], ops=["sum"], batch=1, seed=BASE_SEED + 5),

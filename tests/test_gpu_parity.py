@@ -354,6 +354,32 @@ def test_small_batch_workload_full_size():
 # Full-size workloads, sampled columns
 # ---------------------------------------------------------------------------
 
+@pytest.mark.parametrize("k", [11, 14, 7])
+def test_medium127_workload_full_size(k):
+    """P = 127, n = 2304 fp32 (9 KB), 8192 instances: the rank-slot kernel
+    (k = 11 shifted, k = 14 bandwidth-optimal) and the latency-optimal flat
+    kernel (k = 7) on all instances; the oracle on 128 sampled instances."""
+    w = synth.WORKLOADS["medium127"]
+    P, n, B = 127, w["n"], w["batch"]
+    note("medium127 P=%d n=%d B=%d k=%d" % (P, n, B, k))
+    X = synth.device_ranks(w["seed"], P, B * n, np.float32, w["dist"], DEV)
+    idx = np.sort(np.random.default_rng(k).choice(B, size=128, replace=False))
+    it = torch.from_numpy(idx).to(DEV)
+    xs = X.view(P, B, n)[:, it].cpu().numpy()
+    plan = ar.Plan(P, n, "float32", "sum", k)
+    st = plan.stats()
+    assert st.fused_flat == (1 if k > 7 else 0) and st.fused_launches == 1
+    plan.batched([X[i] for i in range(P)], B, n)
+    torch.cuda.synchronize()
+    got = X.view(P, B, n)[:, it].cpu().numpy()
+    assert np.array_equal(bits(got), bits(oracle.allreduce_batched(xs, k, "sum")))
+    for j in range(0, 128, 32):
+        assert_fp32_bound(got[:, j], xs[:, j])
+    plan.close()
+    del X
+    torch.cuda.empty_cache()
+
+
 def check_full_size(name, P, n, k, op, seed, dist):
     note("%s P=%d n=%d k=%d op=%s: fill" % (name, P, n, k, op))
     X = synth.device_ranks(seed, P, n, np.float32, dist, DEV)
