@@ -97,3 +97,33 @@ def test_packed_and_blocked_tiles_agree_with_oracle(P, n, B, stride, k, group, s
         plan.close()
         assert np.array_equal(bits(got[:, :, :n]), bits(want)), mode
         assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), mode
+
+
+def _random_cases(count, seed):
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        group = ["cyclic", "cyclic", "xor", "ring"][rng.integers(4)]
+        if group == "xor":
+            P = int(2 ** rng.integers(1, 8))
+        else:
+            P = int(rng.integers(2, 129))
+        L = max(0, (P - 1).bit_length())
+        if group == "ring":
+            k, schedule, group = 2 * (P - 1), "ring", "cyclic"
+        else:
+            k, schedule = int(rng.integers(L, 2 * L + 1)), "butterfly"
+        n = int(rng.integers(1, 70 * P))           # blocks of 0 to 70 elements
+        B = int(rng.integers(1, 9))
+        stride = n + int(rng.integers(0, 5))
+        op = ["sum", "sum", "isum", "max"][rng.integers(4)]
+        out.append((P, n, B, stride, k, group, schedule, op))
+    return out
+
+
+@pytest.mark.parametrize("P,n,B,stride,k,group,schedule,op", _random_cases(40, 20261202))
+def test_random_short_block_batches(P, n, B, stride, k, group, schedule, op, monkeypatch):
+    """Seeded random groups, schedules, P, k, n (blocks of up to 70
+    elements), batch sizes and strides, under the default and with flat
+    columns forced on and off: the oracle's bits every time."""
+    test_packed_and_blocked_tiles_agree_with_oracle(P, n, B, stride, k, group, schedule, op, monkeypatch)
