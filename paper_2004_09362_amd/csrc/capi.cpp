@@ -339,14 +339,15 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   const int64_t tiles = std::max<int64_t>(1, (max_len + 63 + 63) / 64);
   a.tiles = ar::make_fastdiv(uint32_t(std::min<int64_t>(tiles, INT32_MAX)));
   a.pdiv = ar::make_fastdiv(uint32_t(s.P));
-  // Latency-optimal plans: one flat column space (every block has the same
-  // trees), so small instances fill whole waves.
+  // Flat columns (the batch * n columns of all instances as one space, so
+  // that small instances fill whole waves): latency-optimal plans, whose
+  // trees are the same for every block, and sums with short blocks
+  // (fused_flat) -- the rank-slot kernel, which rotates each lane's column by
+  // its block, or the XOR group's kernel, whose sums do not see the block.
   const int64_t cols = batch * s.n;
   const bool flat_fits = cols < (int64_t(1) << 32) - 64;
-  // The cyclic butterfly plans with r < L on batches of short blocks: rank
-  // slots on flat columns, each lane's column rotated by its block.
-  const bool rotate = pl->fused_flat && flat_fits;
-  if ((s.r == s.L && pl->fused_kind != kFusedRing && flat_fits) || rotate) {
+  const bool flat_short = pl->fused_flat && flat_fits;
+  if ((s.r == s.L && pl->fused_kind != kFusedRing && flat_fits) || flat_short) {
     a.flat = 1;
     a.flat_cols = uint32_t(cols);
     a.ndiv = ar::make_fastdiv(uint32_t(s.n));
@@ -376,7 +377,7 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   a.lds = cap_lds(pl->fused_cap, device);
   int e;
   if (pl->fused_kind == kFusedXor) e = ar::launch_fused_xor(a, s.P, pl->dtype, pl->op, nt, grid, stream);
-  else if (rotate) e = ar::launch_fused_rot_any(a, s.P, pl->dtype, pl->op, pl->fused_kind == kFusedRing, grid, stream);
+  else if (flat_short) e = ar::launch_fused_rot_any(a, s.P, pl->dtype, pl->op, pl->fused_kind == kFusedRing, grid, stream);
   else if (pl->fused_kind == kFusedRing) e = ar::launch_fused_ring(a, pl->dtype, pl->op, nt, grid, stream);
   else e = ar::launch_fused_col_any(a, s.P, pl->dtype, pl->op, nt, grid, stream);
   if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");

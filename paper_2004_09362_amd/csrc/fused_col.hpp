@@ -206,15 +206,16 @@ __global__ __launch_bounds__(kBlock) void fused_mid_kernel(const ColArgs a) {
   }
 }
 
-// fused_rot_kernel: the cyclic butterfly plans with r < L (the
-// bandwidth-optimal fold and the shifted recursion above) for batches of
-// short blocks, in rank slots over flat columns (sums).  Lane g holds element i of
-// instance g / n; its block b follows from i.  It loads X[y] = V_y[e] for
+// fused_rot_kernel: sums over batches of short blocks, in rank slots over
+// flat columns, for the cyclic butterfly plans with r < L (the
+// bandwidth-optimal fold and the shifted recursion above) and the Ring.
+// Lane g holds element i of instance g / n; its block b follows from i.  It loads X[y] = V_y[e] for
 // every rank y -- each load a whole 256-byte row of one rank buffer,
 // whatever the blocks -- and rotates the column by b, X[p] <- X[b + p], so
 // that X[p] is placement p's value, V_{b+p}, exactly as the block-tiled
-// kernels read it through rotated pointers.  The fold or the recursion then
-// combines the same operand pairs in the same order (the same bits).  The
+// kernels read it through rotated pointers.  The fold, the recursion or the
+// chain then combines the same operand pairs in the same order (the same
+// bits).  The
 // bandwidth-optimal result goes to every rank; in the shifted plan rank
 // b + q receives S[col_src(q)], so the column of results is rotated back by
 // b and rank y stores slot y.  A rotation by a per-lane amount is a
@@ -264,12 +265,12 @@ __device__ __forceinline__ void rot_gather(T (&Z)[P], const T (&S)[P], std::inte
 // RR = 0: the bandwidth-optimal fold; RR >= 1: the shifted recursion with
 // RR distribution steps removed; RR = -1: the Ring of Sec. 6, whose column
 // is the chain acc = V_{b+d} (+) acc, d = 1 .. P-1, from V_b (the order of
-// fused_ring_kernel), its result going to every rank.  RR is a template parameter so that the
-// compiler drops the starred sums that no rank receives (all but 2^RR of
-// them) and the primed sums that only feed those: at P = 127, RR = 4 that
-// is 306 combinations of 1524 and a third of the registers.  Loads and
-// stores are always nontemporal: these launches stream short blocks of many
-// instances once.
+// fused_ring_kernel), its result going to every rank.  RR is a template
+// parameter so that the compiler drops the starred sums that no rank
+// receives (all but 2^RR of them) and the primed sums that only feed those
+// (at P = 127, RR = 4: 306 of 1524 combinations); with all of them kept,
+// the P = 127 kernels spilled registers.  Loads and stores are always
+// nontemporal: these launches stream short blocks of many instances once.
 template <int P, int RR, typename T, int OP>
 __global__ __launch_bounds__(kBlock) void fused_rot_kernel(const ColArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
