@@ -63,7 +63,10 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
 /* How ar_execute runs a plan.
  *   STEPWISE: one kernel launch per communication step of the schedule
  *             (2*ceil(log2 P) - r launches, plus one local copy when P = 2,
- *             k = 1), each pulling the peer's blocks out of HBM.
+ *             k = 1), each pulling the peer's blocks out of HBM.  With
+ *             blocks of at most 256 elements a launch streams each rank's
+ *             run of consecutive blocks that share an operation as one
+ *             flat space, so that batches of small instances fill waves.
  *   FUSED:    one launch that runs every step of the schedule on element
  *             columns held in registers, reading each input and writing
  *             each output once, for every plan with P >= 2: the Sec. 7 fold
@@ -91,6 +94,9 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  * change launch shapes and speed, never results):
  *   AR_STEP_NT, AR_FUSED_NT = 0|1   nontemporal loads and stores never /
  *                                   always (default: by bytes per launch);
+ *   AR_STEP_MERGE = 0|1             step launches block by block / as
+ *                                   merged runs of blocks (default: merged
+ *                                   for blocks of at most 256 elements);
  *   AR_FUSED_MODE = 0|1             latency-optimal kernel with P <= 16:
  *                                   16-byte or 4-byte columns (default 1);
  *   AR_FUSED_SPLIT = 0|1            block-tiled launches: single fused

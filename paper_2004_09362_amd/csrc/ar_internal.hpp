@@ -121,6 +121,16 @@ struct StepArgs {
   int32_t P, n_ranges;
   int32_t group;            // kGroupCyclic or kGroupXor
   DevRange ranges[kMaxRanges];
+  // Merged runs (step_merged_kernel): the placements p0 .. p0+count-1 of a
+  // range touch one run of consecutive blocks of rank x (cyclically), with
+  // one peer and one set of buffers, so the range is streamed as one flat
+  // space per rank: run_len[i] elements per instance (the whole row when
+  // the range covers every placement, else count * ceil(n / P) -- a rank's
+  // run is at most that long), batch * run_len[i] columns in all, tiles of
+  // 256 columns.  Range i's tiles start at tile_first[i], P * tiles[i] of
+  // them (rank-major).
+  FastDiv run_len[kMaxRanges], tiles[kMaxRanges];
+  uint32_t run_cols[kMaxRanges], tile_first[kMaxRanges];
 };
 
 // lds: dynamic LDS each workgroup reserves without using it, so that fewer
@@ -166,6 +176,9 @@ struct ColArgs {
 
 // dtype: 0 int32, 1 float32; op: 0 sum, 1 max.  Returns a hipError_t value.
 int launch_step(const StepArgs& a, int dtype, int op, bool vec, bool nt, int grid, void* stream);
+// One step as merged runs (a.run_len, a.tiles, ...): each range's blocks of a
+// rank streamed as one flat space per instance.
+int launch_step_merged(const StepArgs& a, int dtype, int op, bool nt, int grid, void* stream);
 // Fused latency-optimal kernel; mode 0: 16-byte columns groups, 1: one
 // element per lane (contiguous instances), 2: any instance stride.
 int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, int mode, bool nt, int grid, void* stream);

@@ -166,6 +166,102 @@ __global__ __launch_bounds__(kBlock) void step_kernel(const StepArgs a) {
   }
 }
 
+// Merged runs.  Within one launch, the placements p0 .. p0+count-1 of a
+// range share their operation, their buffers and their peer, and rank x's
+// blocks at those placements -- x - p (cyclic) or x XOR p (XOR group, for
+// an aligned power-of-two range) -- form one run of consecutive blocks,
+// wrapping past block P-1 at most once (cyclic).  Peer and own blocks have
+// the same index, so the whole run is one elementwise operation over a
+// contiguous range of elements per instance, and over the whole row when
+// the range covers every placement (every latency-optimal step).  This
+// kernel streams each (rank, range) as a flat space of batch * run columns,
+// four 4-byte columns per lane (256 per wave tile), so that batches of
+// short blocks fill their waves.  The element operations are exactly those
+// of step_kernel, only grouped differently.
+template <typename T, int OP, int KIND, bool NT>
+__device__ __forceinline__ void merged_cols(T* __restrict__ dst, const T* __restrict__ own, T* __restrict__ dst2,
+                                            const T* __restrict__ own2, const T* __restrict__ src, const int64_t (&e)[4],
+                                            const bool (&live)[4]) {
+  T sv[4], ov[4], o2v[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (live[u]) {
+      sv[u] = ld1<NT>(src + e[u]);
+      if constexpr (KIND != kCopy) ov[u] = ld1<NT>(own + e[u]);
+      if constexpr (KIND == kReduce2) o2v[u] = ld1<NT>(own2 + e[u]);
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (live[u]) {
+      if constexpr (KIND == kCopy) {
+        st1<NT>(dst + e[u], sv[u]);
+      } else {
+        if constexpr (KIND == kReduce2) st1<NT>(dst2 + e[u], comb<OP>(o2v[u], sv[u]));
+        st1<NT>(dst + e[u], comb<OP>(ov[u], sv[u]));
+      }
+    }
+  }
+}
+
+template <typename T, int OP, bool NT, bool XOR>
+__global__ __launch_bounds__(kBlock) void step_merged_kernel(const StepArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const uint32_t wave_in_block = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int32_t P = a.P;
+  for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
+       t += gridDim.x * uint32_t(kWavesPerBlock)) {
+    int ri = 0;
+    while (ri + 1 < a.n_ranges && t >= a.tile_first[ri + 1]) ++ri;
+    const DevRange& R = a.ranges[ri];
+    const uint32_t tr = t - a.tile_first[ri];
+    const uint32_t x32 = fdiv(tr, a.tiles[ri]);
+    const uint32_t tile = tr - x32 * a.tiles[ri].d;
+    const int32_t x = int32_t(x32);
+    const bool whole = R.count == P;
+    int32_t bf, y;  // first block of rank x's run, peer
+    if constexpr (XOR) {
+      bf = (x ^ R.p0) & ~(R.count - 1);
+      y = x ^ R.delta;
+    } else {
+      bf = x - R.p0 - R.count + 1;  // > -2P
+      if (bf < 0) bf += P;
+      if (bf < 0) bf += P;
+      y = x + R.delta;
+      if (y >= P) y -= P;
+      if (y < 0) y += P;
+    }
+    // elements of the run: from block bf on, count blocks, wrapping at n
+    const int64_t off = int64_t(bf) * a.q + (bf < a.m ? bf : a.m);
+    const int32_t be = bf + R.count;  // one past the run's last block, <= 2P
+    const int32_t bw = be > P ? be - P : be;
+    const int64_t off_end = int64_t(bw) * a.q + (bw < a.m ? bw : a.m);
+    const int64_t run = be > P ? a.n - off + off_end : off_end - off;
+    int64_t e[4];
+    bool live[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const uint32_t g = tile * uint32_t(4 * kWave) + uint32_t(u * kWave + lane);
+      const uint32_t inst = fdiv(g, a.run_len[ri]);
+      const int64_t v = int64_t(g) - int64_t(inst) * a.run_len[ri].d;
+      int64_t i = whole ? v : off + v;
+      if (i >= a.n) i -= a.n;
+      live[u] = g < a.run_cols[ri] && (whole || v < run);
+      e[u] = int64_t(inst) * a.stride + i;
+    }
+    T* dst = buf_ptr<T>(a, R.dst, x);
+    const T* src = buf_ptr<T>(a, R.src, y);
+    if (R.kind == kCopy) {
+      merged_cols<T, OP, kCopy, NT>(dst, nullptr, nullptr, nullptr, src, e, live);
+    } else if (R.kind == kReduce) {
+      merged_cols<T, OP, kReduce, NT>(dst, buf_ptr<T>(a, R.own, x), nullptr, nullptr, src, e, live);
+    } else {
+      merged_cols<T, OP, kReduce2, NT>(dst, buf_ptr<T>(a, R.own, x), buf_ptr<T>(a, R.dst2, x),
+                                       buf_ptr<T>(a, R.own2, x), src, e, live);
+    }
+  }
+}
+
 template <typename T, int OP>
 int launch_step_t(const StepArgs& a, bool vec, bool nt, int grid, hipStream_t s) {
   // the group is a template argument: the block / peer arithmetic sits in
@@ -185,6 +281,30 @@ int launch_step_t(const StepArgs& a, bool vec, bool nt, int grid, hipStream_t s)
 }  // namespace
 
 int64_t step_tile_elems() { return kTile; }
+
+int launch_step_merged(const StepArgs& a, int dtype, int op, bool nt, int grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const dim3 g(grid), blk(kBlock);
+#define AR_MERGED(T, OP)                                                                                   \
+  do {                                                                                                     \
+    if (a.group == kGroupXor) {                                                                            \
+      if (nt) hipLaunchKernelGGL((step_merged_kernel<T, OP, true, true>), g, blk, 0, s, a);                 \
+      else hipLaunchKernelGGL((step_merged_kernel<T, OP, false, true>), g, blk, 0, s, a);                   \
+    } else {                                                                                               \
+      if (nt) hipLaunchKernelGGL((step_merged_kernel<T, OP, true, false>), g, blk, 0, s, a);                \
+      else hipLaunchKernelGGL((step_merged_kernel<T, OP, false, false>), g, blk, 0, s, a);                  \
+    }                                                                                                      \
+  } while (0)
+  if (dtype == 0) {
+    if (op == 0) AR_MERGED(int32_t, 0);
+    else AR_MERGED(int32_t, 1);
+  } else {
+    if (op == 0) AR_MERGED(float, 0);
+    else AR_MERGED(float, 1);
+  }
+#undef AR_MERGED
+  return int(hipGetLastError());
+}
 
 int step_grid(int64_t total_tiles) {
   int64_t blocks = (total_tiles + kWavesPerBlock - 1) / kWavesPerBlock;

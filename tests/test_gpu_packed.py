@@ -1,4 +1,5 @@
-"""Packed column tiles against blocked ones, on the GPU, through the C ABI.
+"""Packed column tiles against blocked ones, and merged step launches against
+block-by-block ones, on the GPU, through the C ABI.
 
 When blocks are short (many small instances), a column-fused wave takes one
 block of several instances instead of one block of one instance, so that
@@ -127,3 +128,47 @@ def test_random_short_block_batches(P, n, B, stride, k, group, schedule, op, mon
     elements), batch sizes and strides, under the default and with flat
     columns forced on and off: the oracle's bits every time."""
     test_packed_and_blocked_tiles_agree_with_oracle(P, n, B, stride, k, group, schedule, op, monkeypatch)
+
+
+# ---------------------------------------------------------------------------
+# Step-wise path: merged runs of blocks (AR_STEP_MERGE)
+# ---------------------------------------------------------------------------
+
+MERGE_CASES = _random_cases(30, 20261203) + [
+    (37, 40000, 2, 40007, 9, "cyclic", "butterfly", "sum"),   # blocks of 1081: block tiles by default
+    (24, 5000, 3, 5003, 7, "cyclic", "butterfly", "isum"),    # shifted, blocks of 208
+    (64, 9000, 2, 9000, 9, "xor", "butterfly", "sum"),        # XOR hybrid, aligned ranges
+    (2, 100, 5, 100, 1, "cyclic", "butterfly", "sum"),        # P = 2, k = 1: the local copy launch
+    (13, 13 * 64, 4, 13 * 64 + 1, 8, "cyclic", "butterfly", "max"),
+]
+
+
+@pytest.mark.parametrize("P,n,B,stride,k,group,schedule,op", MERGE_CASES)
+def test_stepwise_merged_runs_agree_with_oracle(P, n, B, stride, k, group, schedule, op, monkeypatch):
+    """One step launch per communication step, with every range streamed as
+    one run of blocks per rank (AR_STEP_MERGE=1), block by block (=0) and by
+    default: the oracle's bits every time, gaps between instances untouched."""
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    rng = np.random.default_rng(P * 7 + n + k)
+    dtype = "int32" if op == "isum" else "float32"
+    if op == "isum":
+        op = "sum"
+        x = rng.integers(-2**31, 2**31, size=(P, B, stride), dtype=np.int64).astype(np.int32)
+    else:
+        x = rng.normal(size=(P, B, stride)).astype(np.float32)
+    want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, op, group=group, schedule=schedule)
+    for merge in ("0", "1", None):
+        if merge is None:
+            monkeypatch.delenv("AR_STEP_MERGE", raising=False)
+        else:
+            monkeypatch.setenv("AR_STEP_MERGE", merge)
+        note("step-wise merge=%s %s/%s P=%d n=%d B=%d k=%d op=%s" % (merge, group, schedule, P, n, B, k, op))
+        plan = ar.Plan(P, n, dtype, op, k, path=ar.AR_PATH_STEPWISE, group=group, schedule=schedule)
+        X = torch.from_numpy(x).to(DEV)
+        plan.batched([X[i] for i in range(P)], B, stride)
+        torch.cuda.synchronize()
+        got = X.cpu().numpy()
+        plan.close()
+        assert np.array_equal(bits(got[:, :, :n]), bits(want)), merge
+        assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), merge
