@@ -11,7 +11,9 @@
 // element -- so the kernel is built for HBM bandwidth: 64-lane waves,
 // 16-byte loads, several loads in flight per lane before the first store,
 // and no LDS (every byte is used exactly once, there is nothing to share
-// across lanes).
+// across lanes).  step_merged_kernel runs the same step for short blocks:
+// each range's run of consecutive blocks of a rank as one flat space, so
+// that batches of small instances fill their waves.
 //
 // The fused kernels are in fused_lo.hip (latency-optimal, small P, no block
 // tiling), fused_col.hpp (column-fused, any P and k) and fused_group.hip
