@@ -187,7 +187,7 @@ enum { AR_KIND_COPY = 0, AR_KIND_REDUCE = 1, AR_KIND_REDUCE2 = 2 };
  * (Secs. 7-9).  Host work only: validates, derives the per-step placement
  * ranges, assigns buffers, proves every launch free of read/write overlap
  * between ranks, and computes the sizes.  No device memory is touched.
- *   P in [1, 128]; n >= 0; k_steps in [ceil(log2 P), 2*ceil(log2 P)]
+ *   P in [1, 128]; n in [0, 2^46]; k_steps in [ceil(log2 P), 2*ceil(log2 P)]
  *   (k_steps = 0 for P = 1); dtype/op from the enums above.
  * Errors: AR_ERR_INVALID_ARG (range), AR_ERR_UNSUPPORTED (dtype/op),
  * AR_ERR_INTERNAL (consistency check failed).  *out_plan is set on AR_OK. */
@@ -222,7 +222,8 @@ ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t strea
 
 /* `batch` independent Allreduce instances per rank: instance j of rank x is
  * the n elements at rank_buffers[x] + j * instance_stride (in elements,
- * instance_stride >= n).  Each instance is split into blocks on its own. */
+ * instance_stride >= n, (batch - 1) * instance_stride + n <= 2^46, else
+ * AR_ERR_INVALID_ARG).  Each instance is split into blocks on its own. */
 ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
                              hipStream_t stream);
 

@@ -10,6 +10,10 @@ namespace ar {
 
 constexpr int kMaxP = 128;       // largest supported number of ranks
 constexpr int kMaxRanges = 8;    // placement ranges per launch
+// Largest extent of one rank's buffer, in elements (2^46: 256 TiB of 4-byte
+// elements, far above any device's memory), so that every size derived from
+// it -- bytes, tiles, products with P -- fits in 64-bit arithmetic.
+constexpr int64_t kMaxRankElems = int64_t(1) << 46;
 constexpr int kFusedMaxP = 16;   // largest P of the register-resident fused kernel
 
 enum Buf : int32_t { kBufNone = -1, kBufU = 0, kBufX = 1, kBufY = 2 };

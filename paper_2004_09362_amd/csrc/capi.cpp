@@ -526,6 +526,10 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
   if (batch == 1 && instance_stride < plan->s.n) instance_stride = plan->s.n;
   if (instance_stride < plan->s.n) return fail(AR_ERR_INVALID_ARG, "instance_stride must be >= n");
   if (plan->s.n == 0) return AR_OK;  // nothing is read or written; the pointers may be NULL
+  // one rank's extent, (batch - 1) * instance_stride + n elements, within
+  // kMaxRankElems (n is, and instance_stride >= n >= 1 here)
+  if (batch - 1 > (ar::kMaxRankElems - plan->s.n) / instance_stride)
+    return fail(AR_ERR_INVALID_ARG, "a rank's extent, (batch - 1) * instance_stride + n, exceeds 2^46 elements");
   bool all16 = false;
   ar_status st = check_buffers(plan, rank_buffers, batch, instance_stride, &all16);
   if (st != AR_OK) return st;
@@ -536,8 +540,6 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
     (void)hipGetLastError();
     return fail(AR_ERR_NO_DEVICE, std::string("no usable GPU: ") + hipGetErrorString(he));
   }
-  const int64_t elems = int64_t(plan->s.P) * plan->s.n * batch;
-  if (elems / batch / plan->s.P != plan->s.n) return fail(AR_ERR_INVALID_ARG, "size overflow");
   const bool fused = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok);
   if (fused && plan->fused_kind != kFusedLo) {
     st = run_fused_col(plan, rank_buffers, batch, instance_stride, stream, device);

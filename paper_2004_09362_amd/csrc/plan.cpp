@@ -181,7 +181,7 @@ std::string build_schedule(int32_t P, int64_t n, int32_t k, Schedule* out) {
 std::string build_schedule_ex(int32_t P, int64_t n, int32_t k, int32_t group, int32_t sched, Schedule* out) {
   Schedule s;
   if (P < 1 || P > kMaxP) return "P must be in [1, 128]";
-  if (n < 0) return "n must be >= 0";
+  if (n < 0 || n > kMaxRankElems) return "n must be in [0, 2^46]";
   if (group != kGroupCyclic && group != kGroupXor) return "unknown group";
   if (sched != kSchedButterfly && sched != kSchedRing) return "unknown schedule";
   if (group == kGroupXor && (P & (P - 1)) != 0) return "the XOR group needs a power-of-two P";

@@ -70,6 +70,7 @@ def test_status_strings():
     ((7, 10, "float32", "sum", 2), ar.AR_ERR_INVALID_ARG),
     ((7, 10, "float32", "sum", 7), ar.AR_ERR_INVALID_ARG),
     ((1, 10, "float32", "sum", 1), ar.AR_ERR_INVALID_ARG),
+    ((7, (1 << 46) + 1, "float32", "sum", 4), ar.AR_ERR_INVALID_ARG),   # beyond 2^46 elements per rank
 ])
 def test_plan_create_rejects(args, status):
     with pytest.raises(ar.ArError) as ei:
@@ -110,6 +111,10 @@ def test_execute_argument_errors_before_any_device_work():
     assert ar.lib.ar_execute_batched(p.handle, tbl, 2, 7, None) == ar.AR_ERR_INVALID_ARG
     assert ar.lib.ar_execute(None, tbl, None) == ar.AR_ERR_INVALID_ARG
     assert ar.lib.ar_execute(p.handle, None, None) == ar.AR_ERR_INVALID_ARG
+    # a rank's extent beyond 2^46 elements, including products that overflow 64 bits
+    assert ar.lib.ar_execute_batched(p.handle, tbl, 1 << 40, 1 << 30, None) == ar.AR_ERR_INVALID_ARG
+    assert ar.lib.ar_execute_batched(p.handle, tbl, (1 << 63) - 1, 8, None) == ar.AR_ERR_INVALID_ARG
+    assert ar.lib.ar_execute_batched(p.handle, tbl, (1 << 38) + 1, 1 << 8, None) == ar.AR_ERR_INVALID_ARG
 
 
 def test_trivial_plans_do_nothing():
