@@ -80,6 +80,10 @@ def jobs_for(name, k_arg, group="cyclic", schedule="butterfly", op=None):
 
 
 DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4, "gradsync32": 10, "medium127": 11}
+# Steps of well under a millisecond get more of them, so that the timed
+# region spans tens of milliseconds (prime3: about 10 us per step).
+DEFAULT_STEPS = {"large": 10, "small_batch": 200, "small_batch127": 100, "medium127": 100, "prime3": 1000}
+DEFAULT_WARMUP = {"large": 2, "small_batch": 20, "small_batch127": 10, "medium127": 10, "prime3": 50}
 
 SHAPES = {
     "small_batch": "small_batch: P in {5,6,7,12}, n=106 fp32 N(0,1), 65536 instances per launch",
@@ -282,8 +286,8 @@ def main():
         copy_probe(args.copy_probe, args.steps or 10)
         return
 
-    steps = args.steps if args.steps is not None else (10 if args.workload == "large" else 20)
-    warmup = args.warmup if args.warmup is not None else (2 if args.workload == "large" else 5)
+    steps = args.steps if args.steps is not None else DEFAULT_STEPS.get(args.workload, 20)
+    warmup = args.warmup if args.warmup is not None else DEFAULT_WARMUP.get(args.workload, 5)
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     if args.schedule == "ring" and args.group != "cyclic":
@@ -337,24 +341,33 @@ def main():
         run_step(s)
     torch.cuda.synchronize()
 
-    # ---- timed region: exactly `steps` steps on the launch stream.  With
-    # several jobs per step, HIP events bracket the dominant job's launch(es)
-    # in every step; with one job, the events around the whole region time it
-    # (no event packets between its back-to-back launches).  The events carry
-    # no system-scope fence (HipEvent) ----
-    per_launch = len(jobs) > 1
-    ev = [(HipEvent(), HipEvent()) for _ in range(steps)] if per_launch else []
+    # ---- timed region: exactly `steps` steps on the launch stream, between
+    # two HIP events and nothing else.  The events carry no system-scope fence
+    # (HipEvent) ----
     start, stop = HipEvent(), HipEvent()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start.record(stream)
     for s in range(steps):
-        run_step(warmup + s, ev[s] if per_launch else None)
+        run_step(warmup + s)
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     total_ms = start.elapsed_time(stop)
-    dom_ms = sum(a.elapsed_time(b) for a, b in ev) / steps if per_launch else total_ms / steps
+    # ---- the dominant kernel's launch time.  With one job the region above
+    # times it.  With several, a second pass of `steps` steps brackets the
+    # dominant job's launch(es) with events in every step; kept out of the
+    # region above, whose step time the event packets would raise (by about
+    # 11 us in a 270 us step of four launches) ----
+    per_launch = len(jobs) > 1
+    if per_launch:
+        ev = [(HipEvent(), HipEvent()) for _ in range(steps)]
+        for s in range(steps):
+            run_step(warmup + steps + s, ev[s])
+        torch.cuda.synchronize()
+        dom_ms = sum(a.elapsed_time(b) for a, b in ev) / steps
+    else:
+        dom_ms = total_ms / steps
 
     eff_bytes = sum(j["P"] * j["n"] * j["batch"] * j["dtype"].itemsize for j in jobs)
     ms_per_step = total_ms / steps
@@ -389,7 +402,8 @@ def main():
             "traffic": traffic_from_profiles(traffic_key(args.workload, args.group, args.schedule), kname, src_hash),
             "kernel": kname, "job_P": dj["P"], "bytes_per_launch": int(bytes_per_launch),
             "launch_ms": round(launch_ms, 5), "launches_per_step": launches,
-            "timed_by": "HIP events around each launch" if per_launch else "HIP events around the timed region"}
+            "timed_by": ("HIP events around each launch, in a second pass of the same steps" if per_launch
+                         else "HIP events around the timed region")}
     step_alg = sum(alg_bytes(j, p)[0] for j, p in zip(jobs, plans))
 
     desc = describe(args.workload, jobs, args.group, args.schedule)

@@ -492,11 +492,13 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
     else pl->fused_cap = P >= 64 ? 0 : 3;
     pl->bcast_cap = P >= kBcastStreamMinP ? 1 : 2;
     // AR_FUSED_CAP = N caps both launches, "N,M" the fused one and the broadcast
+    // (values clamped to [0, 64]; 0 means no cap)
+    auto cap_of = [](const char* str) { return int32_t(std::min(std::strtol(str, nullptr, 10), 64L)); };
     const char* ce = std::getenv("AR_FUSED_CAP");
     if (ce != nullptr && ce[0] >= '0' && ce[0] <= '9') {
-      pl->fused_cap = pl->bcast_cap = std::atoi(ce);
+      pl->fused_cap = pl->bcast_cap = cap_of(ce);
       const char* comma = std::strchr(ce, ',');
-      if (comma != nullptr && comma[1] >= '0' && comma[1] <= '9') pl->bcast_cap = std::atoi(comma + 1);
+      if (comma != nullptr && comma[1] >= '0' && comma[1] <= '9') pl->bcast_cap = cap_of(comma + 1);
     }
   }
   *out_plan = pl;
