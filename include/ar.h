@@ -118,7 +118,9 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   elements);
  *   AR_FUSED_CAP = N or N,M         resident workgroups per CU of the fused
  *                                   launch (and of the broadcast); 0 is no
- *                                   cap (default: per kernel and P). */
+ *                                   cap (default: per kernel and P);
+ *   AR_LOG = 1                      print each plan (ar_plan_dump) to stderr
+ *                                   when it is created. */
 typedef enum { AR_PATH_AUTO = 0, AR_PATH_STEPWISE = 1, AR_PATH_FUSED = 2 } ar_path;
 
 typedef struct ar_plan ar_plan; /* opaque; owned by the caller between create and destroy */
@@ -227,12 +229,36 @@ ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t strea
 ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
                              hipStream_t stream);
 
+/* Per-launch timing, for debugging and for measuring the per-step cost that
+ * the model of Sec. 2 prices (alpha + beta*m + gamma*m per step).  As
+ * ar_execute_batched, and in addition a timing-only HIP event (no
+ * system-scope fence) is recorded on `stream` before the first launch and
+ * after each launch.  The call then waits for the last event, so it returns
+ * once the Allreduce has finished on the device.  The duration of launch i,
+ * in milliseconds, is stored in launch_ms[i] for i < cap, and the number of
+ * launches in *n_launches (0 when n = 0 or P = 1).  The events put a packet
+ * between launches (a few microseconds each), so their sum exceeds the time
+ * of an untimed execute by about that much.  Errors as ar_execute_batched;
+ * AR_ERR_INVALID_ARG for a NULL n_launches, cap < 0, or a NULL launch_ms
+ * with cap > 0; AR_ERR_HIP when an event call fails. */
+ar_status ar_execute_timed(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
+                           hipStream_t stream, float* launch_ms, int32_t cap, int32_t* n_launches);
+
 /* Sizes of the plan; AR_ERR_INVALID_ARG for NULL arguments. */
 ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out);
 
 /* Introspection of the STEPWISE launches (host side, for tests and tools):
  * number of launches, and launch i's description with up to `cap` ranges. */
 ar_status ar_plan_num_launches(const ar_plan* plan, int32_t* out);
+
+/* The plan as text: P, n, k, L, r, w, the step and block counts, the FUSED
+ * path's kernel and choices, and the STEPWISE launch tables, one line per
+ * launch.  Writes at most cap - 1 characters and a NUL into buf (nothing
+ * when cap = 0), and the full length, without the NUL, into *len.  With
+ * AR_LOG=1 in the environment, plan creation prints the same text to stderr.
+ * AR_ERR_INVALID_ARG for a NULL plan or len, cap < 0, or a NULL buf with
+ * cap > 0. */
+ar_status ar_plan_dump(const ar_plan* plan, char* buf, int64_t cap, int64_t* len);
 ar_status ar_plan_launch(const ar_plan* plan, int32_t i, ar_launch_desc* desc, ar_range_desc* ranges, int32_t cap);
 
 /* Cost model (Sec. 2: a message of m bytes costs alpha + beta*m to send and

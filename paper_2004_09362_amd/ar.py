@@ -30,7 +30,7 @@ AR_SCHEDULE_BUTTERFLY, AR_SCHEDULE_RING = 0, 1
 EXPORTS = [
     "ar_plan_create", "ar_plan_create_ex", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
     "ar_plan_num_launches", "ar_plan_launch", "ar_plan_destroy", "ar_status_string", "ar_last_error",
-    "ar_model_time", "ar_model_best_k", "ar_plan_model_time",
+    "ar_model_time", "ar_model_best_k", "ar_plan_model_time", "ar_execute_timed", "ar_plan_dump",
 ]
 
 
@@ -85,6 +85,9 @@ def _load():
     L.ar_plan_stats.argtypes = [vp, ctypes.POINTER(Stats)]
     L.ar_plan_num_launches.argtypes = [vp, ctypes.POINTER(i32)]
     L.ar_plan_launch.argtypes = [vp, i32, ctypes.POINTER(LaunchDesc), ctypes.POINTER(RangeDesc), i32]
+    L.ar_plan_dump.argtypes = [vp, ctypes.c_char_p, i64, ctypes.POINTER(i64)]
+    L.ar_execute_timed.argtypes = [vp, ctypes.POINTER(vp), i64, i64, vp, ctypes.POINTER(ctypes.c_float), i32,
+                                   ctypes.POINTER(i32)]
     L.ar_plan_destroy.argtypes = [vp]
     L.ar_plan_destroy.restype = None
     dbl = ctypes.c_double
@@ -96,7 +99,8 @@ def _load():
     L.ar_last_error.argtypes = []
     L.ar_last_error.restype = ctypes.c_char_p
     for name in ("ar_plan_create", "ar_plan_create_ex", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
-                 "ar_plan_num_launches", "ar_plan_launch", "ar_model_time", "ar_model_best_k", "ar_plan_model_time"):
+                 "ar_plan_num_launches", "ar_plan_launch", "ar_model_time", "ar_model_best_k", "ar_plan_model_time",
+                 "ar_plan_dump", "ar_execute_timed"):
         getattr(L, name).restype = ctypes.c_int
     return L
 
@@ -185,6 +189,28 @@ def ar_execute_batched(plan: int, rank_buffers: Sequence, batch: int, instance_s
     _check(lib.ar_execute_batched(plan, tbl, batch, instance_stride, _stream_handle(stream)), "ar_execute_batched")
 
 
+def ar_execute_timed(plan: int, rank_buffers: Sequence, batch: int = 1, instance_stride: int | None = None,
+                     stream=None) -> list:
+    """Execute, then wait for it; returns each launch's duration in ms."""
+    tbl = _ptr_table(rank_buffers)
+    st = ar_plan_stats(plan)
+    cap = max(st.launches, st.fused_launches, 1)  # launches of either path
+    ms = (ctypes.c_float * cap)()
+    n = ctypes.c_int32()
+    stride = instance_stride if instance_stride is not None else st.n
+    _check(lib.ar_execute_timed(plan, tbl, batch, stride, _stream_handle(stream), ms, cap, ctypes.byref(n)),
+           "ar_execute_timed")
+    return list(ms[:min(n.value, cap)])
+
+
+def ar_plan_dump(plan: int) -> str:
+    n = ctypes.c_int64()
+    _check(lib.ar_plan_dump(plan, None, 0, ctypes.byref(n)), "ar_plan_dump")
+    buf = ctypes.create_string_buffer(n.value + 1)
+    _check(lib.ar_plan_dump(plan, buf, n.value + 1, ctypes.byref(n)), "ar_plan_dump")
+    return buf.value.decode()
+
+
 def ar_plan_stats(plan: int) -> Stats:
     s = Stats()
     _check(lib.ar_plan_stats(plan, ctypes.byref(s)), "ar_plan_stats")
@@ -255,6 +281,13 @@ class Plan:
 
     def batched(self, rank_buffers, batch: int, instance_stride: int, stream=None):
         ar_execute_batched(self.handle, rank_buffers, batch, instance_stride, stream)
+
+    def timed(self, rank_buffers, batch: int = 1, instance_stride: int | None = None, stream=None) -> list:
+        """Execute and wait; the duration of each launch in milliseconds."""
+        return ar_execute_timed(self.handle, rank_buffers, batch, instance_stride, stream)
+
+    def dump(self) -> str:
+        return ar_plan_dump(self.handle)
 
     def close(self):
         if self.handle:

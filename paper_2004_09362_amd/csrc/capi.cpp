@@ -250,8 +250,34 @@ bool use_nt(int32_t mode, int64_t bytes, int64_t threshold = kNtThresholdBytes) 
   return mode == 1 || (mode < 0 && bytes >= threshold);
 }
 
+// Timing-only HIP events (no system-scope fence) recorded on the launch
+// stream before the first launch of an execute and after each launch
+// (ar_execute_timed).  The first failure is kept; the events are destroyed
+// with the timer.
+struct LaunchTimer {
+  hipStream_t stream = nullptr;
+  std::vector<hipEvent_t> ev;
+  hipError_t err = hipSuccess;
+  void mark() {
+    if (err != hipSuccess) return;
+    hipEvent_t e = nullptr;
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
+    if (r == hipSuccess) {
+      ev.push_back(e);
+      r = hipEventRecord(e, stream);
+    }
+    if (r != hipSuccess) err = r;
+  }
+  ~LaunchTimer() {
+    for (hipEvent_t e : ev) (void)hipEventDestroy(e);
+  }
+  LaunchTimer() = default;
+  LaunchTimer(const LaunchTimer&) = delete;
+  LaunchTimer& operator=(const LaunchTimer&) = delete;
+};
+
 ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool vec, hipStream_t stream,
-                       int device) {
+                       int device, LaunchTimer* tm) {
   const ar::Schedule& s = pl->s;
   ar::StepArgs a;
   std::memset(&a, 0, sizeof a);
@@ -279,6 +305,7 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   const int64_t tps = std::max<int64_t>(1, (max_len + 32 + tile - 1) / tile);
   a.tps = ar::make_fastdiv(uint32_t(std::min<int64_t>(tps, INT32_MAX)));
   a.batch = ar::make_fastdiv(uint32_t(std::min<int64_t>(batch, INT32_MAX)));
+  if (tm) tm->mark();
   for (const ar::Launch& l : s.launches) {
     a.n_ranges = int32_t(l.ranges.size());
     int32_t first = 0;
@@ -321,6 +348,7 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
         a.total_tiles = uint32_t(total);
         const int e = ar::launch_step_merged(a, pl->dtype, pl->op, nt, ar::step_grid(total), stream);
         if (e != 0) return hip_fail(hipError_t(e), "merged step kernel launch");
+        if (tm) tm->mark();
         continue;
       }
     }
@@ -331,12 +359,13 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
     const int grid = ar::step_grid(total_tiles);
     const int e = ar::launch_step(a, pl->dtype, pl->op, vec, nt, grid, stream);
     if (e != 0) return hip_fail(hipError_t(e), "step kernel launch");
+    if (tm) tm->mark();
   }
   return AR_OK;
 }
 
 ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool all16, hipStream_t stream,
-                       int device) {
+                       int device, LaunchTimer* tm) {
   const ar::Schedule& s = pl->s;
   ar::FusedArgs a;
   std::memset(&a, 0, sizeof a);
@@ -353,13 +382,15 @@ ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   blocks = std::min<int64_t>(std::max<int64_t>(blocks, 1), int64_t(1) << 22);
   const bool nt = mode != 2 && use_nt(pl->fused_nt_mode, int64_t(2) * s.P * cols * 4, kFusedNtThresholdBytes);
   a.lds = cap_lds(pl->fused_cap, device);
+  if (tm) tm->mark();
   const int e = ar::launch_fused_lo(a, s.P, pl->dtype, pl->op, mode, nt, int(blocks), stream);
   if (e != 0) return hip_fail(hipError_t(e), "fused latency-optimal kernel launch");
+  if (tm) tm->mark();
   return AR_OK;
 }
 
 ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, hipStream_t stream,
-                        int device) {
+                        int device, LaunchTimer* tm) {
   // one ColArgs layout for every column kernel; the XOR kernel reads the
   // first P entries of the rank table, the others a rotation of it
   const ar::Schedule& s = pl->s;
@@ -413,12 +444,14 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   const bool nt = use_nt(pl->fused_nt_mode, int64_t(2) * s.P * s.n * batch * 4, kFusedNtThresholdBytes);
   const int grid = ar::step_grid(a.total_tiles);
   a.lds = cap_lds(pl->fused_cap, device);
+  if (tm) tm->mark();
   int e;
   if (pl->fused_kind == kFusedXor) e = ar::launch_fused_xor(a, s.P, pl->dtype, pl->op, nt, grid, stream);
   else if (flat_short) e = ar::launch_fused_rot_any(a, s.P, pl->dtype, pl->op, pl->fused_kind == kFusedRing, grid, stream);
   else if (pl->fused_kind == kFusedRing) e = ar::launch_fused_ring(a, pl->dtype, pl->op, nt, grid, stream);
   else e = ar::launch_fused_col_any(a, s.P, pl->dtype, pl->op, nt, grid, stream);
   if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");
+  if (tm) tm->mark();
   if (pl->fused_split) {
     a.lds = cap_lds(pl->bcast_cap, device);
     const bool bnt = pl->bcast_nt_mode == 1 ||
@@ -426,10 +459,95 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
                       int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes);
     e = ar::launch_broadcast(a, pl->dtype, bnt, grid, stream);
     if (e != 0) return hip_fail(hipError_t(e), "broadcast kernel launch");
+    if (tm) tm->mark();
   }
   return AR_OK;
 }
 
+ar_status execute_impl(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
+                       hipStream_t stream, LaunchTimer* tm) {
+  if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
+  if (!rank_buffers) return fail(AR_ERR_INVALID_ARG, "rank_buffers is NULL");
+  if (batch < 1) return fail(AR_ERR_INVALID_ARG, "batch must be >= 1");
+  if (batch == 1 && instance_stride < plan->s.n) instance_stride = plan->s.n;
+  if (instance_stride < plan->s.n) return fail(AR_ERR_INVALID_ARG, "instance_stride must be >= n");
+  if (plan->s.n == 0) return AR_OK;  // nothing is read or written; the pointers may be NULL
+  // one rank's extent, (batch - 1) * instance_stride + n elements, within
+  // kMaxRankElems (n is, and instance_stride >= n >= 1 here)
+  if (batch - 1 > (ar::kMaxRankElems - plan->s.n) / instance_stride)
+    return fail(AR_ERR_INVALID_ARG, "a rank's extent, (batch - 1) * instance_stride + n, exceeds 2^46 elements");
+  bool all16 = false;
+  ar_status st = check_buffers(plan, rank_buffers, batch, instance_stride, &all16);
+  if (st != AR_OK) return st;
+  if (plan->s.P == 1) return AR_OK;  // nothing to combine
+  int device = -1;
+  hipError_t he = hipGetDevice(&device);
+  if (he != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(AR_ERR_NO_DEVICE, std::string("no usable GPU: ") + hipGetErrorString(he));
+  }
+  const bool fused = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok);
+  if (fused && plan->fused_kind != kFusedLo) {
+    st = run_fused_col(plan, rank_buffers, batch, instance_stride, stream, device, tm);
+  } else if (fused) {
+    st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream, device, tm);
+  } else {
+    const bool vec = all16 && (batch == 1 || instance_stride % 4 == 0);
+    st = run_stepwise(plan, rank_buffers, batch, instance_stride, vec, stream, device, tm);
+  }
+  if (st == AR_OK) {
+    plan->last_stream = stream;
+    plan->ran = true;
+  }
+  return st;
+}
+
+
+// The plan as text (ar_plan_dump, AR_LOG=1): sizes, path choices and the
+// step-wise launch tables.
+std::string plan_text(const ar_plan* pl) {
+  const ar::Schedule& s = pl->s;
+  const bool xorg = s.group == ar::kGroupXor;
+  std::string out;
+  char line[256];
+  auto add = [&out, &line](int len) {
+    if (len > 0) out.append(line, size_t(std::min<int>(len, int(sizeof line) - 1)));
+  };
+  static const char* const kBuf[] = {"U", "X", "Y"};
+  auto buf = [](int32_t b) { return b >= 0 && b <= 2 ? kBuf[b] : "-"; };
+  add(std::snprintf(line, sizeof line, "ar_plan P=%d n=%lld dtype=%s op=%s group=%s schedule=%s k=%d L=%d r=%d w=%d\n",
+                    s.P, (long long)s.n, pl->dtype == AR_INT32 ? "int32" : "float32", pl->op == AR_SUM ? "sum" : "max",
+                    xorg ? "xor" : "cyclic", s.sched == ar::kSchedRing ? "ring" : "butterfly", s.k, s.L, s.r, s.w));
+  add(std::snprintf(line, sizeof line,
+                    "  steps: %d reduction + %d distribution; per rank and instance: %lld blocks pulled, %lld "
+                    "combines; step-wise HBM %lld blocks, scratch %s\n",
+                    s.rs_steps, s.ag_steps, (long long)s.blocks_pulled_per_rank, (long long)s.combines_per_rank,
+                    (long long)s.hbm_blocks, s.uses_scratch ? "yes" : "no"));
+  static const char* const kKind[] = {"none", "latency-optimal, registers", "cyclic butterfly columns", "XOR group columns",
+                                      "Ring columns"};
+  add(std::snprintf(line, sizeof line,
+                    "  fused: %s; flat short blocks %s; split %s; caps %d/%d; path %s\n",
+                    kKind[pl->fused_kind], pl->fused_flat ? "yes" : "no", pl->fused_split ? "yes" : "no", pl->fused_cap,
+                    pl->bcast_cap,
+                    pl->path == AR_PATH_STEPWISE ? "stepwise" : pl->path == AR_PATH_FUSED ? "fused" : "auto"));
+  static const char* const kPhase[] = {"reduce", "distribute", "local copy"};
+  static const char* const kRange[] = {"copy", "reduce", "reduce2"};
+  for (size_t i = 0; i < s.launches.size(); ++i) {
+    const ar::Launch& l = s.launches[i];
+    add(std::snprintf(line, sizeof line, "  launch %zu (%s):", i, l.phase >= 0 && l.phase <= 2 ? kPhase[l.phase] : "?"));
+    for (const ar::Range& r : l.ranges) {
+      add(std::snprintf(line, sizeof line, xorg ? " [p %d..%d %s from x^%d: %s" : " [p %d..%d %s from x%+d: %s", r.p0,
+                        r.p0 + r.count - 1, r.kind >= 0 && r.kind <= 2 ? kRange[r.kind] : "?", r.delta, buf(r.dst)));
+      if (r.kind == ar::kCopy) add(std::snprintf(line, sizeof line, " = %s", buf(r.src)));
+      else add(std::snprintf(line, sizeof line, " = %s (+) %s", buf(r.own), buf(r.src)));
+      if (r.kind == ar::kReduce2)
+        add(std::snprintf(line, sizeof line, ", %s = %s (+) %s", buf(r.dst2), buf(r.own2), buf(r.src)));
+      out += ']';
+    }
+    out += '\n';
+  }
+  return out;
+}
 }  // namespace
 
 extern "C" {
@@ -501,6 +619,7 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
       if (comma != nullptr && comma[1] >= '0' && comma[1] <= '9') pl->bcast_cap = cap_of(comma + 1);
     }
   }
+  if (env_mode("AR_LOG") == 1) std::fputs(plan_text(pl).c_str(), stderr);
   *out_plan = pl;
   g_err.clear();
   return AR_OK;
@@ -522,44 +641,35 @@ ar_status ar_plan_set_path(ar_plan* plan, ar_path path) {
 
 ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
                              hipStream_t stream) {
-  if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
-  if (!rank_buffers) return fail(AR_ERR_INVALID_ARG, "rank_buffers is NULL");
-  if (batch < 1) return fail(AR_ERR_INVALID_ARG, "batch must be >= 1");
-  if (batch == 1 && instance_stride < plan->s.n) instance_stride = plan->s.n;
-  if (instance_stride < plan->s.n) return fail(AR_ERR_INVALID_ARG, "instance_stride must be >= n");
-  if (plan->s.n == 0) return AR_OK;  // nothing is read or written; the pointers may be NULL
-  // one rank's extent, (batch - 1) * instance_stride + n elements, within
-  // kMaxRankElems (n is, and instance_stride >= n >= 1 here)
-  if (batch - 1 > (ar::kMaxRankElems - plan->s.n) / instance_stride)
-    return fail(AR_ERR_INVALID_ARG, "a rank's extent, (batch - 1) * instance_stride + n, exceeds 2^46 elements");
-  bool all16 = false;
-  ar_status st = check_buffers(plan, rank_buffers, batch, instance_stride, &all16);
-  if (st != AR_OK) return st;
-  if (plan->s.P == 1) return AR_OK;  // nothing to combine
-  int device = -1;
-  hipError_t he = hipGetDevice(&device);
-  if (he != hipSuccess) {
-    (void)hipGetLastError();
-    return fail(AR_ERR_NO_DEVICE, std::string("no usable GPU: ") + hipGetErrorString(he));
-  }
-  const bool fused = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok);
-  if (fused && plan->fused_kind != kFusedLo) {
-    st = run_fused_col(plan, rank_buffers, batch, instance_stride, stream, device);
-  } else if (fused) {
-    st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream, device);
-  } else {
-    const bool vec = all16 && (batch == 1 || instance_stride % 4 == 0);
-    st = run_stepwise(plan, rank_buffers, batch, instance_stride, vec, stream, device);
-  }
-  if (st == AR_OK) {
-    plan->last_stream = stream;
-    plan->ran = true;
-  }
-  return st;
+  return execute_impl(plan, rank_buffers, batch, instance_stride, stream, nullptr);
 }
 
 ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t stream) {
   return ar_execute_batched(plan, rank_buffers, 1, plan ? plan->s.n : 0, stream);
+}
+
+ar_status ar_execute_timed(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
+                           hipStream_t stream, float* launch_ms, int32_t cap, int32_t* n_launches) {
+  if (!n_launches) return fail(AR_ERR_INVALID_ARG, "n_launches is NULL");
+  if (cap < 0 || (cap > 0 && !launch_ms)) return fail(AR_ERR_INVALID_ARG, "launch_ms is NULL or cap < 0");
+  *n_launches = 0;
+  LaunchTimer tm;
+  tm.stream = stream;
+  ar_status st = execute_impl(plan, rank_buffers, batch, instance_stride, stream, &tm);
+  if (st != AR_OK) return st;
+  if (tm.err != hipSuccess) return hip_fail(tm.err, "timing event");
+  if (tm.ev.empty()) return AR_OK;  // nothing was launched (n = 0 or P = 1)
+  hipError_t e = hipEventSynchronize(tm.ev.back());
+  if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+  const int32_t n = int32_t(tm.ev.size()) - 1;
+  for (int32_t i = 0; i < n && i < cap; ++i) {
+    float ms = 0.0f;
+    e = hipEventElapsedTime(&ms, tm.ev[size_t(i)], tm.ev[size_t(i) + 1]);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    launch_ms[i] = ms;
+  }
+  *n_launches = n;
+  return AR_OK;
 }
 
 ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
@@ -611,6 +721,19 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
   out->workspace_bytes = s.uses_scratch ? int64_t(2) * s.P * round_up(s.n, 64) * 4 : 0;
   out->group = s.group;
   out->schedule = s.sched;
+  return AR_OK;
+}
+
+ar_status ar_plan_dump(const ar_plan* plan, char* buf, int64_t cap, int64_t* len) {
+  if (!plan || !len) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+  if (cap < 0 || (cap > 0 && !buf)) return fail(AR_ERR_INVALID_ARG, "buf is NULL or cap < 0");
+  const std::string t = plan_text(plan);
+  *len = int64_t(t.size());
+  if (cap > 0) {
+    const size_t k = std::min<size_t>(t.size(), size_t(cap - 1));
+    std::memcpy(buf, t.data(), k);
+    buf[k] = 0;
+  }
   return AR_OK;
 }
 

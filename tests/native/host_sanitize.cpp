@@ -21,8 +21,10 @@
 //     buffers, sizes that would overflow, no device, a failed scratch
 //     allocation (also on regrowth), a failed launch -- and that the plan
 //     keeps working afterwards;
-//   - device scratch is freed: every fake allocation is released by the
-//     time its plan is destroyed.
+//   - the text dump and the timed execute, into exactly sized buffers;
+//   - device scratch and timing events are freed: every fake allocation is
+//     released by the time its plan is destroyed, every event by the end of
+//     its execute.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -86,6 +88,41 @@ hipError_t hipGetLastError(void) {
   return e;
 }
 const char* hipGetErrorString(hipError_t e) { return e == hipSuccess ? "no error" : "fake HIP error"; }
+// Events: heap objects, so that one never destroyed is a leak; a record
+// stamps the next tick of a fake clock (0.01 ms per tick).
+namespace fake {
+struct Event {
+  int64_t stamp = -1;
+};
+int64_t clock = 0, live_events = 0;
+bool event_fails = false;
+}  // namespace fake
+hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned flags) {
+  if (fake::event_fails) return fake::last = hipErrorOutOfMemory;
+  if (flags != hipEventDisableSystemFence) return fake::last = hipErrorInvalidValue;
+  *e = reinterpret_cast<hipEvent_t>(new fake::Event);
+  ++fake::live_events;
+  return hipSuccess;
+}
+hipError_t hipEventRecord(hipEvent_t e, hipStream_t) {
+  if (!e) return fake::last = hipErrorInvalidHandle;
+  reinterpret_cast<fake::Event*>(e)->stamp = ++fake::clock;
+  return hipSuccess;
+}
+hipError_t hipEventSynchronize(hipEvent_t e) { return e ? hipSuccess : hipErrorInvalidHandle; }
+hipError_t hipEventElapsedTime(float* ms, hipEvent_t a, hipEvent_t b) {
+  const auto* ea = reinterpret_cast<fake::Event*>(a);
+  const auto* eb = reinterpret_cast<fake::Event*>(b);
+  if (!ea || !eb || ea->stamp < 0 || eb->stamp < 0) return hipErrorInvalidHandle;
+  *ms = float(eb->stamp - ea->stamp) * 0.01f;
+  return hipSuccess;
+}
+hipError_t hipEventDestroy(hipEvent_t e) {
+  if (!e) return hipErrorInvalidHandle;
+  delete reinterpret_cast<fake::Event*>(e);
+  --fake::live_events;
+  return hipSuccess;
+}
 hipError_t hipDeviceGetAttribute(int* v, hipDeviceAttribute_t attr, int device) {
   if (device != 0) return hipErrorInvalidDevice;
   if (attr == hipDeviceAttributeMaxSharedMemoryPerMultiprocessor) *v = 160 * 1024;
@@ -350,6 +387,19 @@ static void exercise(int P, int64_t n, int k, int group, int sched, int dtype, i
   }
   double t = -1;
   EXPECT(ar_plan_model_time(pl, 2e-6, 1e-10, 1e-11, &t) == AR_OK && t >= 0, "%s: model time", what);
+  {  // the text dump: header, two summary lines and one line per launch, into exactly sized buffers
+    int64_t len = -1, len2 = -1;
+    EXPECT(ar_plan_dump(pl, nullptr, 0, &len) == AR_OK && len > 0, "%s: dump length", what);
+    char* full = new char[size_t(len) + 1];
+    EXPECT(ar_plan_dump(pl, full, len + 1, &len2) == AR_OK && len2 == len && int64_t(std::strlen(full)) == len,
+           "%s: dump", what);
+    EXPECT(std::count(full, full + len, '\n') == 3 + nl, "%s: dump lines", what);
+    char* part = new char[7];
+    EXPECT(ar_plan_dump(pl, part, 7, &len2) == AR_OK && std::strlen(part) == 6 && std::strncmp(part, full, 6) == 0,
+           "%s: truncated dump", what);
+    delete[] full;
+    delete[] part;
+  }
   if (n > 0 && n <= 4 * P + 8 && dtype == AR_INT32) replay(pl, P, n, group == AR_GROUP_XOR, op, uint64_t(P) * 7919 + k, what);
 
   // executes on every path; the fake buffers are never dereferenced
@@ -370,6 +420,16 @@ static void exercise(int P, int64_t n, int k, int group, int sched, int dtype, i
       const size_t expect = (n == 0 || P == 1) ? 0 : fused ? size_t(s.fused_launches) : size_t(nl);
       EXPECT(fake::launches.size() == expect, "%s: path %d made %zu launches, stats say %zu", what, path,
              fake::launches.size(), expect);
+      // the timed execute: one duration per launch, into an exactly sized array (cap may be short)
+      const int32_t cap = int32_t(std::min<size_t>(expect, 3));
+      float* ms = new float[size_t(cap) + (cap == 0)];
+      int32_t got = -1;
+      fake::launches.clear();
+      st = ar_execute_timed(pl, bufs.data(), batch, stride, stream_tag(), cap ? ms : nullptr, cap, &got);
+      EXPECT(st == AR_OK && got == int32_t(expect) && fake::launches.size() == expect, "%s: timed execute", what);
+      for (int32_t i = 0; i < cap; ++i) EXPECT(ms[i] > 0.0f, "%s: launch %d timed at %g ms", what, i, ms[i]);
+      EXPECT(fake::live_events == 0, "%s: %lld events left", what, (long long)fake::live_events);
+      delete[] ms;
     }
   }
   ar_plan_destroy(pl);
@@ -405,6 +465,24 @@ static void errors() {
   int32_t k = 0;
   double tau = 0, rc = 0;
   EXPECT(ar_plan_stats(nullptr, &s) == AR_ERR_INVALID_ARG, "stats of NULL");
+  {
+    ar_plan* p3 = nullptr;
+    int64_t len = 0;
+    char b[4];
+    float ms[2];
+    int32_t got = 0;
+    void* bufs3[3] = {reinterpret_cast<void*>(0x10000), reinterpret_cast<void*>(0x20000), reinterpret_cast<void*>(0x30000)};
+    EXPECT(ar_plan_create(3, 8, AR_INT32, AR_SUM, 2, &p3) == AR_OK, "create P=3");
+    EXPECT(ar_plan_dump(nullptr, b, 4, &len) == AR_ERR_INVALID_ARG, "dump of NULL");
+    EXPECT(ar_plan_dump(p3, b, 4, nullptr) == AR_ERR_INVALID_ARG, "dump without len");
+    EXPECT(ar_plan_dump(p3, b, -1, &len) == AR_ERR_INVALID_ARG, "dump cap < 0");
+    EXPECT(ar_plan_dump(p3, nullptr, 4, &len) == AR_ERR_INVALID_ARG, "dump NULL buf with cap");
+    EXPECT(ar_execute_timed(p3, bufs3, 1, 8, nullptr, ms, 2, nullptr) == AR_ERR_INVALID_ARG, "timed without count");
+    EXPECT(ar_execute_timed(p3, bufs3, 1, 8, nullptr, ms, -1, &got) == AR_ERR_INVALID_ARG, "timed cap < 0");
+    EXPECT(ar_execute_timed(p3, bufs3, 1, 8, nullptr, nullptr, 2, &got) == AR_ERR_INVALID_ARG, "timed NULL array");
+    EXPECT(ar_execute_timed(nullptr, bufs3, 1, 8, nullptr, ms, 2, &got) == AR_ERR_INVALID_ARG, "timed NULL plan");
+    ar_plan_destroy(p3);
+  }
   EXPECT(ar_plan_set_path(nullptr, AR_PATH_AUTO) == AR_ERR_INVALID_ARG, "path of NULL");
   EXPECT(ar_execute(nullptr, nullptr, nullptr) == AR_ERR_INVALID_ARG, "execute NULL");
   EXPECT(ar_model_time(0, 1e6, 0, 1, 1, 1, &tau) == AR_ERR_INVALID_ARG, "model P = 0");
@@ -481,6 +559,15 @@ static void execute_errors() {
   EXPECT(ar_execute(pl, bufs.data(), stream_tag()) == AR_ERR_HIP, "fused launch failure");
   fake::launch_error = 0;
   EXPECT(ar_execute(pl, bufs.data(), stream_tag()) == AR_OK, "execute after the launch failure");
+  // a timing event that cannot be created is reported, and no event is left behind
+  fake::event_fails = true;
+  float ms[8];
+  int32_t got = -1;
+  EXPECT(ar_execute_timed(pl, bufs.data(), 1, n, stream_tag(), ms, 8, &got) == AR_ERR_HIP && got == 0,
+         "event failure");
+  fake::event_fails = false;
+  EXPECT(fake::live_events == 0, "events left after a failure");
+  EXPECT(ar_execute_timed(pl, bufs.data(), 1, n, stream_tag(), ms, 8, &got) == AR_OK && got == 1, "timed fused");
   ar_plan_destroy(pl);
   EXPECT(fake::live_allocs == 0, "scratch not freed by destroy");
   // n = 0: nothing is touched, NULL pointers allowed
