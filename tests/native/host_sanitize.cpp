@@ -22,17 +22,22 @@
 //     allocation (also on regrowth), a failed launch -- and that the plan
 //     keeps working afterwards;
 //   - the text dump and the timed execute, into exactly sized buffers;
+//   - with "threads", the same from several threads at once (the mode for
+//     ThreadSanitizer: the error text is per thread, the LDS sizes cached
+//     in atomics);
 //   - device scratch and timing events are freed: every fake allocation is
 //     released by the time its plan is destroyed, every event by the end of
 //     its execute.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "ar.h"
@@ -43,24 +48,25 @@
 // addresses (never dereferenced), failures on request.
 // ---------------------------------------------------------------------------
 
+// The state is per thread (like HIP's last error), so that several threads
+// can drive the library at once; addresses come from one atomic counter.
 namespace fake {
-bool device_ok = true;
-bool malloc_fails = false;
-int launch_error = 0;          // hipError_t value every launcher returns when set
-int64_t live_allocs = 0, total_allocs = 0;
-uintptr_t next_addr = uintptr_t(1) << 44;
-hipError_t last = hipSuccess;
+thread_local bool device_ok = true;
+thread_local bool malloc_fails = false;
+thread_local int launch_error = 0;  // hipError_t value every launcher returns when set
+thread_local int64_t live_allocs = 0, total_allocs = 0;
+std::atomic<uintptr_t> next_addr{uintptr_t(1) << 44};
+thread_local hipError_t last = hipSuccess;
 
 struct Rec {
   const char* kind;
   int P, grid;
   uint32_t total_tiles;
 };
-std::vector<Rec> launches;
-int problems = 0;
+thread_local std::vector<Rec> launches;
+std::atomic<int> problems{0};
 void problem(const char* what, int P) {
-  if (problems < 20) std::printf("LAUNCH CONTRACT: %s (P=%d)\n", what, P);
-  ++problems;
+  if (problems.fetch_add(1) < 20) std::printf("LAUNCH CONTRACT: %s (P=%d)\n", what, P);
 }
 }  // namespace fake
 
@@ -72,8 +78,7 @@ hipError_t hipGetDevice(int* d) {
 hipError_t hipSetDevice(int d) { return d == 0 ? hipSuccess : (fake::last = hipErrorInvalidDevice); }
 hipError_t hipMalloc(void** p, size_t bytes) {
   if (fake::malloc_fails || bytes == 0) return fake::last = hipErrorOutOfMemory;
-  *p = reinterpret_cast<void*>(fake::next_addr);
-  fake::next_addr += (bytes + 0xFFFF) & ~size_t(0xFFFF);
+  *p = reinterpret_cast<void*>(fake::next_addr.fetch_add((bytes + 0xFFFF) & ~size_t(0xFFFF)));
   ++fake::live_allocs;
   ++fake::total_allocs;
   return hipSuccess;
@@ -94,8 +99,8 @@ namespace fake {
 struct Event {
   int64_t stamp = -1;
 };
-int64_t clock = 0, live_events = 0;
-bool event_fails = false;
+thread_local int64_t clock = 0, live_events = 0;
+thread_local bool event_fails = false;
 }  // namespace fake
 hipError_t hipEventCreateWithFlags(hipEvent_t* e, unsigned flags) {
   if (fake::event_fails) return fake::last = hipErrorOutOfMemory;
@@ -255,7 +260,7 @@ int64_t step_tile_elems() { return 256; }
 // The checks
 // ---------------------------------------------------------------------------
 
-static int fails = 0;
+static std::atomic<int> fails{0};
 #define EXPECT(cond, ...)                                     \
   do {                                                        \
     if (!(cond)) {                                            \
@@ -578,14 +583,10 @@ static void execute_errors() {
   ar_plan_destroy(pl);
 }
 
-int main(int argc, char** argv) {
-  std::vector<const void*> keep;
-  ar::keep_launchers<128>(&keep);
-  const int pmax = argc > 1 ? std::atoi(argv[1]) : 128;
-  errors();
-  execute_errors();
+// Every plan of P = first, first + step, ... up to pmax.
+static int sweep(int first, int step, int pmax) {
   int plans = 0;
-  for (int P = 1; P <= pmax; ++P) {
+  for (int P = first; P <= pmax; P += step) {
     const int L = ceil_log2(P);
     const bool pow2 = (P & (P - 1)) == 0;
     std::vector<int64_t> ns = {0, 1, 3 * int64_t(P) + 2, 64 * int64_t(P) + 5, int64_t(1) << 22};
@@ -603,6 +604,34 @@ int main(int argc, char** argv) {
       ++plans;
     }
   }
-  std::printf("%d plans, %d launch contract problems, %d failures\n", plans, fake::problems, fails);
+  return plans;
+}
+
+// argv: [pmax] runs everything on one thread; "threads" T pmax runs the
+// error checks and the sweep on T threads at once (P dealt out round robin),
+// the mode for ThreadSanitizer.
+int main(int argc, char** argv) {
+  std::vector<const void*> keep;
+  ar::keep_launchers<128>(&keep);
+  int plans = 0;
+  if (argc > 1 && std::strcmp(argv[1], "threads") == 0) {
+    const int nt = argc > 2 ? std::atoi(argv[2]) : 8;
+    const int pmax = argc > 3 ? std::atoi(argv[3]) : 40;
+    std::vector<std::thread> th;
+    std::vector<int> counts(size_t(nt), 0);
+    th.emplace_back([] {
+      errors();
+      execute_errors();
+    });
+    for (int t = 0; t < nt; ++t) th.emplace_back([t, nt, pmax, &counts] { counts[size_t(t)] = sweep(1 + t, nt, pmax); });
+    for (std::thread& x : th) x.join();
+    for (int c : counts) plans += c;
+  } else {
+    const int pmax = argc > 1 ? std::atoi(argv[1]) : 128;
+    errors();
+    execute_errors();
+    plans = sweep(1, 1, pmax);
+  }
+  std::printf("%d plans, %d launch contract problems, %d failures\n", plans, fake::problems.load(), fails.load());
   return (fails || fake::problems) ? 1 : 0;
 }

@@ -17,8 +17,9 @@ only; no HIP source is built with a sanitizer:
   summation-order error bound for fp32 sums), the column sampling, the
   batching and the term mode.
 
+host_sanitize.cpp also runs on eight threads at once under ThreadSanitizer.
 Either driver exits non-zero on a failed check, and a sanitizer report
-aborts it (-fno-sanitize-recover).
+aborts it (-fno-sanitize-recover, halt_on_error).
 """
 import os
 import shutil
@@ -48,9 +49,30 @@ def test_library_host_code_under_sanitizers(tmp_path):
     subprocess.run(["g++", "-std=c++17", *SAN, "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROCM, "include"),
                     "-I", os.path.join(ROOT, "include"), "-I", CSRC, "-o", str(exe),
                     os.path.join(NATIVE, "host_sanitize.cpp"), os.path.join(CSRC, "capi.cpp"),
-                    os.path.join(CSRC, "plan.cpp")], check=True)
+                    os.path.join(CSRC, "plan.cpp"), "-pthread"], check=True)
     rc, out = _run(exe)
     assert rc == 0, out[-4000:]
+    assert "0 launch contract problems, 0 failures" in out, out[-4000:]
+
+
+@pytest.mark.skipif(shutil.which("g++") is None, reason="g++ is not installed")
+def test_library_host_code_from_eight_threads_under_thread_sanitizer(tmp_path):
+    """Plans created, dumped, timed and executed (fake runtime) on eight
+    threads at once, with the error checks on a ninth: the error text is
+    per thread and the device LDS sizes are cached in atomics, so
+    ThreadSanitizer must find no race."""
+    if not os.path.exists(os.path.join(ROCM, "include", "hip", "hip_runtime_api.h")):
+        pytest.skip("HIP headers not found")
+    exe = tmp_path / "host_tsan"
+    subprocess.run(["g++", "-std=c++17", "-O1", "-g", "-fsanitize=thread", "-fno-omit-frame-pointer",
+                    "-D__HIP_PLATFORM_AMD__", "-I", os.path.join(ROCM, "include"), "-I", os.path.join(ROOT, "include"),
+                    "-I", CSRC, "-o", str(exe), os.path.join(NATIVE, "host_sanitize.cpp"),
+                    os.path.join(CSRC, "capi.cpp"), os.path.join(CSRC, "plan.cpp"), "-pthread"], check=True)
+    env = dict(os.environ, TSAN_OPTIONS="halt_on_error=1")
+    res = subprocess.run([str(exe), "threads", "8", "48"], capture_output=True, text=True, timeout=600, env=env)
+    out = res.stdout + res.stderr
+    assert res.returncode == 0, out[-4000:]
+    assert "ThreadSanitizer" not in out, out[-4000:]
     assert "0 launch contract problems, 0 failures" in out, out[-4000:]
 
 
