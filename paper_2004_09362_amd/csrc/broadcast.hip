@@ -16,7 +16,9 @@
 // Layout and tiles as in the reducing launch (col_tile_column,
 // device_common.hpp): one wave per 64 columns of one block of one instance,
 // tiles laid on 256-byte boundaries of rank b's buffer, or one short block
-// of several instances per wave.  Loads and stores are nontemporal (NT) or
+// of several instances per wave.  After a reducing launch on flat columns
+// (a.flat: batches of short blocks) every column's result is on rank 0, and
+// the waves take 64 consecutive flat columns each.  Loads and stores are nontemporal (NT) or
 // ordinary: from P = 96 ranks, streaming the P - 1 stores nontemporally at
 // one resident workgroup per CU was 3-4% faster; below, ordinary stores
 // streamed as fast or faster.
@@ -38,9 +40,17 @@ __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
   const int32_t P = a.P;
   for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
        t += gridDim.x * uint32_t(kWavesPerBlock)) {
-    int32_t b;
+    int32_t b = 0;
     int64_t e;
-    const bool live = col_tile_column(a, t, lane, b, e);
+    bool live;
+    if (a.flat) {
+      const uint32_t g = t * uint32_t(kWave) + uint32_t(lane);
+      const uint32_t inst = fdiv(g, a.ndiv);
+      e = int64_t(inst) * a.stride + int64_t(g - inst * a.ndiv.d);
+      live = g < a.flat_cols;
+    } else {
+      live = col_tile_column(a, t, lane, b, e);
+    }
     void* const* rot = a.user + b;  // rot[d] is rank (b + d) mod P
     if (live) {
       const T v = ld1<NT>(static_cast<const T*>(rot[0]) + e);

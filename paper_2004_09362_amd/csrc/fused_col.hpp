@@ -215,8 +215,9 @@ __global__ __launch_bounds__(kBlock) void fused_mid_kernel(const ColArgs a) {
 // that X[p] is placement p's value, V_{b+p}, exactly as the block-tiled
 // kernels read it through rotated pointers.  The fold, the recursion or the
 // chain then combines the same operand pairs in the same order (the same
-// bits).  The
-// bandwidth-optimal result goes to every rank; in the shifted plan rank
+// bits).  The bandwidth-optimal and Ring result goes to every rank (with
+// a.split, to rank 0 alone, and the broadcast copies it); in the shifted
+// plan rank
 // b + q receives S[col_src(q)], so the column of results is rotated back by
 // b and rank y stores slot y.  A rotation by a per-lane amount is a
 // log-depth network of static rotations by 2^j, each applied on the lanes
@@ -288,16 +289,22 @@ __global__ __launch_bounds__(kBlock) void fused_rot_kernel(const ColArgs a) {
 #pragma unroll
       for (int y = 0; y < P; ++y) X[y] = ld1<true>(static_cast<const T*>(a.user[y]) + e);
       rotate_lanes<P, 0, T>(X, b);
-      if constexpr (RR < 0) {
-        T acc = X[0];
+      if constexpr (RR <= 0) {
+        T acc;
+        if constexpr (RR < 0) {
+          acc = X[0];
 #pragma unroll
-        for (int d = 1; d < P; ++d) acc = comb<OP>(X[d], acc);
+          for (int d = 1; d < P; ++d) acc = comb<OP>(X[d], acc);
+        } else {
+          bo_fold<P, OP, T, P>(X);
+          acc = X[0];
+        }
+        if (a.split) {  // every rank receives acc: rank 0 holds it first, the broadcast copies it
+          st1<true>(static_cast<T*>(a.user[0]) + e, acc);
+        } else {
 #pragma unroll
-        for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(a.user[y]) + e, acc);
-      } else if constexpr (RR == 0) {
-        bo_fold<P, OP, T, P>(X);
-#pragma unroll
-        for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(a.user[y]) + e, X[0]);
+          for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(a.user[y]) + e, acc);
+        }
       } else {
         T S[P];
 #pragma unroll

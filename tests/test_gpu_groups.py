@@ -231,24 +231,26 @@ def test_ring_gradsync_shape():
 def test_split_and_single_fused_launch_agree(P, k, group, schedule, monkeypatch):
     """AR_FUSED_SPLIT forces either form, and AR_BCAST_NT either kind of
     broadcast store; all must give the oracle's bits, on a ragged batch with
-    gaps between instances."""
+    gaps between instances, with block tiles and on flat columns
+    (AR_FUSED_ROTATE=1: rank 0 holds every result before the broadcast)."""
     rng = np.random.default_rng(P * 3 + k)
     n, B, stride = 5 * P + 3, 3, 5 * P + 11
     x = rng.normal(size=(P, B, stride)).astype(np.float32)
     want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, "sum", group=group, schedule=schedule)
-    monkeypatch.setenv("AR_FUSED_ROTATE", "0")  # short blocks: keep the block-tiled launches that split
-    for split, bnt in (("0", "0"), ("1", "0"), ("1", "1")):
+    for (rotate, split, bnt) in [(r, s, b) for r in ("0", "1") for s, b in (("0", "0"), ("1", "0"), ("1", "1"))]:
+        monkeypatch.setenv("AR_FUSED_ROTATE", rotate)
         monkeypatch.setenv("AR_FUSED_SPLIT", split)
         monkeypatch.setenv("AR_BCAST_NT", bnt)
         plan = ar.Plan(P, n, "float32", "sum", k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
         assert plan.stats().fused_launches == (2 if split == "1" else 1)
-        note("split=%s broadcast nt=%s %s/%s P=%d k=%d" % (split, bnt, group, schedule, P, k))
+        assert plan.stats().fused_flat == int(rotate == "1")
+        note("flat=%s split=%s broadcast nt=%s %s/%s P=%d k=%d" % (rotate, split, bnt, group, schedule, P, k))
         X = torch.from_numpy(x).to(DEV)
         plan.batched([X[i] for i in range(P)], B, stride)
         torch.cuda.synchronize()
         got = X.cpu().numpy()
-        assert np.array_equal(bits(got[:, :, :n]), bits(want)), split
-        assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), split
+        assert np.array_equal(bits(got[:, :, :n]), bits(want)), (rotate, split, bnt)
+        assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), (rotate, split, bnt)
         plan.close()
 
 

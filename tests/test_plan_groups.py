@@ -176,3 +176,20 @@ def test_random_plans_reproduce_oracle(case):
     st_ = plan.stats()
     assert st_.rs_steps + st_.ag_steps == k
     assert st_.bytes_pulled_total == st_.blocks_pulled_per_rank * n * 4
+
+
+@pytest.mark.parametrize("P,n,k,group,schedule,launches", [
+    (128, 128 * 18, 14, "xor", "butterfly", 2),      # Recursive Halving, flat columns: reduce, then broadcast
+    (64, 64 * 18, 12, "xor", "butterfly", 2),
+    (32, 32 * 18, 10, "xor", "butterfly", 1),        # below 64 ranks: one launch
+    (128, 128 * 18, 10, "xor", "butterfly", 1),      # hybrid: the ranks receive different results
+    (127, 127 * 18, 14, "cyclic", "butterfly", 1),   # rank slots: the split would cost more than it saves
+    (127, 127 * 18, 252, "cyclic", "ring", 1),
+    (127, 127 * 100, 14, "cyclic", "butterfly", 2),  # blocks of 100: block tiles, split
+    (127, 127 * 100, 252, "cyclic", "ring", 2),
+])
+def test_default_split_of_one_result_plans(P, n, k, group, schedule, launches):
+    st = ar.Plan(P, n, "float32", "sum", k, group=group, schedule=schedule).stats()
+    assert st.fused_launches == launches
+    assert st.fused_flat == int(n // P <= 64)
+    assert st.hbm_bytes_fused == (2 * P + (launches == 2)) * n * 4

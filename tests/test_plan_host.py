@@ -207,6 +207,7 @@ def test_plan_sizes_match_oracle_counts(P):
         assert st.fused_launches == (0 if P == 1 else 2 if split else 1)
         # blocks of 10-11 elements: the rank-slot kernel runs these plans in one launch
         assert not split
+        assert st.fused_flat == int(P >= 2 and k > ceil_log2(P))
         big = ar.Plan(P, 100 * P + 3, "float32", "sum", k).stats()
         assert (big.fused_launches == 2) == (P >= 64 and k == 2 * ceil_log2(P))
         assert st.hbm_bytes_fused == ((2 * P + split) * st.n * 4 if P > 1 else 0)
