@@ -65,7 +65,7 @@ constexpr int64_t kMergeMaxLen = 256;
 //   split launches (P = 127): the reducing launch at 3-6, the broadcast at 2
 //     (1 with nontemporal stores, from kBcastStreamMinP ranks up);
 //   flat columns for short blocks (fused_flat): P = 12 at 3-4, P = 24, 32 and
-//     37 at 2 (3-7%); at P = 127 registers allow one wave per SIMD.
+//     37 at 2 (3-7%); none from P = 64 (caps of 1-4 the same or slower).
 // AR_FUSED_CAP = N (both launches) or N,M (fused launch, broadcast) overrides
 // them; 0 is no cap.
 static int32_t lo_cap(int32_t P) { return P <= 4 ? 0 : P == 6 ? 4 : P <= 7 ? 5 : P <= 11 ? 4 : 3; }
@@ -100,9 +100,9 @@ struct ar_plan {
   // Sums whose blocks hold at most kPackMaxLen elements run on flat columns
   // whenever the batch's columns fit in 32 bits: the cyclic butterfly plans
   // with r < L and the Ring in the rank-slot kernel, the XOR group's plans
-  // in its own kernel with the block left out.  Split there (by default in
-  // the XOR group only), the reducing launch stores every column's result
-  // on rank 0 and the broadcast copies it to the others.
+  // in its own kernel with the block left out.  Split there, the reducing
+  // launch stores every column's result on rank 0 and the broadcast copies
+  // it to the others.
   bool fused_flat = false;
   // Occupancy caps (resident workgroups per CU; 0: none) of the fused launch
   // and of the broadcast that follows a split one (AR_FUSED_CAP overrides).
@@ -600,14 +600,7 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
     pl->fused_flat = kind && pl->op == AR_SUM &&
                      (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && max_len <= kPackMaxLen));
   }
-  // On flat columns the split pays only in the XOR group, whose reducing
-  // launch streams at 6.5 TB/s (P = 128, 9 KB messages: the pair 17-20%
-  // faster).  The rank-slot kernel's rotation network makes its reducing
-  // launch cost two thirds of the single launch, and the pair ran 7-18%
-  // slower at P = 96-127 (even at P = 64).
-  const bool split_pays = !pl->fused_flat || pl->fused_kind == kFusedXor;
-  pl->fused_split = one_result && (pl->split_mode == 1 ||
-                                   (pl->split_mode < 0 && pl->s.P >= kSplitMinP && split_pays));
+  pl->fused_split = one_result && (pl->split_mode == 1 || (pl->split_mode < 0 && pl->s.P >= kSplitMinP));
   {
     const int32_t P = pl->s.P;
     if (pl->fused_split) pl->fused_cap = 6;

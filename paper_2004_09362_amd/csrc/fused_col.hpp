@@ -279,6 +279,10 @@ __global__ __launch_bounds__(kBlock) void fused_rot_kernel(const ColArgs a) {
   for (uint32_t t = blockIdx.x * uint32_t(kWavesPerBlock) + wave_in_block; t < a.total_tiles;
        t += gridDim.x * uint32_t(kWavesPerBlock)) {
     const uint32_t g = t * uint32_t(kWave) + uint32_t(lane);
+    // tbl is a.user (t < 2^31); indexing it by t >> 31 keeps the compiler
+    // from hoisting the P rank pointers out of the loop, where they would stay
+    // live across iterations in SGPRs spilled to VGPR lanes
+    void* const* tbl = a.user + (t >> 31);
     if (g < a.flat_cols) {
       const uint32_t inst = fdiv(g, a.ndiv);
       const uint32_t i = g - inst * a.ndiv.d;
@@ -287,7 +291,7 @@ __global__ __launch_bounds__(kBlock) void fused_rot_kernel(const ColArgs a) {
       const int64_t e = int64_t(inst) * a.stride + i;
       T X[P];
 #pragma unroll
-      for (int y = 0; y < P; ++y) X[y] = ld1<true>(static_cast<const T*>(a.user[y]) + e);
+      for (int y = 0; y < P; ++y) X[y] = ld1<true>(static_cast<const T*>(tbl[y]) + e);
       rotate_lanes<P, 0, T>(X, b);
       if constexpr (RR <= 0) {
         T acc;
@@ -300,10 +304,10 @@ __global__ __launch_bounds__(kBlock) void fused_rot_kernel(const ColArgs a) {
           acc = X[0];
         }
         if (a.split) {  // every rank receives acc: rank 0 holds it first, the broadcast copies it
-          st1<true>(static_cast<T*>(a.user[0]) + e, acc);
+          st1<true>(static_cast<T*>(tbl[0]) + e, acc);
         } else {
 #pragma unroll
-          for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(a.user[y]) + e, acc);
+          for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(tbl[y]) + e, acc);
         }
       } else {
         T S[P];
@@ -314,7 +318,7 @@ __global__ __launch_bounds__(kBlock) void fused_rot_kernel(const ColArgs a) {
         rot_gather<P, RR, T>(X, S, std::make_integer_sequence<int, P>{});
         rotate_lanes<P, 0, T>(X, b == 0 ? 0u : uint32_t(P) - b);
 #pragma unroll
-        for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(a.user[y]) + e, X[y]);
+        for (int y = 0; y < P; ++y) st1<true>(static_cast<T*>(tbl[y]) + e, X[y]);
       }
     }
   }

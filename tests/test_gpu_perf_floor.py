@@ -49,9 +49,13 @@ def achieved(P, n, B, k, group, schedule, reps=10):
     ("XOR Recursive Halving P=128, split", 128, 1 << 23, 1, 14, "xor", "butterfly", 0.50),
     ("XOR hybrid P=128", 128, 1 << 23, 1, 10, "xor", "butterfly", 0.50),
     ("Ring P=24", 24, 1 << 23, 1, 46, "cyclic", "ring", 0.55),
-    # short blocks, rank slots on flat columns: 8192 messages of 9 KB at P = 127, k = 11 (blocks of 18
-    # elements), measured 63%; XOR and Ring batches of 4-5-element blocks, 70-79% and 65-70%
-    ("shifted P=127, 8192 x 2304, rank slots", 127, 2304, 8192, 11, "cyclic", "butterfly", 0.45),
+    # short blocks, rank slots on flat columns: 8192 messages of 9 KB at P = 127 (blocks of 18 elements),
+    # measured 66% shifted (k = 11) and 80% split (k = 14, the Ring); the XOR group's Recursive Halving split
+    # at P = 128, 79%; XOR and Ring batches of 4-5-element blocks, 70-79% and 65-70%
+    ("shifted P=127, 8192 x 2304, rank slots", 127, 2304, 8192, 11, "cyclic", "butterfly", 0.55),
+    ("bandwidth-optimal P=127, 8192 x 2304, rank slots, split", 127, 2304, 8192, 14, "cyclic", "butterfly", 0.6),
+    ("Ring P=127, 8192 x 2304, rank slots, split", 127, 2304, 8192, 252, "cyclic", "ring", 0.6),
+    ("XOR Recursive Halving P=128, 8192 x 2304, flat, split", 128, 2304, 8192, 14, "xor", "butterfly", 0.6),
     ("XOR P=32, 65536 x 128, flat", 32, 128, 65536, 10, "xor", "butterfly", 0.50),
     ("Ring P=24, 65536 x 106, rank slots", 24, 106, 65536, 46, "cyclic", "ring", 0.45),
 ])

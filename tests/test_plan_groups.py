@@ -183,8 +183,10 @@ def test_random_plans_reproduce_oracle(case):
     (64, 64 * 18, 12, "xor", "butterfly", 2),
     (32, 32 * 18, 10, "xor", "butterfly", 1),        # below 64 ranks: one launch
     (128, 128 * 18, 10, "xor", "butterfly", 1),      # hybrid: the ranks receive different results
-    (127, 127 * 18, 14, "cyclic", "butterfly", 1),   # rank slots: the split would cost more than it saves
-    (127, 127 * 18, 252, "cyclic", "ring", 1),
+    (127, 127 * 18, 14, "cyclic", "butterfly", 2),   # rank slots, split
+    (127, 127 * 18, 252, "cyclic", "ring", 2),
+    (127, 127 * 18, 11, "cyclic", "butterfly", 1),   # shifted: the ranks receive different results
+    (37, 37 * 18, 12, "cyclic", "butterfly", 1),     # below 64 ranks
     (127, 127 * 100, 14, "cyclic", "butterfly", 2),  # blocks of 100: block tiles, split
     (127, 127 * 100, 252, "cyclic", "ring", 2),
 ])
