@@ -102,10 +102,11 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *   AR_FUSED_SPLIT = 0|1            single fused launch, or reduce plus
  *                                   broadcast where every rank receives the
  *                                   same result (default: split for
- *                                   P >= 64);
+ *                                   P >= 64, and for P >= 33 in the rank-
+ *                                   slot kernel on short blocks);
  *   AR_BCAST_NT = 0|1               nontemporal loads and stores in that
- *                                   broadcast (default: for P >= 96 and
- *                                   large launches);
+ *                                   broadcast (default: for large launches
+ *                                   with P >= 96, or on flat columns);
  *   AR_FUSED_PACKED = 0|1           column launches other than the latency-
  *                                   optimal ones: a wave takes 64 columns of
  *                                   one block of one instance, or one block
@@ -157,7 +158,8 @@ typedef struct {
   int32_t group, schedule;           /* ar_group and ar_schedule of the plan              */
   int32_t fused_launches;            /* FUSED path: 1, or 2 when split into a reducing
                                         launch and a broadcast (every rank receives the
-                                        same result and P >= 64)                          */
+                                        same result and P >= 64; P >= 33 for sums with
+                                        short blocks outside the XOR group)              */
   int32_t fused_flat;                /* FUSED path of a sum with short blocks: 1 when it
                                         runs on flat columns (the rank-slot kernel, or
                                         the XOR group's kernel without the block) for

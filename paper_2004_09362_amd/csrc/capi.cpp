@@ -29,6 +29,12 @@ constexpr int64_t kFusedNtThresholdBytes = int64_t(128) << 20;
 // many ranks up (broadcast.hip): measured faster at P = 64 and 127, slower
 // at P = 24 and 48.
 constexpr int32_t kSplitMinP = 64;
+// Flat short-block sums in the rank-slot kernel (not the XOR group's) split
+// from this many ranks up: their single launch streams 5.0-5.6 TB/s there and
+// the pair up to 6.0 (P = 37: 7%, P = 48: 15% faster with caps 4 and 2 and a
+// nontemporal broadcast; P = 24 even; the Ring at P = 24 and the XOR kernel
+// at P = 32 slower).
+constexpr int32_t kFlatSplitMinP = 33;
 // From this many ranks up the broadcast streams its P - 1 stores
 // nontemporally (at kFusedNtThresholdBytes and above) with one workgroup per
 // CU: 3-4% faster at P = 100-128 than cached stores at two workgroups per CU,
@@ -63,7 +69,8 @@ constexpr int64_t kMergeMaxLen = 256;
 //     one wave per SIMD, and a cap changes nothing;
 //   the Ring at P = 24: 4 (2%);
 //   split launches (P = 127): the reducing launch at 3-6, the broadcast at 2
-//     (1 with nontemporal stores, from kBcastStreamMinP ranks up);
+//     (1 with nontemporal stores, from kBcastStreamMinP ranks up); the
+//     rank-slot kernel's reducing launch below kSplitMinP ranks at 4;
 //   flat columns for short blocks (fused_flat): P = 12 at 3-4, P = 24, 32 and
 //     37 at 2 (3-7%); none from P = 64 (caps of 1-4 the same or slower).
 // AR_FUSED_CAP = N (both launches) or N,M (fused launch, broadcast) overrides
@@ -456,8 +463,10 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   if (tm) tm->mark();
   if (pl->fused_split) {
     a.lds = cap_lds(pl->bcast_cap, device);
+    // nontemporal stores from kBcastStreamMinP ranks up, and on flat columns
+    // at any P (P = 37: 11% faster, P = 48-128: 1-3%)
     const bool bnt = pl->bcast_nt_mode == 1 ||
-                     (pl->bcast_nt_mode < 0 && s.P >= kBcastStreamMinP &&
+                     (pl->bcast_nt_mode < 0 && (s.P >= kBcastStreamMinP || flat_short) &&
                       int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes);
     e = ar::launch_broadcast(a, pl->dtype, bnt, grid, stream);
     if (e != 0) return hip_fail(hipError_t(e), "broadcast kernel launch");
@@ -600,10 +609,12 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
     pl->fused_flat = kind && pl->op == AR_SUM &&
                      (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && max_len <= kPackMaxLen));
   }
-  pl->fused_split = one_result && (pl->split_mode == 1 || (pl->split_mode < 0 && pl->s.P >= kSplitMinP));
+  const bool rank_slots = pl->fused_flat && pl->fused_kind != kFusedXor;
+  const int32_t split_min = rank_slots ? kFlatSplitMinP : kSplitMinP;
+  pl->fused_split = one_result && (pl->split_mode == 1 || (pl->split_mode < 0 && pl->s.P >= split_min));
   {
     const int32_t P = pl->s.P;
-    if (pl->fused_split) pl->fused_cap = 6;
+    if (pl->fused_split) pl->fused_cap = (rank_slots && P < kSplitMinP) ? 4 : 6;
     else if (pl->fused_flat) pl->fused_cap = P <= 16 ? 4 : P < 64 ? 2 : 0;
     else if (pl->fused_kind == kFusedLo) pl->fused_cap = lo_cap(P);
     else if (pl->fused_kind == kFusedRing) pl->fused_cap = 4;

@@ -186,7 +186,9 @@ def test_random_plans_reproduce_oracle(case):
     (127, 127 * 18, 14, "cyclic", "butterfly", 2),   # rank slots, split
     (127, 127 * 18, 252, "cyclic", "ring", 2),
     (127, 127 * 18, 11, "cyclic", "butterfly", 1),   # shifted: the ranks receive different results
-    (37, 37 * 18, 12, "cyclic", "butterfly", 1),     # below 64 ranks
+    (37, 37 * 18, 12, "cyclic", "butterfly", 2),     # rank slots split from 33 ranks up
+    (32, 32 * 18, 10, "cyclic", "butterfly", 1),
+    (37, 37 * 100, 12, "cyclic", "butterfly", 1),    # block tiles split from 64 ranks up
     (127, 127 * 100, 14, "cyclic", "butterfly", 2),  # blocks of 100: block tiles, split
     (127, 127 * 100, 252, "cyclic", "ring", 2),
 ])

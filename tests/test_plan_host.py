@@ -205,9 +205,9 @@ def test_plan_sizes_match_oracle_counts(P):
         assert st.bytes_pulled_total == st.blocks_pulled_per_rank * st.n * 4
         split = st.fused_launches == 2
         assert st.fused_launches == (0 if P == 1 else 2 if split else 1)
-        # plans whose ranks all receive the same result split from P = 64 up, on flat columns (blocks of 10-11
-        # elements, the rank-slot kernel) as on block tiles
-        assert split == (P >= 64 and k == 2 * ceil_log2(P))
+        # plans whose ranks all receive the same result split: from P = 33 up on flat columns (blocks of 10-11
+        # elements, the rank-slot kernel), from P = 64 up on block tiles
+        assert split == (P >= 33 and k == 2 * ceil_log2(P))
         assert st.fused_flat == int(P >= 2 and k > ceil_log2(P))
         big = ar.Plan(P, 100 * P + 3, "float32", "sum", k).stats()
         assert (big.fused_launches == 2) == (P >= 64 and k == 2 * ceil_log2(P))
