@@ -241,7 +241,9 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
  * between launches (a few microseconds each), so their sum exceeds the time
  * of an untimed execute by about that much.  Errors as ar_execute_batched;
  * AR_ERR_INVALID_ARG for a NULL n_launches, cap < 0, or a NULL launch_ms
- * with cap > 0; AR_ERR_HIP when an event call fails. */
+ * with cap > 0; AR_ERR_HIP when an event call fails -- the launches are
+ * then enqueued all the same (the Allreduce runs, in place), and
+ * *n_launches is 0. */
 ar_status ar_execute_timed(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
                            hipStream_t stream, float* launch_ms, int32_t cap, int32_t* n_launches);
 
