@@ -22,6 +22,9 @@ Workloads (seeded synthetic rank buffers, resident in HBM before timing):
   small_batch127         P = 127, n = 106 fp32 N(0,1), 65536 instances, k = 7
   medium127              P = 127, n = 2304 fp32 N(0,1) (9 KB), 8192 instances,
                          --k 7..14 (default 11)
+  medium128              P = 128, n = 2304 fp32 N(0,1) (9 KB), 8192 instances,
+                         --k 7..14 (default 14); with --group xor, Recursive
+                         Halving at k = 14
 
 --group xor runs the butterfly schedules over the XOR group (power-of-two P:
 Recursive Halving at k = 2 log2 P, Recursive Doubling at k = log2 P);
@@ -79,11 +82,14 @@ def jobs_for(name, k_arg, group="cyclic", schedule="butterfly", op=None):
     return w, jobs
 
 
-DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4, "gradsync32": 10, "medium127": 11}
+DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4, "gradsync32": 10, "medium127": 11,
+             "medium128": 14}
 # Steps of well under a millisecond get more of them, so that the timed
 # region spans tens of milliseconds (prime3: about 10 us per step).
-DEFAULT_STEPS = {"large": 10, "small_batch": 200, "small_batch127": 100, "medium127": 100, "prime3": 1000}
-DEFAULT_WARMUP = {"large": 2, "small_batch": 20, "small_batch127": 10, "medium127": 10, "prime3": 50}
+DEFAULT_STEPS = {"large": 10, "small_batch": 200, "small_batch127": 100, "medium127": 100, "medium128": 100,
+                 "prime3": 1000}
+DEFAULT_WARMUP = {"large": 2, "small_batch": 20, "small_batch127": 10, "medium127": 10, "medium128": 10,
+                  "prime3": 50}
 
 SHAPES = {
     "small_batch": "small_batch: P in {5,6,7,12}, n=106 fp32 N(0,1), 65536 instances per launch",
@@ -94,6 +100,7 @@ SHAPES = {
     "gradsync32": "gradsync32: P=32, n=16777216 fp32 N(0,1e-3)",
     "small_batch127": "small_batch127: P=127, n=106 fp32 N(0,1), 65536 instances per launch",
     "medium127": "medium127: P=127, n=2304 fp32 N(0,1), 8192 instances per launch",
+    "medium128": "medium128: P=128, n=2304 fp32 N(0,1), 8192 instances per launch",
 }
 
 
@@ -259,7 +266,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=None)
     ap.add_argument("--workload", default="small_batch",
                     choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3", "gradsync32",
-                             "small_batch127", "medium127"])
+                             "small_batch127", "medium127", "medium128"])
     ap.add_argument("--k", type=int, default=None)
     ap.add_argument("--op", choices=["sum", "max"], default=None,
                     help="the reduction (default: the workload's first; prime_sweep also runs max)")

@@ -104,6 +104,9 @@ WORKLOADS = {
     # model with the measured cluster parameters picks k = 11 (blocks of 18-19 elements)
     "medium127": dict(P=[127], n=2304, dtype=np.float32, dist=Dist("normal", 0.0, 1.0),
                       ks=[7, 8, 9, 10, 11, 12, 13, 14], ops=["sum"], batch=8192, seed=BASE_SEED + 7),
+    # the same 9 KB message at P = 128, a power of two, where the XOR group applies (Recursive Halving at k = 14)
+    "medium128": dict(P=[128], n=2304, dtype=np.float32, dist=Dist("normal", 0.0, 1.0),
+                      ks=[7, 8, 9, 10, 11, 12, 13, 14], ops=["sum"], batch=8192, seed=BASE_SEED + 8),
     # the gradient-sync shape at a power of two, where the XOR group applies
     "gradsync32": dict(P=[32], n=16777216, dtype=np.float32, dist=Dist("normal", 0.0, 1e-3),
                        ks=[5, 6, 7, 8, 9, 10], ops=["sum"], batch=1, seed=BASE_SEED + 5),

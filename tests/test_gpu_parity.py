@@ -381,6 +381,31 @@ def test_medium127_workload_full_size(k):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("group,k", [("xor", 14), ("xor", 10), ("cyclic", 14)])
+def test_medium128_workload_full_size(group, k):
+    """P = 128, n = 2304 fp32 (9 KB), 8192 instances: the XOR group's flat
+    kernel (Recursive Halving at k = 14, split into the reducing launch and
+    the broadcast; the hybrid at k = 10) and the rank-slot kernel (cyclic,
+    k = 14, split) on all instances; the oracle on 96 sampled instances."""
+    w = synth.WORKLOADS["medium128"]
+    P, n, B = 128, w["n"], w["batch"]
+    note("medium128 %s P=%d n=%d B=%d k=%d" % (group, P, n, B, k))
+    X = synth.device_ranks(w["seed"], P, B * n, np.float32, w["dist"], DEV)
+    idx = np.sort(np.random.default_rng(k).choice(B, size=96, replace=False))
+    it = torch.from_numpy(idx).to(DEV)
+    xs = X.view(P, B, n)[:, it].cpu().numpy()
+    plan = ar.Plan(P, n, "float32", "sum", k, group=group)
+    st = plan.stats()
+    assert st.fused_flat == 1 and st.fused_launches == (2 if k == 14 else 1)
+    plan.batched([X[i] for i in range(P)], B, n)
+    torch.cuda.synchronize()
+    got = X.view(P, B, n)[:, it].cpu().numpy()
+    assert np.array_equal(bits(got), bits(oracle.allreduce_batched(xs, k, "sum", group=group)))
+    plan.close()
+    del X
+    torch.cuda.empty_cache()
+
+
 def check_full_size(name, P, n, k, op, seed, dist):
     note("%s P=%d n=%d k=%d op=%s: fill" % (name, P, n, k, op))
     X = synth.device_ranks(seed, P, n, np.float32, dist, DEV)
