@@ -130,6 +130,36 @@ def test_random_short_block_batches(P, n, B, stride, k, group, schedule, op, mon
     test_packed_and_blocked_tiles_agree_with_oracle(P, n, B, stride, k, group, schedule, op, monkeypatch)
 
 
+@pytest.mark.parametrize("P,n,B,stride,k,group,schedule,op", _random_cases(24, 20261204))
+def test_random_batches_with_the_split_forced_either_way(P, n, B, stride, k, group, schedule, op, monkeypatch):
+    """Seeded random plans with AR_FUSED_SPLIT forced off and on (where every
+    rank receives the same result: reduce on rank 0 or the block's rank, then
+    broadcast), with either kind of broadcast store: the oracle's bits, gaps
+    untouched."""
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    rng = np.random.default_rng(P * 11 + n + k)
+    dtype = "int32" if op == "isum" else "float32"
+    if op == "isum":
+        op = "sum"
+        x = rng.integers(-2**31, 2**31, size=(P, B, stride), dtype=np.int64).astype(np.int32)
+    else:
+        x = rng.normal(size=(P, B, stride)).astype(np.float32)
+    want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, op, group=group, schedule=schedule)
+    for split, bnt in (("0", "0"), ("1", "0"), ("1", "1")):
+        monkeypatch.setenv("AR_FUSED_SPLIT", split)
+        monkeypatch.setenv("AR_BCAST_NT", bnt)
+        note("split=%s nt=%s %s/%s P=%d n=%d B=%d k=%d op=%s" % (split, bnt, group, schedule, P, n, B, k, op))
+        plan = ar.Plan(P, n, dtype, op, k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
+        X = torch.from_numpy(x).to(DEV)
+        plan.batched([X[i] for i in range(P)], B, stride)
+        torch.cuda.synchronize()
+        got = X.cpu().numpy()
+        plan.close()
+        assert np.array_equal(bits(got[:, :, :n]), bits(want)), (split, bnt)
+        assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), (split, bnt)
+
+
 # ---------------------------------------------------------------------------
 # Step-wise path: merged runs of blocks (AR_STEP_MERGE)
 # ---------------------------------------------------------------------------
