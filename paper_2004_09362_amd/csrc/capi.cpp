@@ -71,6 +71,9 @@ constexpr int64_t kMergeMaxLen = 256;
 //   split launches (P = 127): the reducing launch at 3-6, the broadcast at 2
 //     (1 with nontemporal stores, from kBcastStreamMinP ranks up); the
 //     rank-slot kernel's reducing launch below kSplitMinP ranks at 4;
+//   block-tiled launches of every kind up to P = 8: none up to P = 6, 6 at
+//     P = 7-8 (large messages: P = 2 4.45 against 2.80 TB/s at the former
+//     cap of 4, P = 4 6.06 against 4.56, shifted P = 4 6.17 against 3.88);
 //   flat columns for short blocks (fused_flat): none up to P = 6 (a cap of 4
 //     cost 10-29% there), P = 7-8 at 6, P = 12 at 3-4, P = 24, 32 and 37 at 2
 //     (3-7%); none from P = 64 (caps of 1-4 the same or slower).
@@ -618,6 +621,7 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
     if (pl->fused_split) pl->fused_cap = (rank_slots && P < kSplitMinP) ? 4 : 6;
     else if (pl->fused_flat) pl->fused_cap = P <= 6 ? 0 : P <= 8 ? 6 : P <= 16 ? 4 : P < 64 ? 2 : 0;
     else if (pl->fused_kind == kFusedLo) pl->fused_cap = lo_cap(P);
+    else if (P <= 8) pl->fused_cap = P <= 6 ? 0 : 6;  // few rank rows per wave: more waves resident
     else if (pl->fused_kind == kFusedRing) pl->fused_cap = 4;
     else if (pl->s.r == 0) pl->fused_cap = P <= 32 ? 4 : 3;
     else pl->fused_cap = P >= 64 ? 0 : 3;
