@@ -113,7 +113,8 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   of several instances when blocks hold at
  *                                   most 64 elements (default: the latter
  *                                   for batches with blocks that short);
- *   AR_FUSED_ROTATE = 0|1           sums (other than latency-optimal):
+ *   AR_FUSED_ROTATE = 0|1           sums (other than latency-optimal), and
+ *                                   max in bandwidth-optimal and Ring plans:
  *                                   never / always on flat columns as above
  *                                   (default: when blocks hold at most 64
  *                                   elements);
@@ -160,7 +161,8 @@ typedef struct {
                                         launch and a broadcast (every rank receives the
                                         same result and P >= 64; P >= 33 for sums with
                                         short blocks outside the XOR group)              */
-  int32_t fused_flat;                /* FUSED path of a sum with short blocks: 1 when it
+  int32_t fused_flat;                /* FUSED path with short blocks (sums; max in the
+                                        bandwidth-optimal and Ring plans): 1 when it
                                         runs on flat columns (the rank-slot kernel, or
                                         the XOR group's kernel without the block) for
                                         batches of fewer than 2^32 - 64 columns           */

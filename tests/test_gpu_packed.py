@@ -58,6 +58,11 @@ CASES = [
     (16, 100, 9, 103, 5, "xor", "butterfly", "isum"),        # int32, XOR hybrid
     (64, 300, 6, 300, 12, "xor", "butterfly", "sum"),        # Recursive Halving at P = 64
     (24, 100, 17, 100, 46, "cyclic", "ring", "isum"),        # int32, Ring
+    (24, 100, 50, 104, 10, "cyclic", "butterfly", "max"),    # max, bandwidth-optimal: rank slots
+    (127, 1000, 9, 1003, 14, "cyclic", "butterfly", "max"),  # max at P = 127, split
+    (24, 100, 17, 100, 46, "cyclic", "ring", "max"),         # max, Ring
+    (48, 1000, 5, 1001, 94, "cyclic", "ring", "max"),        # max, Ring, split
+    (32, 200, 13, 200, 10, "xor", "butterfly", "max"),       # XOR max: packed tiles
 ]
 
 SETTINGS = [  # AR_FUSED_ROTATE, AR_FUSED_PACKED (None: unset, the default)
