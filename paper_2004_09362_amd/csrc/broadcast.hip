@@ -18,10 +18,11 @@
 // tiles laid on 256-byte boundaries of rank b's buffer, or one short block
 // of several instances per wave.  After a reducing launch on flat columns
 // (a.flat: batches of short blocks) every column's result is on rank 0, and
-// the waves take 64 consecutive flat columns each.  Loads and stores are nontemporal (NT) or
-// ordinary: from P = 96 ranks, streaming the P - 1 stores nontemporally at
-// one resident workgroup per CU was 3-4% faster; below, ordinary stores
-// streamed as fast or faster.
+// the waves take 64 consecutive flat columns each.  Loads and stores are
+// nontemporal (NT) or ordinary: from P = 96 ranks, streaming the P - 1
+// stores nontemporally at one resident workgroup per CU was 3-4% faster,
+// and on flat columns nontemporal stores were 1-11% faster at any P; below
+// P = 96 on block tiles, ordinary stores streamed as fast or faster.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>

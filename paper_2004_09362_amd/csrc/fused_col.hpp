@@ -206,20 +206,21 @@ __global__ __launch_bounds__(kBlock) void fused_mid_kernel(const ColArgs a) {
   }
 }
 
-// fused_rot_kernel: sums over batches of short blocks, in rank slots over
-// flat columns, for the cyclic butterfly plans with r < L (the
-// bandwidth-optimal fold and the shifted recursion above) and the Ring.
-// Lane g holds element i of instance g / n; its block b follows from i.  It loads X[y] = V_y[e] for
-// every rank y -- each load a whole 256-byte row of one rank buffer,
-// whatever the blocks -- and rotates the column by b, X[p] <- X[b + p], so
-// that X[p] is placement p's value, V_{b+p}, exactly as the block-tiled
-// kernels read it through rotated pointers.  The fold, the recursion or the
-// chain then combines the same operand pairs in the same order (the same
-// bits).  The bandwidth-optimal and Ring result goes to every rank (with
-// a.split, to rank 0 alone, and the broadcast copies it); in the shifted
-// plan rank
-// b + q receives S[col_src(q)], so the column of results is rotated back by
-// b and rank y stores slot y.  A rotation by a per-lane amount is a
+// fused_rot_kernel: batches of short blocks in rank slots over flat
+// columns, for the cyclic butterfly plans with r < L (the bandwidth-optimal
+// fold and the shifted recursion above) and the Ring; sums, and max where
+// every rank receives one result.  Lane g holds element i of instance
+// g / n; its block b follows from i.  It loads X[y] = V_y[e] for every rank
+// y -- each load a whole 256-byte row of one rank buffer, whatever the
+// blocks -- and rotates the column by b, X[p] <- X[b + p], so that X[p] is
+// placement p's value, V_{b+p}, exactly as the block-tiled kernels read it
+// through rotated pointers.  The fold, the recursion or the chain then
+// combines the same operand pairs in the same order (the same bits, also
+// for a max of signed zeros or NaNs).  The bandwidth-optimal and Ring
+// result goes to every rank (with a.split, to rank 0 alone, and the
+// broadcast copies it); in the shifted plan rank b + q receives
+// S[col_src(q)], so the column of results is rotated back by b and rank y
+// stores slot y.  A rotation by a per-lane amount is a
 // log-depth network of static rotations by 2^j, each applied on the lanes
 // whose amount has bit j set (P selects per stage; a stage no lane needs is
 // skipped).
