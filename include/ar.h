@@ -114,7 +114,8 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   most 64 elements (default: the latter
  *                                   for batches with blocks that short);
  *   AR_FUSED_ROTATE = 0|1           sums (other than latency-optimal), and
- *                                   max in bandwidth-optimal and Ring plans:
+ *                                   max in bandwidth-optimal, Ring and XOR
+ *                                   plans:
  *                                   never / always on flat columns as above
  *                                   (default: when blocks hold at most 64
  *                                   elements);
@@ -162,7 +163,7 @@ typedef struct {
                                         same result and P >= 64; P >= 33 for sums with
                                         short blocks outside the XOR group)              */
   int32_t fused_flat;                /* FUSED path with short blocks (sums; max in the
-                                        bandwidth-optimal and Ring plans): 1 when it
+                                        bandwidth-optimal, Ring and XOR plans): 1 when it
                                         runs on flat columns (the rank-slot kernel, or
                                         the XOR group's kernel without the block) for
                                         batches of fewer than 2^32 - 64 columns           */

@@ -610,11 +610,11 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
     const int64_t max_len = pl->s.P > 0 ? pl->s.n / pl->s.P + (pl->s.n % pl->s.P ? 1 : 0) : 0;
     const bool kind = pl->fused_kind == kFusedRing || pl->fused_kind == kFusedXor ||
                       (pl->fused_kind == kFusedCol && pl->s.r < pl->s.L);
-    // max: the rank-slot kernel's bandwidth-optimal fold and Ring only (the
-    // XOR group's flat kernel leaves out the operand order, which a max of
-    // signed zeros or NaNs can see)
-    const bool op_ok = pl->op == AR_SUM ||
-                       (pl->fused_kind == kFusedRing || (pl->fused_kind == kFusedCol && pl->s.r == 0));
+    // max: the rank-slot kernel's bandwidth-optimal fold and Ring (its
+    // shifted max plans keep packed tiles, saving their instantiations), and
+    // the XOR group, whose flat kernel then takes each lane's block
+    const bool op_ok = pl->op == AR_SUM || pl->fused_kind == kFusedRing || pl->fused_kind == kFusedXor ||
+                       (pl->fused_kind == kFusedCol && pl->s.r == 0);
     pl->fused_flat = kind && op_ok && (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && max_len <= kPackMaxLen));
   }
   const bool rank_slots = pl->fused_flat && pl->fused_kind != kFusedXor;

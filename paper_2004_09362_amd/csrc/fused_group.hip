@@ -99,14 +99,20 @@ __global__ __launch_bounds__(kBlock) void fused_xor_kernel(const ColArgs a) {
     int32_t b;
     int64_t e;
     bool live;
-    // Flat columns where no result depends on the block: Recursive
-    // Doubling, and sums at any R (the block only orders the operands of a
-    // halving pair, and a sum is the same either way).
-    if ((R == xor_L(P) || OP == 0) && a.flat) {
+    // Flat columns (batches of short blocks, and Recursive Doubling): the
+    // block only orders the operands of a halving pair, which a sum does
+    // not see, so sums and Recursive Doubling leave it out; a max takes the
+    // lane's own block (the halving's order then differs from lane to lane).
+    if (a.flat) {
       const uint32_t g = t * uint32_t(kWave) + uint32_t(lane);
       const uint32_t inst = fdiv(g, a.ndiv);
+      const uint32_t i = g - inst * a.ndiv.d;
       b = 0;
-      e = int64_t(inst) * a.stride + int64_t(g - inst * a.ndiv.d);
+      if constexpr (OP != 0 && R != xor_L(P)) {
+        const uint32_t longer = uint32_t(a.m) * (uint32_t(a.q) + 1);  // elements in the blocks of q + 1
+        b = int32_t(i < longer ? fdiv(i, a.q1div) : uint32_t(a.m) + fdiv(i - longer, a.qdiv));
+      }
+      e = int64_t(inst) * a.stride + int64_t(i);
       live = g < a.flat_cols;
     } else {
       live = col_tile_column(a, t, lane, b, e);
@@ -117,8 +123,8 @@ __global__ __launch_bounds__(kBlock) void fused_xor_kernel(const ColArgs a) {
       for (int y = 0; y < P; ++y) X[y] = ld1<NT>(static_cast<const T*>(tbl[y]) + e);
       xor_halving<P, W, P / 2, OP, T>(X, uint32_t(b));
       xor_doubling<P, W, W / 2, OP, T>(X);
-      if (W == 1 && a.split) {  // Recursive Halving: one result, rank b holds it first
-        st1<NT>(static_cast<T*>(tbl[b]) + e, X[0]);
+      if (W == 1 && a.split) {  // Recursive Halving: one result, held first by rank b (rank 0 on flat columns)
+        st1<NT>(static_cast<T*>(tbl[a.flat ? 0 : b]) + e, X[0]);
       } else {
 #pragma unroll
         for (int x = 0; x < P; ++x) st1<NT>(static_cast<T*>(tbl[x]) + e, X[x & (W - 1)]);

@@ -62,7 +62,9 @@ CASES = [
     (127, 1000, 9, 1003, 14, "cyclic", "butterfly", "max"),  # max at P = 127, split
     (24, 100, 17, 100, 46, "cyclic", "ring", "max"),         # max, Ring
     (48, 1000, 5, 1001, 94, "cyclic", "ring", "max"),        # max, Ring, split
-    (32, 200, 13, 200, 10, "xor", "butterfly", "max"),       # XOR max: packed tiles
+    (32, 200, 13, 200, 10, "xor", "butterfly", "max"),       # XOR max, flat: each lane's block orders the pairs
+    (32, 200, 13, 200, 7, "xor", "butterfly", "max"),        # XOR max, hybrid r = 3
+    (128, 2000, 5, 2003, 14, "xor", "butterfly", "max"),     # XOR max, flat, split
 ]
 
 SETTINGS = [  # AR_FUSED_ROTATE, AR_FUSED_PACKED (None: unset, the default)
@@ -163,6 +165,33 @@ def test_random_batches_with_the_split_forced_either_way(P, n, B, stride, k, gro
         plan.close()
         assert np.array_equal(bits(got[:, :, :n]), bits(want)), (split, bnt)
         assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), (split, bnt)
+
+
+@pytest.mark.parametrize("P,n,B,k,group,schedule", [
+    (32, 200, 13, 10, "xor", "butterfly"), (32, 200, 13, 7, "xor", "butterfly"), (128, 2000, 5, 14, "xor", "butterfly"),
+    (24, 100, 17, 10, "cyclic", "butterfly"), (24, 100, 17, 46, "cyclic", "ring"), (127, 1000, 9, 14, "cyclic", "butterfly"),
+])
+def test_max_of_signed_zeros_follows_the_schedules_operand_order(P, n, B, k, group, schedule, monkeypatch):
+    """Inputs of +0.0 and -0.0 only: a max of two zeros returns the kept
+    operand, so the result bits show whether every combine took its operands
+    in the schedule's order -- on flat columns (each lane's own block) and on
+    packed tiles alike."""
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    rng = np.random.default_rng(P + n + k)
+    x = np.where(rng.integers(0, 2, size=(P, B, n)) == 1, np.float32(-0.0), np.float32(0.0)).astype(np.float32)
+    want = oracle.allreduce_batched(x, k, "max", group=group, schedule=schedule)
+    assert np.unique(bits(want)).size == 2  # both zeros occur among the results
+    for rotate in ("0", "1"):
+        monkeypatch.setenv("AR_FUSED_ROTATE", rotate)
+        plan = ar.Plan(P, n, "float32", "max", k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
+        note("signed zeros rotate=%s %s/%s P=%d k=%d flat=%d" % (rotate, group, schedule, P, k, plan.stats().fused_flat))
+        X = torch.from_numpy(x).to(DEV)
+        plan.batched([X[i] for i in range(P)], B, n)
+        torch.cuda.synchronize()
+        got = X.cpu().numpy()
+        plan.close()
+        assert np.array_equal(bits(got), bits(want)), rotate
 
 
 # ---------------------------------------------------------------------------

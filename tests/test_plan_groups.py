@@ -201,9 +201,10 @@ def test_default_split_of_one_result_plans(P, n, k, group, schedule, launches):
 
 @pytest.mark.parametrize("P,k,group,schedule,flat", [
     (24, 10, "cyclic", "butterfly", 1), (127, 14, "cyclic", "butterfly", 1), (24, 46, "cyclic", "ring", 1),
-    (24, 7, "cyclic", "butterfly", 0), (32, 10, "xor", "butterfly", 0), (12, 4, "cyclic", "butterfly", 0),
+    (24, 7, "cyclic", "butterfly", 0), (32, 10, "xor", "butterfly", 1), (32, 7, "xor", "butterfly", 1),
+    (12, 4, "cyclic", "butterfly", 0),
 ])
-def test_max_with_short_blocks_runs_in_rank_slots_where_every_rank_gets_one_result(P, k, group, schedule, flat):
+def test_max_with_short_blocks_on_flat_columns(P, k, group, schedule, flat):
     for dtype in ("float32", "int32"):
         st = ar.Plan(P, 18 * P, dtype, "max", k, group=group, schedule=schedule).stats()
         assert st.fused_flat == flat, (P, k, group, schedule, dtype)
