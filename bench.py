@@ -10,13 +10,17 @@ over the workload's instances), and the achieved algorithmic HBM bandwidth
 of the dominant kernel against the MI355X peak of 8 TB/s.
 
 Workloads (seeded synthetic rank buffers, resident in HBM before timing):
-  small_batch (default)  P in {5, 6, 7, 12}, n = 106 fp32 N(0,1) (about the
+  small_batch            P in {5, 6, 7, 12}, n = 106 fp32 N(0,1) (about the
                          425-byte average message the paper quotes), 65536
                          instances per launch, latency-optimal k = ceil(log2 P)
   gradsync               P = 24, n = 2^24 fp32 N(0,1e-3), k = 10
   prime_sweep            P = 37, n = 2^22 fp32 U(-1,1), --k in 6..12 (default 12),
                          --op sum (default) or max
-  large                  P = 127, n = 2^26 fp32 N(0,1e-2), --k 14 (default) or 10
+  large (default)        P = 127, n = 2^26 fp32 N(0,1e-2) (31.75 GiB of rank
+                         buffers, the largest shape that fits one GPU), --k 14
+                         (default) or 10; without --k the line reports k = 14
+                         and carries k = 10, timed on the same buffers, under
+                         "extra"
   prime3                 P = 3, n = 1024 int32 U[-1000,1000], --k 2..4 (default 4)
   gradsync32             P = 32, n = 2^24 fp32 N(0,1e-3), --k 5..10 (default 10)
   small_batch127         P = 127, n = 106 fp32 N(0,1), 65536 instances, k = 7
@@ -88,6 +92,8 @@ DEFAULT_K = {"gradsync": 10, "prime_sweep": 12, "large": 14, "prime3": 4, "grads
 # region spans tens of milliseconds (prime3: about 10 us per step).
 DEFAULT_STEPS = {"large": 10, "small_batch": 200, "small_batch127": 100, "medium127": 100, "medium128": 100,
                  "prime3": 1000}
+# further k timed on the same buffers when --k is not given
+EXTRA_K = {"large": [10]}
 DEFAULT_WARMUP = {"large": 2, "small_batch": 20, "small_batch127": 10, "medium127": 10, "medium128": 10,
                   "prime3": 50}
 
@@ -142,8 +148,32 @@ def traffic_key(workload, group, schedule):
     return workload + ("/xor" if group == "xor" else "") + ("/ring" if schedule == "ring" else "")
 
 
-def cpu_baseline(jobs, host_sets, budget_s=12.0, group="cyclic", schedule="butterfly"):
-    """The CPU oracle (single thread, as it stands) on a bounded sample."""
+def host_facts():
+    """Threads this process may use, and the CPU model, from the OS."""
+    try:
+        usable = len(os.sched_getaffinity(0))
+    except (AttributeError, OSError):
+        usable = os.cpu_count() or 1
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for ln in fh:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"nproc": usable, "cpu_model": model}
+
+
+def cpu_baseline(jobs, fetchers, budget_s=12.0, group="cyclic", schedule="butterfly"):
+    """The CPU oracle (single thread, as it stands) on a bounded sample.
+
+    ``fetchers[i](kind, count)`` copies job i's sample to the host: the first
+    ``count`` instances of a batch ([P, count, n]), or the first ``count``
+    columns of every block of a single instance (then it returns the [P,
+    ncols] values and their column indices).  Only the sample crosses PCIe.
+    """
     import numpy as np
 
     import oracle
@@ -151,45 +181,92 @@ def cpu_baseline(jobs, host_sets, budget_s=12.0, group="cyclic", schedule="butte
     oracle.lib()
     total_bytes, total_t, parts = 0, 0.0, []
     per_job_budget = budget_s / len(jobs)
-    for job, x in zip(jobs, host_sets):
+    for job, fetch in zip(jobs, fetchers):
         P, n, B, k = job["P"], job["n"], job["batch"], job["k"]
         if B > 1:
-            # whole instances; repeat the full set if it takes less than the budget
+            # whole instances; repeat the set if it takes less than the budget
             b = 64
             reps = 1
             while True:
-                xb = np.ascontiguousarray(x[:, :b])
+                xb = fetch("instances", b)
                 t0 = time.perf_counter()
                 for _ in range(reps):
                     oracle.allreduce_batched(xb, k, job["op"], group=group, schedule=schedule)
                 dt = time.perf_counter() - t0
                 if dt >= per_job_budget:
                     break
-                if b < x.shape[1]:
-                    b = min(x.shape[1], max(b * 2, int(b * per_job_budget / max(dt, 1e-3))))
+                if b < B:
+                    b = min(B, max(b * 2, int(b * per_job_budget / max(dt, 1e-3))))
                 else:
                     reps = max(reps + 1, int(reps * per_job_budget / max(dt, 1e-3)) + 1)
             total_bytes += P * n * b * reps * job["dtype"].itemsize
             parts.append("P=%d: %d of %d instances x%d" % (P, b, B, reps))
         else:
-            # sampled columns: `c` per block, the same replay as a full run at those columns
-            q = n // P
-            c = 256
+            # sampled columns: the first `c` of every block (at most the prefetched
+            # fetch.cmax), the same replay as a full run at those columns; repeated
+            # if that takes less than the budget
+            c = min(256, fetch.cmax)
+            reps = 1
             while True:
-                cols = np.unique(np.concatenate([np.arange(bb * q, bb * q + min(c, q)) for bb in range(P)]))
-                xs = np.ascontiguousarray(x[:, cols])
+                xs, cols = fetch("columns", c)
                 t0 = time.perf_counter()
-                oracle.allreduce(xs, k, job["op"], n=n, cols=cols, group=group, schedule=schedule)
+                for _ in range(reps):
+                    oracle.allreduce(xs, k, job["op"], n=n, cols=cols, group=group, schedule=schedule)
                 dt = time.perf_counter() - t0
-                if dt >= per_job_budget or c >= q:
+                if dt >= per_job_budget:
                     break
-                c = min(q, max(c * 2, int(c * per_job_budget / max(dt, 1e-3))))
+                if c < fetch.cmax:
+                    c = min(fetch.cmax, max(c * 2, int(c * per_job_budget / max(dt, 1e-3))))
+                else:
+                    reps = max(reps + 1, int(reps * per_job_budget / max(dt, 1e-3)) + 1)
             b = len(cols)
-            total_bytes += P * b * job["dtype"].itemsize
-            parts.append("P=%d: %d of %d columns" % (P, b, n))
+            total_bytes += P * b * reps * job["dtype"].itemsize
+            parts.append("P=%d: %d of %d columns (the first %d of every block) x%d" % (P, b, n, c, reps))
         total_t += dt
+    facts = host_facts()
     return {"value": round(total_bytes / total_t / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": "; ".join(parts) + " (single-threaded C replay, %.1f s)" % total_t}
+            "sample": "; ".join(parts) + " (single-threaded C replay, %.1f s)" % total_t,
+            "nproc": facts["nproc"], "cpu_model": facts["cpu_model"]}
+
+
+# Columns per block copied to the host for the oracle's sample (at P = 127
+# about 1 GB); the oracle replays them as often as its time budget allows.
+SAMPLE_COLS_PER_BLOCK = 16384
+
+
+def sample_fetchers(jobs, tensors):
+    """Copy each job's oracle sample to the host now (before any step changes
+    the buffers in place) and return one fetch function per job (see
+    cpu_baseline).  Batches are copied whole (at most 1.6 GB in the batched
+    workloads); single instances only the first SAMPLE_COLS_PER_BLOCK columns
+    of every block."""
+    import numpy as np
+    import torch
+
+    def make(j, X):
+        P, n, B = j["P"], j["n"], j["batch"]
+        if B > 1:
+            host = X.view(P, B, n).cpu().numpy()
+
+            def fetch_inst(kind, count):
+                return np.ascontiguousarray(host[:, :count])
+
+            return fetch_inst
+        q, m = n // P, n % P
+        cmax = max(1, min(q, SAMPLE_COLS_PER_BLOCK))
+        starts = np.array([bb * q + min(bb, m) for bb in range(P)], dtype=np.int64)
+        cols_all = (starts[:, None] + np.arange(cmax, dtype=np.int64)[None, :])  # [block, c]
+        idx = torch.from_numpy(cols_all.reshape(-1)).to(X.device)
+        host = X.index_select(1, idx).cpu().numpy().reshape(P, P, cmax)  # [rank, block, c]
+
+        def fetch_cols(kind, count):
+            c = min(count, cmax)
+            return np.ascontiguousarray(host[:, :, :c].reshape(P, P * c)), cols_all[:, :c].reshape(-1).copy()
+
+        fetch_cols.cmax = cmax
+        return fetch_cols
+
+    return [make(j, X) for j, X in zip(jobs, tensors)]
 
 
 class HipEvent:
@@ -264,7 +341,7 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--workload", default="small_batch",
+    ap.add_argument("--workload", default="large",
                     choices=["small_batch", "gradsync", "prime_sweep", "large", "prime3", "gradsync32",
                              "small_batch127", "medium127", "medium128"])
     ap.add_argument("--k", type=int, default=None)
@@ -301,34 +378,71 @@ def main():
         raise SystemExit("the Ring runs over the cyclic group")
     w, jobs = jobs_for(args.workload, args.k, args.group, args.schedule, args.op)
     path = {"auto": ar.AR_PATH_AUTO, "stepwise": ar.AR_PATH_STEPWISE, "fused": ar.AR_PATH_FUSED}[args.path]
+    # the large workload without --k: k = 14 on the line, k = 10 under "extra"
+    extra_ks = EXTRA_K.get(args.workload, []) if (args.k is None and args.schedule == "butterfly"
+                                                 and args.group == "cyclic") else []
 
-    # ---- plans and resident inputs ----
+    # ---- resident inputs ----
     set_bytes = sum(j["P"] * j["n"] * j["batch"] * j["dtype"].itemsize for j in jobs)
     n_sets = int(max(1, min(steps + warmup, -(-POOL_BYTES // set_bytes))))
-    plans, sets = [], []
-    for j in jobs:
-        p = ar.Plan(j["P"], j["n"], j["dtype"].name, j["op"], j["k"], path=path, group=args.group,
-                    schedule=args.schedule)
-        plans.append(p)
     log("workload %s: %d job(s), %d input set(s) of %.1f MB" % (args.workload, len(jobs), n_sets, set_bytes / 1e6))
+    sets = []
     for s in range(n_sets):
         per = []
         for j in jobs:
             X = synth.device_ranks(j["seed"] + 7919 * s, j["P"], j["n"] * j["batch"], j["dtype"], j["dist"], dev)
             per.append(X)
         sets.append(per)
-    host_sets = None
-    if not args.no_cpu_baseline:
-        host_sets = []
-        for j, X in zip(jobs, sets[0]):
-            if j["batch"] > 1:
-                host_sets.append(X.view(j["P"], j["batch"], j["n"]).cpu().numpy())
-            else:
-                host_sets.append(X.cpu().numpy())
+    fetchers = None if args.no_cpu_baseline else sample_fetchers(jobs, sets[0])
     ptr_tables = [[[X[i] for i in range(j["P"])] for j, X in zip(jobs, per)] for per in sets]
     torch.cuda.synchronize()
-
     stream = torch.cuda.current_stream()
+
+    res = measure(args, jobs, path, ptr_tables, n_sets, steps, warmup, stream)
+    desc = describe(args.workload, jobs, args.group, args.schedule)
+    out = {
+        "metric": METRIC, "value": res["value"], "unit": "GB/s", "n_gpus": 1, "steps": steps,
+        "warmup": warmup, "ms_per_step": res["ms_per_step"], "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "int32" if jobs[0]["dtype"] == np.int32 else "f32",
+        "data": "synthetic (seeded; %d rotating input set(s) resident in HBM)" % n_sets,
+        "config": {"workload": desc, "P": [j["P"] for j in jobs], "n": jobs[0]["n"], "batch": jobs[0]["batch"],
+                   "k": [j["k"] for j in jobs], "op": jobs[0]["op"],
+                   "path": res["path"], "group": args.group, "schedule": args.schedule,
+                   "parallelism": "1 GPU, P virtual ranks"},
+        "hbm_algorithmic_GBps_step": res["hbm_algorithmic_GBps_step"],
+        "wall_s_timed": res["wall_s_timed"],
+        "roofline": res["roofline"],
+        "source_hash": res["source_hash"],
+    }
+    if extra_ks:
+        # the same buffers, timed again with each further k (they hold the
+        # previous results by then; the values do not change the traffic)
+        out["extra"] = []
+        for k in extra_ks:
+            _, jobs_k = jobs_for(args.workload, k, args.group, args.schedule, args.op)
+            rk = measure(args, jobs_k, path, ptr_tables, n_sets, steps, warmup, stream)
+            rk["workload"] = describe(args.workload, jobs_k, args.group, args.schedule)
+            rk["k"] = [j["k"] for j in jobs_k]
+            out["extra"].append(rk)
+    if fetchers is not None:
+        log("timing the CPU oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(jobs, fetchers, group=args.group, schedule=args.schedule)
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+
+
+def measure(args, jobs, path, ptr_tables, n_sets, steps, warmup, stream):
+    """Time `steps` steps of the jobs' Allreduces (after `warmup` untimed
+    ones) and the dominant job's launches; returns the step time, the
+    effective bandwidth and the roofline of the dominant kernel."""
+    import torch
+
+    from paper_2004_09362_amd import ar
+
+    plans = [ar.Plan(j["P"], j["n"], j["dtype"].name, j["op"], j["k"], path=path, group=args.group,
+                     schedule=args.schedule) for j in jobs]
+
     # the dominant job: the one moving the most algorithmic bytes
     def alg_bytes(j, p):
         st_ = p.stats()
@@ -387,6 +501,24 @@ def main():
     bytes_per_launch = alg / launches
     launch_ms = dom_ms / launches
     achieved = bytes_per_launch / (launch_ms * 1e-3) / 1e9
+    kname = kernel_name(args, dj, st, fused)
+    src_hash = kernel_source_hash(kname)
+    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4),
+            "traffic": traffic_from_profiles(traffic_key(args.workload, args.group, args.schedule), kname, src_hash),
+            "kernel": kname, "job_P": dj["P"], "bytes_per_launch": int(bytes_per_launch),
+            "launch_ms": round(launch_ms, 5), "launches_per_step": launches,
+            "timed_by": ("HIP events around each launch, in a second pass of the same steps" if per_launch
+                         else "HIP events around the timed region")}
+    step_alg = sum(alg_bytes(j, p)[0] for j, p in zip(jobs, plans))
+    return {"value": round(value, 2), "ms_per_step": round(ms_per_step, 5),
+            "path": "fused" if fused else "stepwise",
+            "hbm_algorithmic_GBps_step": round(step_alg / (ms_per_step * 1e-3) / 1e9, 1),
+            "wall_s_timed": round(wall, 4), "roofline": roof, "source_hash": src_hash}
+
+
+def kernel_name(args, dj, st, fused):
+    """Name of the dominant job's kernel(s) as the profiles list it."""
     if not fused:
         kname = "step_kernel<k=%d>" % dj["k"]
     elif st.fused_flat and args.group != "xor":
@@ -403,37 +535,7 @@ def main():
         kname = "fused_mid_kernel<P=%d>" % dj["P"]
     if fused and st.fused_launches == 2:
         kname += "+broadcast"  # the pair: reducing launch, then the broadcast
-    src_hash = kernel_source_hash(kname)
-    roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-            "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": traffic_from_profiles(traffic_key(args.workload, args.group, args.schedule), kname, src_hash),
-            "kernel": kname, "job_P": dj["P"], "bytes_per_launch": int(bytes_per_launch),
-            "launch_ms": round(launch_ms, 5), "launches_per_step": launches,
-            "timed_by": ("HIP events around each launch, in a second pass of the same steps" if per_launch
-                         else "HIP events around the timed region")}
-    step_alg = sum(alg_bytes(j, p)[0] for j, p in zip(jobs, plans))
-
-    desc = describe(args.workload, jobs, args.group, args.schedule)
-    out = {
-        "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1, "steps": steps,
-        "warmup": warmup, "ms_per_step": round(ms_per_step, 5), "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "int32" if jobs[0]["dtype"] == np.int32 else "f32",
-        "data": "synthetic (seeded; %d rotating input sets resident in HBM)" % n_sets,
-        "config": {"workload": desc, "P": [j["P"] for j in jobs], "n": jobs[0]["n"], "batch": jobs[0]["batch"],
-                   "k": [j["k"] for j in jobs], "op": jobs[0]["op"],
-                   "path": "fused" if fused else "stepwise", "group": args.group, "schedule": args.schedule,
-                   "parallelism": "1 GPU, P virtual ranks"},
-        "hbm_algorithmic_GBps_step": round(step_alg / (ms_per_step * 1e-3) / 1e9, 1),
-        "wall_s_timed": round(wall, 4),
-        "roofline": roof,
-        "source_hash": src_hash,
-    }
-    if host_sets is not None:
-        log("timing the CPU oracle on a sample")
-        out["cpu_baseline"] = cpu_baseline(jobs, host_sets, group=args.group, schedule=args.schedule)
-    else:
-        out["cpu_baseline"] = None
-    print(json.dumps(out), flush=True)
+    return kname
 
 
 if __name__ == "__main__":

@@ -167,6 +167,14 @@ typedef struct {
                                         runs on flat columns (the rank-slot kernel, or
                                         the XOR group's kernel without the block) for
                                         batches of fewer than 2^32 - 64 columns           */
+  int32_t exec_path;                 /* path ar_execute takes: AR_PATH_STEPWISE or
+                                        AR_PATH_FUSED (AR_PATH_AUTO resolved); 0 when
+                                        there is nothing to run (P = 1)                  */
+  int64_t hbm_bytes_algorithmic;     /* algorithmic HBM bytes of the step-by-step
+                                        schedule over all ranks (the paper's steps as
+                                        separate passes: a combine reads two blocks and
+                                        writes one, a copy reads and writes one); equal
+                                        to hbm_bytes_stepwise                            */
 } ar_stats;
 
 /* One launch of the STEPWISE path: a list of placement ranges.  In a range,
@@ -189,12 +197,17 @@ typedef struct {
 
 enum { AR_KIND_COPY = 0, AR_KIND_REDUCE = 1, AR_KIND_REDUCE2 = 2 };
 
+/* k_steps value that asks plan creation to choose the step count (and the
+ * path) from the cost model, as ar_plan_create_auto does with the default
+ * parameters, one instance and the group of the call. */
+#define AR_K_AUTO (-1)
+
 /* Build the schedule for P ranks, n elements per rank and k_steps steps
  * (Secs. 7-9).  Host work only: validates, derives the per-step placement
  * ranges, assigns buffers, proves every launch free of read/write overlap
  * between ranks, and computes the sizes.  No device memory is touched.
  *   P in [1, 128]; n in [0, 2^46]; k_steps in [ceil(log2 P), 2*ceil(log2 P)]
- *   (k_steps = 0 for P = 1); dtype/op from the enums above.
+ *   (k_steps = 0 for P = 1), or AR_K_AUTO; dtype/op from the enums above.
  * Errors: AR_ERR_INVALID_ARG (range), AR_ERR_UNSUPPORTED (dtype/op),
  * AR_ERR_INTERNAL (consistency check failed).  *out_plan is set on AR_OK. */
 ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_plan** out_plan);
@@ -206,7 +219,8 @@ ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t
  * per block, then doubling levels; Ring: the chain of Sec. 6), bit-identical
  * to STEPWISE.  Errors as ar_plan_create, and AR_ERR_INVALID_ARG for an
  * unknown group or schedule, AR_GROUP_XOR with P not a power of two, the
- * Ring over AR_GROUP_XOR, or a Ring k_steps other than 2(P-1). */
+ * Ring over AR_GROUP_XOR, or a Ring k_steps other than 2(P-1).  AR_K_AUTO
+ * is accepted for the butterfly schedules only. */
 ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_group group,
                             ar_schedule schedule, ar_plan** out_plan);
 
@@ -214,22 +228,33 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
  * FUSED is asked for and the plan cannot run fused. */
 ar_status ar_plan_set_path(ar_plan* plan, ar_path path);
 
-/* Allreduce in place.  rank_buffers: host array of P device pointers, rank
+/* Allreduce in place (Sec. 1): afterwards every rank buffer holds the
+ * elementwise combination (Sec. 5.4) of all P input vectors.  The schedule's
+ * exchanges (Sec. 5.3: in a step, rank x receives the blocks of its peer
+ * under the step's operator) are pulls here: the kernels of a step read the
+ * peer's block out of HBM.  rank_buffers: host array of P device pointers, rank
  * x's n elements at rank_buffers[x].  Pointers must be 4-byte aligned and
  * must not overlap (AR_ERR_ALIAS); 16-byte aligned buffers take the
  * vectorised kernels.  With n = 0 nothing is touched and the pointers may be
  * NULL.  The first call on a plan that needs scratch (r > 0,
- * STEPWISE) allocates it on the current device; it is reused afterwards.
- * A plan must not run on two streams at once (shared scratch).  An execute
- * only enqueues kernels (no memset, no synchronisation, no allocation once
- * the scratch exists), so after one call with the same device, batch and
- * stride it may be captured into a HIP graph. */
+ * STEPWISE) allocates it on the current device; it is reused afterwards,
+ * and a call that needs more (a larger batch or stride, another device)
+ * allocates a larger one and keeps the old one until ar_plan_destroy, so
+ * that graphs captured before stay valid.  A plan must not run on two
+ * streams at once (shared scratch).  An execute only enqueues kernels (no
+ * memset, no synchronisation, no allocation once the scratch exists), so
+ * after one call with the same device, batch and stride it may be captured
+ * into a HIP graph; a captured call that would have to allocate returns
+ * AR_ERR_UNSUPPORTED instead.  Graphs holding a plan's launches must not be
+ * replayed after ar_plan_destroy. */
 ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t stream);
 
-/* `batch` independent Allreduce instances per rank: instance j of rank x is
- * the n elements at rank_buffers[x] + j * instance_stride (in elements,
- * instance_stride >= n, (batch - 1) * instance_stride + n <= 2^46, else
- * AR_ERR_INVALID_ARG).  Each instance is split into blocks on its own. */
+/* `batch` independent Allreduce instances per rank (Sec. 1's operation
+ * applied to each; the exchanges of Sec. 5.3 as in ar_execute): instance j
+ * of rank x is the n elements at rank_buffers[x] + j * instance_stride (in
+ * elements, instance_stride >= n, (batch - 1) * instance_stride + n <= 2^46,
+ * else AR_ERR_INVALID_ARG).  Each instance is split into blocks on its own.
+ * Otherwise as ar_execute. */
 ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
                              hipStream_t stream);
 
@@ -287,6 +312,48 @@ ar_status ar_model_best_k(int32_t P, double m_bytes, double alpha, double beta, 
                           double* r_closed_form);
 ar_status ar_plan_model_time(const ar_plan* plan, double alpha, double beta, double gamma, double* tau_seconds);
 
+/* The Sec. 2 model for this library's two ways of running a plan on one GPU,
+ * where the P ranks share one HBM: a launch costs a fixed time (the paper's
+ * alpha) plus its HBM bytes over a bandwidth.  STEPWISE runs one launch per
+ * step and moves hbm_bytes_algorithmic (so with u bytes per block, a
+ * received block costs about 2P*u / step_bytes_per_s and a combination
+ * P*u / step_bytes_per_s: the paper's beta and gamma for P ranks on one
+ * device); FUSED runs fused_launches launches moving hbm_bytes_fused.
+ * Times are per call of ar_execute_batched with `batch` instances. */
+typedef struct {
+  double step_alpha;         /* seconds per step launch                          */
+  double step_bytes_per_s;   /* HBM bytes per second of a step launch            */
+  double fused_alpha;        /* seconds per fused launch                          */
+  double fused_bytes_per_s;  /* HBM bytes per second of the fused launches        */
+} ar_model_params;
+
+/* Parameters fitted on MI355X (gfx950) by timing both paths over message
+ * sizes (the library's calibration tool prints them for another device). */
+ar_status ar_model_default_params(ar_model_params* out);
+
+/* Model time of one call of ar_execute_batched on `plan` with `batch`
+ * instances on `path` (AR_PATH_AUTO: the path ar_execute would take).
+ * NULL params: the defaults.  AR_ERR_INVALID_ARG for NULL plan/output,
+ * batch < 1, non-positive bandwidths or negative alphas; AR_ERR_UNSUPPORTED
+ * for FUSED on a plan that cannot run fused. */
+ar_status ar_plan_model_seconds(const ar_plan* plan, const ar_model_params* params, int64_t batch, ar_path path,
+                                double* seconds);
+
+/* Plan with the step count chosen by the cost model (Sec. 8 picks the
+ * number of steps from alpha, beta and gamma measured on the machine;
+ * Sec. 10 measures them): every k in [L, 2L] of the butterfly schedules is
+ * priced on the STEPWISE path (ar_plan_model_seconds), and the cheapest k
+ * is taken (the smallest on a tie).  With `path` AR_PATH_AUTO the plan then
+ * runs FUSED if that path's model time is below the step-wise one at that
+ * k, else STEPWISE; AR_PATH_STEPWISE or AR_PATH_FUSED fixes the path (every
+ * fused plan moves the same bytes whatever k, so k still follows the
+ * step-wise prices, the paper's choice).  The plan's results are those of
+ * the chosen k (ar_plan_stats reports k and exec_path).  NULL params: the
+ * defaults.  Errors as ar_plan_create_ex, AR_ERR_INVALID_ARG for batch < 1
+ * or bad params, AR_ERR_UNSUPPORTED for FUSED with P = 1. */
+ar_status ar_plan_create_auto(int32_t P, int64_t n, ar_dtype dtype, ar_op op, ar_group group, int64_t batch,
+                              ar_path path, const ar_model_params* params, ar_plan** out_plan);
+
 /* Wait for the plan's last stream, free its scratch and the plan.  NULL is
  * accepted.  Must not be called while another thread executes the plan. */
 void ar_plan_destroy(ar_plan* plan);
@@ -294,7 +361,10 @@ void ar_plan_destroy(ar_plan* plan);
 /* Static text for a status code. */
 const char* ar_status_string(ar_status s);
 
-/* Detail of the last failure on the calling thread ("" if none). */
+/* Detail of the last failure on the calling thread ("" if none), e.g. the
+ * HIP error text.  The string stays valid until the thread's next call into
+ * the library.  ar_last_error is the same function under a shorter name. */
+const char* ar_last_error_message(void);
 const char* ar_last_error(void);
 
 #ifdef __cplusplus

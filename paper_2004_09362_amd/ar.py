@@ -27,10 +27,13 @@ AR_KIND_COPY, AR_KIND_REDUCE, AR_KIND_REDUCE2 = 0, 1, 2
 AR_GROUP_CYCLIC, AR_GROUP_XOR = 0, 1
 AR_SCHEDULE_BUTTERFLY, AR_SCHEDULE_RING = 0, 1
 
+AR_K_AUTO = -1
+
 EXPORTS = [
     "ar_plan_create", "ar_plan_create_ex", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
     "ar_plan_num_launches", "ar_plan_launch", "ar_plan_destroy", "ar_status_string", "ar_last_error",
-    "ar_model_time", "ar_model_best_k", "ar_plan_model_time", "ar_execute_timed", "ar_plan_dump",
+    "ar_last_error_message", "ar_model_time", "ar_model_best_k", "ar_plan_model_time", "ar_execute_timed",
+    "ar_plan_dump", "ar_model_default_params", "ar_plan_model_seconds", "ar_plan_create_auto",
 ]
 
 
@@ -52,8 +55,17 @@ class Stats(ctypes.Structure):
         ("hbm_bytes_stepwise", ctypes.c_int64), ("hbm_bytes_fused", ctypes.c_int64),
         ("workspace_bytes", ctypes.c_int64),
         ("group", ctypes.c_int32), ("schedule", ctypes.c_int32), ("fused_launches", ctypes.c_int32),
-        ("fused_flat", ctypes.c_int32),
+        ("fused_flat", ctypes.c_int32), ("exec_path", ctypes.c_int32), ("hbm_bytes_algorithmic", ctypes.c_int64),
     ]
+
+    def as_dict(self):
+        return {name: getattr(self, name) for name, _ in self._fields_}
+
+
+class ModelParams(ctypes.Structure):
+    """ar_model_params: the per-launch cost and HBM bandwidth of each path."""
+    _fields_ = [("step_alpha", ctypes.c_double), ("step_bytes_per_s", ctypes.c_double),
+                ("fused_alpha", ctypes.c_double), ("fused_bytes_per_s", ctypes.c_double)]
 
     def as_dict(self):
         return {name: getattr(self, name) for name, _ in self._fields_}
@@ -98,9 +110,16 @@ def _load():
     L.ar_status_string.restype = ctypes.c_char_p
     L.ar_last_error.argtypes = []
     L.ar_last_error.restype = ctypes.c_char_p
+    L.ar_last_error_message.argtypes = []
+    L.ar_last_error_message.restype = ctypes.c_char_p
+    L.ar_model_default_params.argtypes = [ctypes.POINTER(ModelParams)]
+    L.ar_plan_model_seconds.argtypes = [vp, ctypes.POINTER(ModelParams), i64, ctypes.c_int, ctypes.POINTER(dbl)]
+    L.ar_plan_create_auto.argtypes = [i32, i64, ctypes.c_int, ctypes.c_int, ctypes.c_int, i64, ctypes.c_int,
+                                      ctypes.POINTER(ModelParams), ctypes.POINTER(vp)]
     for name in ("ar_plan_create", "ar_plan_create_ex", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
                  "ar_plan_num_launches", "ar_plan_launch", "ar_model_time", "ar_model_best_k", "ar_plan_model_time",
-                 "ar_plan_dump", "ar_execute_timed"):
+                 "ar_plan_dump", "ar_execute_timed", "ar_model_default_params", "ar_plan_model_seconds",
+                 "ar_plan_create_auto"):
         getattr(L, name).restype = ctypes.c_int
     return L
 
@@ -114,6 +133,10 @@ def status_name(s: int) -> str:
 
 def ar_last_error() -> str:
     return lib.ar_last_error().decode()
+
+
+def ar_last_error_message() -> str:
+    return lib.ar_last_error_message().decode()
 
 
 def ar_status_string(s: int) -> str:
@@ -137,10 +160,21 @@ def _op_code(op) -> int:
     return {"sum": AR_SUM, "max": AR_MAX, AR_SUM: AR_SUM, AR_MAX: AR_MAX}[op]
 
 
+# What the binding checks rank buffers against before a call reaches the
+# library: P, n and dtype of each plan it created, by handle.
+_PLAN_INFO: dict = {}
+
+
+def _register(h: int, P: int, n: int, dtype_code: int) -> int:
+    _PLAN_INFO[h] = (P, n, dtype_code)
+    return h
+
+
 def ar_plan_create(P: int, n: int, dtype, op, k_steps: int) -> int:
     h = ctypes.c_void_p()
-    _check(lib.ar_plan_create(P, n, _dtype_code(dtype), _op_code(op), k_steps, ctypes.byref(h)), "ar_plan_create")
-    return h.value
+    dt = _dtype_code(dtype)
+    _check(lib.ar_plan_create(P, n, dt, _op_code(op), k_steps, ctypes.byref(h)), "ar_plan_create")
+    return _register(h.value, P, n, dt)
 
 
 def _group_code(group) -> int:
@@ -155,20 +189,109 @@ def _schedule_code(schedule) -> int:
 
 def ar_plan_create_ex(P: int, n: int, dtype, op, k_steps: int, group="cyclic", schedule="butterfly") -> int:
     h = ctypes.c_void_p()
-    _check(lib.ar_plan_create_ex(P, n, _dtype_code(dtype), _op_code(op), k_steps, _group_code(group),
+    dt = _dtype_code(dtype)
+    _check(lib.ar_plan_create_ex(P, n, dt, _op_code(op), k_steps, _group_code(group),
                                  _schedule_code(schedule), ctypes.byref(h)), "ar_plan_create_ex")
-    return h.value
+    return _register(h.value, P, n, dt)
+
+
+def ar_model_default_params() -> ModelParams:
+    mp = ModelParams()
+    _check(lib.ar_model_default_params(ctypes.byref(mp)), "ar_model_default_params")
+    return mp
+
+
+def _params(params):
+    """None, a ModelParams, or a dict with its four fields."""
+    if params is None:
+        return None
+    if isinstance(params, ModelParams):
+        return ctypes.byref(params)
+    mp = ar_model_default_params()
+    for key, val in dict(params).items():
+        if key not in dict(ModelParams._fields_):
+            raise KeyError("unknown model parameter %r" % key)
+        setattr(mp, key, float(val))
+    return ctypes.byref(mp)
+
+
+def ar_plan_create_auto(P: int, n: int, dtype, op, group="cyclic", batch: int = 1, path: int = AR_PATH_AUTO,
+                        params=None) -> int:
+    h = ctypes.c_void_p()
+    dt = _dtype_code(dtype)
+    _check(lib.ar_plan_create_auto(P, n, dt, _op_code(op), _group_code(group), batch, int(path), _params(params),
+                                   ctypes.byref(h)), "ar_plan_create_auto")
+    return _register(h.value, P, n, dt)
+
+
+def ar_plan_model_seconds(plan: int, params=None, batch: int = 1, path: int = AR_PATH_AUTO) -> float:
+    t = ctypes.c_double()
+    _check(lib.ar_plan_model_seconds(plan, _params(params), batch, int(path), ctypes.byref(t)),
+           "ar_plan_model_seconds")
+    return t.value
 
 
 def ar_plan_set_path(plan: int, path: int):
     _check(lib.ar_plan_set_path(plan, int(path)), "ar_plan_set_path")
 
 
-def _ptr_table(rank_buffers) -> ctypes.Array:
+_TORCH_DTYPE = {AR_INT32: torch.int32, AR_FLOAT32: torch.float32}
+
+
+def _ptr_table(plan: int, rank_buffers, batch: int = 1, instance_stride: int | None = None,
+               _on_gpu: bool = True) -> ctypes.Array:
+    """The host table of rank pointers, after checking what the library
+    cannot see: P entries, and for each torch tensor that it is contiguous,
+    on the current GPU, of the plan's dtype, and that its storage holds the
+    rank's (batch - 1) * instance_stride + n elements from the tensor's start.
+    Raw integers are taken as device addresses, unchecked.  A failed check
+    raises ArError(AR_ERR_INVALID_ARG) before anything is launched.
+    (``_on_gpu=False`` skips the device checks so that the host tests can
+    exercise the others on CPU tensors; every execute call keeps them.)"""
+    bufs = list(rank_buffers)
+    info = _PLAN_INFO.get(plan)
+    if info is None:  # a handle this binding did not create
+        st = ar_plan_stats(plan)
+        info = _PLAN_INFO[plan] = (st.P, st.n, None)
+    P, n, dt = info
+    if len(bufs) != P:
+        raise ArError(AR_ERR_INVALID_ARG, "rank buffers", "the plan has P=%d ranks, got %d buffers" % (P, len(bufs)))
+    if batch < 1:
+        raise ArError(AR_ERR_INVALID_ARG, "rank buffers", "batch must be >= 1")
+    stride = n if instance_stride is None or (batch == 1 and instance_stride < n) else instance_stride
+    extent = (batch - 1) * stride + n if n > 0 else 0
+    want = _TORCH_DTYPE.get(dt)
+    dev = None
+    storage_elems = {}
     addrs = []
-    for b in rank_buffers:
-        addrs.append(b.data_ptr() if isinstance(b, torch.Tensor) else int(b))
-    return (ctypes.c_void_p * len(addrs))(*addrs)
+    for x, b in enumerate(bufs):
+        if not isinstance(b, torch.Tensor):
+            addrs.append(int(b))
+            continue
+        if extent > 0:
+            if _on_gpu and not b.is_cuda:
+                raise ArError(AR_ERR_INVALID_ARG, "rank buffers", "rank %d's tensor is not on a GPU" % x)
+            if _on_gpu and dev is None:
+                dev = torch.cuda.current_device()
+            if _on_gpu and b.get_device() != dev:
+                raise ArError(AR_ERR_INVALID_ARG, "rank buffers",
+                              "rank %d's tensor is on cuda:%d, the current device is cuda:%d" % (x, b.get_device(), dev))
+            if want is not None and b.dtype != want:
+                raise ArError(AR_ERR_INVALID_ARG, "rank buffers",
+                              "rank %d's tensor is %s, the plan's dtype is %s" % (x, b.dtype, want))
+            if b.element_size() != 4 or not b.is_contiguous():
+                raise ArError(AR_ERR_INVALID_ARG, "rank buffers",
+                              "rank %d's tensor must be contiguous with 4-byte elements" % x)
+            base = b._base if b._base is not None else b
+            have = storage_elems.get(id(base))
+            if have is None:
+                have = storage_elems[id(base)] = base.untyped_storage().nbytes() // 4
+            if have - b.storage_offset() < extent:
+                raise ArError(AR_ERR_INVALID_ARG, "rank buffers",
+                              "rank %d's tensor holds %d elements from its start, the call needs %d "
+                              "((batch - 1) * instance_stride + n)" % (x, have - b.storage_offset(), extent))
+        addrs.append(b.data_ptr())
+    return (ctypes.c_void_p * P)(*addrs)
 
 
 def _stream_handle(stream) -> int:
@@ -180,24 +303,24 @@ def _stream_handle(stream) -> int:
 
 
 def ar_execute(plan: int, rank_buffers: Sequence, stream=None):
-    tbl = _ptr_table(rank_buffers)
+    tbl = _ptr_table(plan, rank_buffers)
     _check(lib.ar_execute(plan, tbl, _stream_handle(stream)), "ar_execute")
 
 
 def ar_execute_batched(plan: int, rank_buffers: Sequence, batch: int, instance_stride: int, stream=None):
-    tbl = _ptr_table(rank_buffers)
+    tbl = _ptr_table(plan, rank_buffers, batch, instance_stride)
     _check(lib.ar_execute_batched(plan, tbl, batch, instance_stride, _stream_handle(stream)), "ar_execute_batched")
 
 
 def ar_execute_timed(plan: int, rank_buffers: Sequence, batch: int = 1, instance_stride: int | None = None,
                      stream=None) -> list:
     """Execute, then wait for it; returns each launch's duration in ms."""
-    tbl = _ptr_table(rank_buffers)
     st = ar_plan_stats(plan)
+    stride = instance_stride if instance_stride is not None else st.n
+    tbl = _ptr_table(plan, rank_buffers, batch, stride)
     cap = max(st.launches, st.fused_launches, 1)  # launches of either path
     ms = (ctypes.c_float * cap)()
     n = ctypes.c_int32()
-    stride = instance_stride if instance_stride is not None else st.n
     _check(lib.ar_execute_timed(plan, tbl, batch, stride, _stream_handle(stream), ms, cap, ctypes.byref(n)),
            "ar_execute_timed")
     return list(ms[:min(n.value, cap)])
@@ -250,18 +373,28 @@ def ar_plan_model_time(plan: int, alpha: float, beta: float, gamma: float) -> fl
 
 
 def ar_plan_destroy(plan: int):
+    _PLAN_INFO.pop(plan, None)
     lib.ar_plan_destroy(plan)
 
 
 class Plan:
     """Owning handle around ``ar_plan*``.  ``k`` defaults to the
-    bandwidth-optimal 2 ceil(log2 P) (the Ring: 2(P-1))."""
+    bandwidth-optimal 2 ceil(log2 P) (the Ring: 2(P-1)); ``k="auto"`` (or
+    AR_K_AUTO) lets the cost model choose k and, unless ``path`` fixes it,
+    the path (ar_plan_create_auto, for ``batch`` instances per call)."""
 
-    def __init__(self, P: int, n: int, dtype, op="sum", k: int | None = None, path: int = AR_PATH_AUTO,
-                 group="cyclic", schedule="butterfly"):
+    def __init__(self, P: int, n: int, dtype, op="sum", k=None, path: int = AR_PATH_AUTO,
+                 group="cyclic", schedule="butterfly", batch: int = 1, params=None):
         L = max(0, (P - 1).bit_length())
         self.P, self.n = P, n
+        self.handle = None
         ring = _schedule_code(schedule) == AR_SCHEDULE_RING
+        if k in ("auto", AR_K_AUTO):
+            if ring:
+                raise ArError(AR_ERR_INVALID_ARG, "Plan", "the Ring has one step count, 2(P-1)")
+            self.handle = ar_plan_create_auto(P, n, dtype, op, group, batch, path, params)
+            self.k = ar_plan_stats(self.handle).k
+            return
         self.k = (2 * (P - 1) if ring else 2 * L) if k is None else k
         self.handle = ar_plan_create_ex(P, n, dtype, op, self.k, group, schedule)
         if path != AR_PATH_AUTO:
@@ -288,6 +421,9 @@ class Plan:
 
     def dump(self) -> str:
         return ar_plan_dump(self.handle)
+
+    def model_seconds(self, params=None, batch: int = 1, path: int = AR_PATH_AUTO) -> float:
+        return ar_plan_model_seconds(self.handle, params, batch, path)
 
     def close(self):
         if self.handle:

@@ -124,6 +124,9 @@ struct ar_plan {
   void* scratch = nullptr;
   size_t scratch_bytes = 0;
   int scratch_device = -1;
+  // Scratch buffers replaced by larger ones, with their devices: kept until
+  // ar_plan_destroy, since graphs captured earlier may still address them.
+  std::vector<std::pair<void*, int>> retired;
   hipStream_t last_stream = nullptr;
   bool ran = false;
 };
@@ -207,24 +210,28 @@ ar_status check_buffers(const ar_plan* pl, void* const* bufs, int64_t batch, int
   return AR_OK;
 }
 
-ar_status ensure_scratch(ar_plan* pl, size_t need, int device) {
+ar_status ensure_scratch(ar_plan* pl, size_t need, int device, hipStream_t stream) {
   if (pl->scratch && pl->scratch_bytes >= need && pl->scratch_device == device) return AR_OK;
-  if (pl->scratch) {
-    int cur = 0;
-    (void)hipGetDevice(&cur);
-    (void)hipSetDevice(pl->scratch_device);
-    hipError_t e = hipFree(pl->scratch);  // waits for work that still uses it
-    (void)hipSetDevice(cur);
-    pl->scratch = nullptr;
-    pl->scratch_bytes = 0;
-    if (e != hipSuccess) return hip_fail(e, "hipFree(scratch)");
+  // An allocation cannot be captured into a graph: refuse it there (the call
+  // is then not enqueued) rather than fail the capture.
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(stream, &cap) != hipSuccess) {
+    (void)hipGetLastError();
+    cap = hipStreamCaptureStatusNone;
   }
+  if (cap != hipStreamCaptureStatusNone)
+    return fail(AR_ERR_UNSUPPORTED, "the plan needs " + std::to_string(need) +
+                                        " bytes of scratch, which cannot be allocated while the stream is captured; "
+                                        "run one call with this device, batch and stride before capturing");
   void* p = nullptr;
   hipError_t e = hipMalloc(&p, need);
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(AR_ERR_OUT_OF_MEMORY, "scratch of " + std::to_string(need) + " bytes: " + hipGetErrorString(e));
   }
+  // the old buffer stays allocated until ar_plan_destroy: work already
+  // enqueued, and graphs captured earlier, may still use it
+  if (pl->scratch) pl->retired.push_back({pl->scratch, pl->scratch_device});
   pl->scratch = p;
   pl->scratch_bytes = need;
   pl->scratch_device = device;
@@ -306,7 +313,7 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
     // phase), one region per rank, X then Y.
     const int64_t rank_stride = round_up((batch - 1) * stride + s.n, 64);
     const size_t need = size_t(2) * s.P * size_t(rank_stride) * 4;
-    ar_status st = ensure_scratch(pl, need, device);
+    ar_status st = ensure_scratch(pl, need, device, stream);
     if (st != AR_OK) return st;
     a.scratch_rank_stride = rank_stride;
     a.scratch[0] = static_cast<char*>(pl->scratch);
@@ -565,10 +572,40 @@ std::string plan_text(const ar_plan* pl) {
 }
 }  // namespace
 
-extern "C" {
+namespace {
 
-ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_group group,
-                            ar_schedule schedule, ar_plan** out_plan) {
+// Cost-model parameters fitted on MI355X (gfx950): step-wise launches of
+// the gradient-sync and prime-sweep shapes and of the calibration sweeps
+// (P = 8, 37, 127) moved 6.0-6.3 TB/s of their algorithmic bytes, with
+// 3.4-4.2 us of fixed cost per launch when executes are enqueued back to
+// back; the fused kernels moved 5.2-6.4 TB/s, one launch (or a reducing
+// launch and a broadcast) per execute.
+constexpr ar_model_params kDefaultModel = {3.7e-6, 6.0e12, 4.0e-6, 5.6e12};
+
+bool model_params_ok(const ar_model_params& mp) {
+  return mp.step_alpha >= 0 && mp.fused_alpha >= 0 && mp.step_bytes_per_s > 0 && mp.fused_bytes_per_s > 0 &&
+         std::isfinite(mp.step_alpha) && std::isfinite(mp.fused_alpha) && std::isfinite(mp.step_bytes_per_s) &&
+         std::isfinite(mp.fused_bytes_per_s);
+}
+
+// Sec. 2's model on one GPU: every launch costs alpha, and its HBM bytes
+// cost 1 / bandwidth each (P ranks share the device).
+double model_seconds(const ar_plan* pl, const ar_model_params& mp, int64_t batch, int32_t path) {
+  const ar::Schedule& s = pl->s;
+  if (s.P < 2 || s.n == 0) return 0.0;
+  if (path == AR_PATH_FUSED) {
+    const double launches = pl->fused_split ? 2.0 : 1.0;
+    const double bytes = double(int64_t(2) * s.P + (pl->fused_split ? 1 : 0)) * double(s.n) * 4.0 * double(batch);
+    return launches * mp.fused_alpha + bytes / mp.fused_bytes_per_s;
+  }
+  const double bytes = double(s.hbm_blocks) * double(s.n) * 4.0 * double(batch);
+  return double(s.launches.size()) * mp.step_alpha + bytes / mp.step_bytes_per_s;
+}
+
+// Plan creation proper (ar_plan_create_ex without AR_K_AUTO); `log` lets
+// AR_LOG=1 print the plan (not the candidates the automatic choice prices).
+ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_group group,
+                      ar_schedule schedule, bool log, ar_plan** out_plan) {
   if (!out_plan) return fail(AR_ERR_INVALID_ARG, "out_plan is NULL");
   *out_plan = nullptr;
   if (int(dtype) != AR_INT32 && int(dtype) != AR_FLOAT32) return fail(AR_ERR_UNSUPPORTED, "dtype must be int32 or float32");
@@ -640,10 +677,26 @@ ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int3
       if (comma != nullptr && comma[1] >= '0' && comma[1] <= '9') pl->bcast_cap = cap_of(comma + 1);
     }
   }
-  if (env_mode("AR_LOG") == 1) std::fputs(plan_text(pl).c_str(), stderr);
+  if (log && env_mode("AR_LOG") == 1) std::fputs(plan_text(pl).c_str(), stderr);
   *out_plan = pl;
   g_err.clear();
   return AR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+ar_status ar_plan_create_ex(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_group group,
+                            ar_schedule schedule, ar_plan** out_plan) {
+  if (k_steps == AR_K_AUTO) {
+    if (!out_plan) return fail(AR_ERR_INVALID_ARG, "out_plan is NULL");
+    *out_plan = nullptr;
+    if (int(schedule) != AR_SCHEDULE_BUTTERFLY)
+      return fail(AR_ERR_INVALID_ARG, "AR_K_AUTO chooses among the butterfly schedules only");
+    return ar_plan_create_auto(P, n, dtype, op, group, 1, AR_PATH_AUTO, nullptr, out_plan);
+  }
+  return create_plan(P, n, dtype, op, k_steps, group, schedule, true, out_plan);
 }
 
 ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_plan** out_plan) {
@@ -742,6 +795,10 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
   out->workspace_bytes = s.uses_scratch ? int64_t(2) * s.P * round_up(s.n, 64) * 4 : 0;
   out->group = s.group;
   out->schedule = s.sched;
+  out->exec_path = s.P < 2 ? 0 : (plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok))
+                                     ? AR_PATH_FUSED
+                                     : AR_PATH_STEPWISE;
+  out->hbm_bytes_algorithmic = out->hbm_bytes_stepwise;
   return AR_OK;
 }
 
@@ -844,14 +901,90 @@ ar_status ar_plan_model_time(const ar_plan* plan, double alpha, double beta, dou
   return AR_OK;
 }
 
+ar_status ar_model_default_params(ar_model_params* out) {
+  if (!out) return fail(AR_ERR_INVALID_ARG, "out is NULL");
+  *out = kDefaultModel;
+  return AR_OK;
+}
+
+ar_status ar_plan_model_seconds(const ar_plan* plan, const ar_model_params* params, int64_t batch, ar_path path,
+                                double* seconds) {
+  if (!plan || !seconds) return fail(AR_ERR_INVALID_ARG, "NULL argument");
+  if (batch < 1) return fail(AR_ERR_INVALID_ARG, "batch must be >= 1");
+  const ar_model_params& mp = params ? *params : kDefaultModel;
+  if (!model_params_ok(mp)) return fail(AR_ERR_INVALID_ARG, "model alphas must be >= 0 and bandwidths > 0");
+  if (path != AR_PATH_AUTO && path != AR_PATH_STEPWISE && path != AR_PATH_FUSED)
+    return fail(AR_ERR_INVALID_ARG, "unknown path");
+  if (path == AR_PATH_AUTO)
+    path = plan->path == AR_PATH_FUSED || (plan->path == AR_PATH_AUTO && plan->fused_ok) ? AR_PATH_FUSED
+                                                                                         : AR_PATH_STEPWISE;
+  if (path == AR_PATH_FUSED && !plan->fused_ok) return fail(AR_ERR_UNSUPPORTED, "the plan cannot run fused");
+  *seconds = model_seconds(plan, mp, batch, path);
+  return AR_OK;
+}
+
+ar_status ar_plan_create_auto(int32_t P, int64_t n, ar_dtype dtype, ar_op op, ar_group group, int64_t batch,
+                              ar_path path, const ar_model_params* params, ar_plan** out_plan) {
+  if (!out_plan) return fail(AR_ERR_INVALID_ARG, "out_plan is NULL");
+  *out_plan = nullptr;
+  if (batch < 1) return fail(AR_ERR_INVALID_ARG, "batch must be >= 1");
+  if (path != AR_PATH_AUTO && path != AR_PATH_STEPWISE && path != AR_PATH_FUSED)
+    return fail(AR_ERR_INVALID_ARG, "unknown path");
+  const ar_model_params& mp = params ? *params : kDefaultModel;
+  if (!model_params_ok(mp)) return fail(AR_ERR_INVALID_ARG, "model alphas must be >= 0 and bandwidths > 0");
+  if (P < 1 || P > ar::kMaxP) return fail(AR_ERR_INVALID_ARG, "P must be in [1, 128]");
+  int32_t L = 0;
+  while ((1 << L) < P) ++L;
+  // Sec. 8: the number of steps that the model prices cheapest on the
+  // step-by-step schedule; the smallest k on a tie
+  ar_plan* best = nullptr;
+  double best_t = 0;
+  for (int32_t k = L; k <= 2 * L; ++k) {
+    ar_plan* p = nullptr;
+    const ar_status st = create_plan(P, n, dtype, op, k, group, AR_SCHEDULE_BUTTERFLY, false, &p);
+    if (st != AR_OK) {
+      ar_plan_destroy(best);
+      return st;
+    }
+    const double t = model_seconds(p, mp, batch, AR_PATH_STEPWISE);
+    if (!best || t < best_t) {
+      ar_plan_destroy(best);
+      best = p;
+      best_t = t;
+    } else {
+      ar_plan_destroy(p);
+    }
+  }
+  ar_path chosen = path;
+  if (path == AR_PATH_FUSED && !best->fused_ok) {
+    ar_plan_destroy(best);
+    return fail(AR_ERR_UNSUPPORTED, "a single rank has nothing to fuse");
+  }
+  if (path == AR_PATH_AUTO)
+    chosen = best->fused_ok && model_seconds(best, mp, batch, AR_PATH_FUSED) < best_t ? AR_PATH_FUSED
+                                                                                     : AR_PATH_STEPWISE;
+  best->path = chosen;
+  auto env_on = [](const char* name) {
+    const char* e = std::getenv(name);
+    return e != nullptr && e[0] == '1';
+  };
+  if (env_on("AR_LOG")) std::fputs(plan_text(best).c_str(), stderr);
+  *out_plan = best;
+  g_err.clear();
+  return AR_OK;
+}
+
 void ar_plan_destroy(ar_plan* plan) {
   if (!plan) return;
-  if (plan->scratch) {
+  if (plan->scratch) plan->retired.push_back({plan->scratch, plan->scratch_device});
+  if (!plan->retired.empty()) {
     // hipFree waits for the device to finish the work that still uses it
     int cur = 0;
     (void)hipGetDevice(&cur);
-    (void)hipSetDevice(plan->scratch_device);
-    (void)hipFree(plan->scratch);
+    for (const auto& r : plan->retired) {
+      (void)hipSetDevice(r.second);
+      (void)hipFree(r.first);
+    }
     (void)hipSetDevice(cur);
   }
   delete plan;
@@ -870,6 +1003,8 @@ const char* ar_status_string(ar_status s) {
   }
   return "unknown status";
 }
+
+const char* ar_last_error_message(void) { return g_err.c_str(); }
 
 const char* ar_last_error(void) { return g_err.c_str(); }
 

@@ -53,6 +53,7 @@
 namespace fake {
 thread_local bool device_ok = true;
 thread_local bool malloc_fails = false;
+thread_local bool capturing = false;  // every stream reports an active graph capture
 thread_local int launch_error = 0;  // hipError_t value every launcher returns when set
 thread_local int64_t live_allocs = 0, total_allocs = 0;
 std::atomic<uintptr_t> next_addr{uintptr_t(1) << 44};
@@ -81,6 +82,10 @@ hipError_t hipMalloc(void** p, size_t bytes) {
   *p = reinterpret_cast<void*>(fake::next_addr.fetch_add((bytes + 0xFFFF) & ~size_t(0xFFFF)));
   ++fake::live_allocs;
   ++fake::total_allocs;
+  return hipSuccess;
+}
+hipError_t hipStreamIsCapturing(hipStream_t, hipStreamCaptureStatus* st) {
+  *st = fake::capturing ? hipStreamCaptureStatusActive : hipStreamCaptureStatusNone;
   return hipSuccess;
 }
 hipError_t hipFree(void* p) {
@@ -545,13 +550,23 @@ static void execute_errors() {
   EXPECT(fake::launches.empty() && fake::live_allocs == 0, "launched or kept memory after a failed allocation");
   fake::malloc_fails = false;
   EXPECT(ar_execute(pl, bufs.data(), stream_tag()) == AR_OK && fake::live_allocs == 1, "execute after the failure");
-  // regrowth for a larger batch fails: the old scratch is released, the error reported
+  // regrowth for a larger batch fails: the error is reported and the old
+  // scratch stays (graphs captured earlier may address it)
   std::vector<void*> big = fake_buffers(7, 4 * n * 4);
   fake::malloc_fails = true;
   EXPECT(ar_execute_batched(pl, big.data(), 4, n, stream_tag()) == AR_ERR_OUT_OF_MEMORY, "regrowth failure");
-  EXPECT(fake::live_allocs == 0, "scratch kept after a failed regrowth");
+  EXPECT(fake::live_allocs == 1, "old scratch released after a failed regrowth");
   fake::malloc_fails = false;
-  EXPECT(ar_execute_batched(pl, big.data(), 4, n, stream_tag()) == AR_OK && fake::live_allocs == 1, "regrowth");
+  // regrowth while the stream is being captured: refused before any launch
+  // or allocation; a call that fits the scratch may be captured
+  fake::capturing = true;
+  fake::launches.clear();
+  EXPECT(ar_execute_batched(pl, big.data(), 4, n, stream_tag()) == AR_ERR_UNSUPPORTED, "regrowth under capture");
+  EXPECT(fake::launches.empty() && fake::live_allocs == 1, "work or allocation after a refused capture");
+  EXPECT(ar_execute(pl, bufs.data(), stream_tag()) == AR_OK, "capture without regrowth");
+  fake::capturing = false;
+  EXPECT(ar_execute_batched(pl, big.data(), 4, n, stream_tag()) == AR_OK && fake::live_allocs == 2,
+         "regrowth keeps the old scratch until destroy");
   // a smaller call reuses the scratch
   const int64_t before = fake::total_allocs;
   EXPECT(ar_execute(pl, bufs.data(), stream_tag()) == AR_OK && fake::total_allocs == before, "scratch reuse");

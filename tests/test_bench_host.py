@@ -83,12 +83,34 @@ def test_kernel_families_cover_every_source():
 
 
 def test_cpu_baseline_runs_the_oracle_on_a_sample():
+    import torch
+
     for workload, group, schedule in (("gradsync32", "xor", "butterfly"), ("gradsync", "cyclic", "ring")):
         _, jobs = bench.jobs_for(workload, 10 if group == "xor" else None, group, schedule)
-        j = dict(jobs[0], n=64 * jobs[0]["P"])
+        j = dict(jobs[0], n=64 * jobs[0]["P"] + 5)
         x = np.random.default_rng(0).normal(size=(j["P"], j["n"])).astype(np.float32)
-        cb = bench.cpu_baseline([j], [x], budget_s=0.05, group=group, schedule=schedule)
+        fetchers = bench.sample_fetchers([j], [torch.from_numpy(x)])
+        # the sample is the first columns of every block, copied before any step
+        xs, cols = fetchers[0]("columns", 3)
+        starts = [b * (j["n"] // j["P"]) + min(b, j["n"] % j["P"]) for b in range(j["P"])]
+        assert list(cols) == [s + c for s in starts for c in range(3)]
+        assert np.array_equal(xs, x[:, cols])
+        cb = bench.cpu_baseline([j], fetchers, budget_s=0.05, group=group, schedule=schedule)
         assert cb["kind"] == "oracle" and cb["cores"] == 1 and cb["value"] > 0 and cb["unit"] == "GB/s"
+        assert cb["nproc"] >= 1 and isinstance(cb["cpu_model"], str)
+    # a batch: whole instances
+    _, jobs = bench.jobs_for("small_batch", None)
+    j = dict(jobs[0], batch=8)
+    x = np.random.default_rng(1).normal(size=(j["P"], j["batch"] * j["n"])).astype(np.float32)
+    fetchers = bench.sample_fetchers([j], [torch.from_numpy(x)])
+    assert np.array_equal(fetchers[0]("instances", 3), x.reshape(j["P"], 8, j["n"])[:, :3])
+    cb = bench.cpu_baseline([j], fetchers, budget_s=0.05)
+    assert cb["value"] > 0 and "instances" in cb["sample"]
+
+
+def test_host_facts():
+    f = bench.host_facts()
+    assert f["nproc"] >= 1 and f["cpu_model"]
 
 
 def _write_counters(d, counter, rows):

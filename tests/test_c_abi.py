@@ -1,8 +1,9 @@
 """The C ABI used from C: a C99 program includes include/ar.h, links
 libar.so directly (no Python, no torch) and exercises every entry point that
 needs no device memory -- plan construction for each group and schedule,
-stats, launch introspection, the cost model, and the argument errors that
-are reported before any launch.  No GPU is needed; nothing is launched."""
+the automatic step count, stats, launch introspection, the cost model, and
+the argument errors that are reported before any launch.  No GPU is needed;
+nothing is launched (tests/test_gpu_c_abi.py runs a C program on the GPU)."""
 import os
 import subprocess
 
@@ -106,6 +107,26 @@ int main(void) {
     CHECK(ar_model_best_k(127, 425.0, 3e-5, 1e-8, 2e-10, &k, &r) == AR_OK && k == 7);
     CHECK(ar_model_time(127, 425.0, 14, 3e-5, 1e-8, 2e-10, &t) == AR_OK && t > 14 * 3e-5);
     CHECK(ar_model_time(127, 425.0, 15, 3e-5, 1e-8, 2e-10, &t) == AR_ERR_INVALID_ARG);
+  }
+  /* automatic step count and path: the sentinel and the explicit call */
+  {
+    ar_model_params mp;
+    double ts = 0, tf = 0;
+    CHECK(ar_model_default_params(&mp) == AR_OK && mp.step_alpha > 0 && mp.fused_bytes_per_s > 0);
+    CHECK(ar_plan_create(37, 1 << 20, AR_FLOAT32, AR_SUM, AR_K_AUTO, &p) == AR_OK);
+    CHECK(ar_plan_stats(p, &st) == AR_OK && st.k >= 6 && st.k <= 12 && st.exec_path == AR_PATH_FUSED);
+    CHECK(st.hbm_bytes_algorithmic == st.hbm_bytes_stepwise);
+    CHECK(ar_plan_model_seconds(p, &mp, 1, AR_PATH_STEPWISE, &ts) == AR_OK);
+    CHECK(ar_plan_model_seconds(p, NULL, 1, AR_PATH_FUSED, &tf) == AR_OK && tf < ts);
+    ar_plan_destroy(p);
+    mp.fused_bytes_per_s = 1.0; /* a fused path this slow loses: the plan runs step by step */
+    CHECK(ar_plan_create_auto(37, 1 << 20, AR_FLOAT32, AR_SUM, AR_GROUP_CYCLIC, 1, AR_PATH_AUTO, &mp, &p) == AR_OK);
+    CHECK(ar_plan_stats(p, &st) == AR_OK && st.exec_path == AR_PATH_STEPWISE);
+    ar_plan_destroy(p);
+    mp.step_alpha = -1.0;
+    CHECK(ar_plan_create_auto(37, 100, AR_FLOAT32, AR_SUM, AR_GROUP_CYCLIC, 1, AR_PATH_AUTO, &mp, &p) ==
+          AR_ERR_INVALID_ARG);
+    CHECK(strlen(ar_last_error_message()) > 0 && strcmp(ar_last_error_message(), ar_last_error()) == 0);
   }
   CHECK(strcmp(ar_status_string(AR_OK), "ok") == 0);
   CHECK(strcmp(ar_status_string((ar_status)42), "unknown status") == 0);

@@ -121,3 +121,104 @@ def test_model_rejects_bad_arguments():
         ar.ar_model_time(7, 1.0, 3, -1.0, BETA, GAMMA)
     k, r = ar.ar_model_best_k(2, 425.0, ALPHA, BETA, GAMMA)
     assert k == 1 and math.isnan(r)
+
+
+# ---- automatic step count and path (ar_plan_create_auto, AR_K_AUTO) ----
+
+def _stats(h):
+    return ar.ar_plan_stats(h)
+
+
+def test_model_seconds_is_launches_plus_bytes_over_bandwidth():
+    mp = {"step_alpha": 2e-6, "step_bytes_per_s": 5e12, "fused_alpha": 3e-6, "fused_bytes_per_s": 4e12}
+    for P, n, k in ((7, 1000, 5), (37, 4096, 12), (127, 2304, 10), (128, 999, 14), (2, 10, 1)):
+        plan = ar.Plan(P, n, "float32", "sum", k)
+        st = plan.stats()
+        for batch in (1, 9):
+            step = plan.model_seconds(mp, batch, ar.AR_PATH_STEPWISE)
+            assert step == pytest.approx(st.launches * 2e-6 + st.hbm_bytes_algorithmic * batch / 5e12, rel=1e-12)
+            fused = plan.model_seconds(mp, batch, ar.AR_PATH_FUSED)
+            assert fused == pytest.approx(st.fused_launches * 3e-6 + st.hbm_bytes_fused * batch / 4e12, rel=1e-12)
+            assert plan.model_seconds(mp, batch) == fused  # AUTO: the path ar_execute takes
+    assert st.hbm_bytes_algorithmic == st.hbm_bytes_stepwise
+
+
+@pytest.mark.parametrize("P", [2, 3, 7, 8, 12, 24, 37, 64, 127, 128])
+def test_auto_k_is_the_cheapest_step_count(P):
+    """Sec. 8: the number of steps is the one the model prices cheapest; the
+    plan then runs on the cheaper path at that k."""
+    L = ceil_log2(P)
+    mp = ar.ar_model_default_params()
+    for n in (P, 106 * P, 2304 * P, 1 << 22, 1 << 26):
+        for batch in (1, 64):
+            h = ar.ar_plan_create_auto(P, n, "float32", "sum", batch=batch)
+            st = _stats(h)
+            cost = {}
+            for k in range(L, 2 * L + 1):
+                p = ar.Plan(P, n, "float32", "sum", k)
+                cost[k] = p.model_seconds(mp, batch, ar.AR_PATH_STEPWISE)
+            best = min(cost.values())
+            assert st.k == min(k for k in cost if cost[k] == best), (P, n, batch)
+            chosen = ar.Plan(P, n, "float32", "sum", st.k)
+            fused = chosen.model_seconds(mp, batch, ar.AR_PATH_FUSED)
+            want_path = ar.AR_PATH_FUSED if fused < best else ar.AR_PATH_STEPWISE
+            assert st.exec_path == want_path, (P, n, batch)
+            ar.ar_plan_destroy(h)
+
+
+def test_auto_k_follows_the_latency_bandwidth_trade_off():
+    """With a per-step cost that dominates small messages (the situation of
+    Sec. 8), small messages get the latency-optimal k = L and large ones the
+    bandwidth-optimal k = 2L, and k never falls as the message grows."""
+    mp = {"step_alpha": 1e-4, "step_bytes_per_s": 1e10, "fused_alpha": 1e-4, "fused_bytes_per_s": 1e10}
+    for P in (5, 12, 37, 127):
+        L = ceil_log2(P)
+        ks = []
+        for e in range(0, 28, 3):
+            h = ar.ar_plan_create_auto(P, P << e, "float32", "sum", path=ar.AR_PATH_STEPWISE, params=mp)
+            ks.append(_stats(h).k)
+            assert _stats(h).exec_path == ar.AR_PATH_STEPWISE
+            ar.ar_plan_destroy(h)
+        assert ks[0] == L and ks[-1] == 2 * L, (P, ks)
+        assert ks == sorted(ks), (P, ks)
+
+
+def test_auto_k_sentinel_and_fixed_paths():
+    h = ar.ar_plan_create(37, 1 << 20, "float32", "sum", ar.AR_K_AUTO)
+    h2 = ar.ar_plan_create_auto(37, 1 << 20, "float32", "sum")
+    assert _stats(h).k == _stats(h2).k and _stats(h).exec_path == _stats(h2).exec_path
+    for path in (ar.AR_PATH_STEPWISE, ar.AR_PATH_FUSED):
+        h3 = ar.ar_plan_create_auto(37, 1 << 20, "int32", "max", "cyclic", 1, path)
+        assert _stats(h3).exec_path == path and _stats(h3).k == _stats(h).k
+        ar.ar_plan_destroy(h3)
+    hx = ar.ar_plan_create_auto(32, 1 << 20, "float32", "sum", "xor")
+    assert _stats(hx).group == ar.AR_GROUP_XOR and 5 <= _stats(hx).k <= 10
+    p = ar.Plan(24, 1000, "float32", "sum", "auto")
+    assert p.k == p.stats().k
+    for hh in (h, h2, hx):
+        ar.ar_plan_destroy(hh)
+    # one rank: k = 0 on the step-wise path, nothing to fuse
+    h1 = ar.ar_plan_create_auto(1, 100, "float32", "sum")
+    assert _stats(h1).k == 0 and _stats(h1).exec_path == 0
+    ar.ar_plan_destroy(h1)
+
+
+def test_auto_k_rejections():
+    def refused(fn, status):
+        with pytest.raises(ar.ArError) as ei:
+            fn()
+        assert ei.value.status == status
+
+    refused(lambda: ar.ar_plan_create_auto(37, 100, "float32", "sum", batch=0), ar.AR_ERR_INVALID_ARG)
+    refused(lambda: ar.ar_plan_create_auto(37, 100, "float32", "sum", params={"step_bytes_per_s": 0.0}),
+            ar.AR_ERR_INVALID_ARG)
+    refused(lambda: ar.ar_plan_create_auto(37, 100, "float32", "sum", params={"fused_alpha": -1.0}),
+            ar.AR_ERR_INVALID_ARG)
+    refused(lambda: ar.ar_plan_create_auto(12, 100, "float32", "sum", "xor"), ar.AR_ERR_INVALID_ARG)
+    refused(lambda: ar.ar_plan_create_auto(129, 100, "float32", "sum"), ar.AR_ERR_INVALID_ARG)
+    refused(lambda: ar.ar_plan_create_auto(1, 100, "float32", "sum", path=ar.AR_PATH_FUSED), ar.AR_ERR_UNSUPPORTED)
+    refused(lambda: ar.ar_plan_create_ex(7, 100, "float32", "sum", ar.AR_K_AUTO, "cyclic", "ring"),
+            ar.AR_ERR_INVALID_ARG)
+    plan = ar.Plan(1, 100, "float32", "sum", 0)
+    refused(lambda: plan.model_seconds(None, 1, ar.AR_PATH_FUSED), ar.AR_ERR_UNSUPPORTED)
+    refused(lambda: plan.model_seconds(None, 0), ar.AR_ERR_INVALID_ARG)
