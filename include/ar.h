@@ -258,6 +258,22 @@ ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t strea
 ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
                              hipStream_t stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): ar_execute_batched
+ * that never allocates.  Fused plans need no scratch; a step-wise plan with
+ * r > 0 keeps its X and Y buffers in a device array inside the library
+ * instead of the plan's scratch: 2 * P * round_up((batch - 1) *
+ * instance_stride + n, 64) * 4 bytes must not exceed 64 MiB
+ * (AR_ERR_UNSUPPORTED otherwise, nothing enqueued).  Each GPU that runs this
+ * call holds that array from its first call until the process ends, and
+ * every call on that GPU, from any plan or thread, shares it: calls that may
+ * overlap on one GPU (other streams, other threads) race and must be
+ * ordered by the caller.  Nothing in the array needs clearing: each call
+ * writes every scratch element before reading it.  No hipMalloc, hipFree,
+ * memset or host synchronisation; otherwise as ar_execute_batched. */
+ar_status ar_execute_noalloc(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
+                             hipStream_t stream);
+
 /* Per-launch timing, for debugging and for measuring the per-step cost that
  * the model of Sec. 2 prices (alpha + beta*m + gamma*m per step).  As
  * ar_execute_batched, and in addition a timing-only HIP event (no

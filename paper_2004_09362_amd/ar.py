@@ -34,6 +34,7 @@ EXPORTS = [
     "ar_plan_num_launches", "ar_plan_launch", "ar_plan_destroy", "ar_status_string", "ar_last_error",
     "ar_last_error_message", "ar_model_time", "ar_model_best_k", "ar_plan_model_time", "ar_execute_timed",
     "ar_plan_dump", "ar_model_default_params", "ar_plan_model_seconds", "ar_plan_create_auto",
+    "ar_execute_noalloc",
 ]
 
 
@@ -94,6 +95,7 @@ def _load():
     L.ar_plan_set_path.argtypes = [vp, ctypes.c_int]
     L.ar_execute.argtypes = [vp, ctypes.POINTER(vp), vp]
     L.ar_execute_batched.argtypes = [vp, ctypes.POINTER(vp), i64, i64, vp]
+    L.ar_execute_noalloc.argtypes = [vp, ctypes.POINTER(vp), i64, i64, vp]
     L.ar_plan_stats.argtypes = [vp, ctypes.POINTER(Stats)]
     L.ar_plan_num_launches.argtypes = [vp, ctypes.POINTER(i32)]
     L.ar_plan_launch.argtypes = [vp, i32, ctypes.POINTER(LaunchDesc), ctypes.POINTER(RangeDesc), i32]
@@ -119,7 +121,7 @@ def _load():
     for name in ("ar_plan_create", "ar_plan_create_ex", "ar_plan_set_path", "ar_execute", "ar_execute_batched", "ar_plan_stats",
                  "ar_plan_num_launches", "ar_plan_launch", "ar_model_time", "ar_model_best_k", "ar_plan_model_time",
                  "ar_plan_dump", "ar_execute_timed", "ar_model_default_params", "ar_plan_model_seconds",
-                 "ar_plan_create_auto"):
+                 "ar_plan_create_auto", "ar_execute_noalloc"):
         getattr(L, name).restype = ctypes.c_int
     return L
 
@@ -312,6 +314,13 @@ def ar_execute_batched(plan: int, rank_buffers: Sequence, batch: int, instance_s
     _check(lib.ar_execute_batched(plan, tbl, batch, instance_stride, _stream_handle(stream)), "ar_execute_batched")
 
 
+def ar_execute_noalloc(plan: int, rank_buffers: Sequence, batch: int, instance_stride: int, stream=None):
+    """ar_execute_batched that never allocates device memory (scratch from
+    the library's per-device array; see include/ar.h)."""
+    tbl = _ptr_table(plan, rank_buffers, batch, instance_stride)
+    _check(lib.ar_execute_noalloc(plan, tbl, batch, instance_stride, _stream_handle(stream)), "ar_execute_noalloc")
+
+
 def ar_execute_timed(plan: int, rank_buffers: Sequence, batch: int = 1, instance_stride: int | None = None,
                      stream=None) -> list:
     """Execute, then wait for it; returns each launch's duration in ms."""
@@ -414,6 +423,9 @@ class Plan:
 
     def batched(self, rank_buffers, batch: int, instance_stride: int, stream=None):
         ar_execute_batched(self.handle, rank_buffers, batch, instance_stride, stream)
+
+    def noalloc(self, rank_buffers, batch: int, instance_stride: int, stream=None):
+        ar_execute_noalloc(self.handle, rank_buffers, batch, instance_stride, stream)
 
     def timed(self, rank_buffers, batch: int = 1, instance_stride: int | None = None, stream=None) -> list:
         """Execute and wait; the duration of each launch in milliseconds."""

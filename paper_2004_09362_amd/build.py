@@ -17,7 +17,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libar.so")
 SOURCES = [os.path.join(CSRC, f) for f in ["plan.cpp", "capi.cpp", "kernels.hip", "fused_lo.hip", "fused_group.hip",
-                                           "broadcast.hip"] +
+                                           "broadcast.hip", "noalloc.hip"] +
            ["fused_col_g%d.hip" % i for i in range(8)]]
 HEADERS = [os.path.join(CSRC, f) for f in ("ar_internal.hpp", "device_common.hpp", "fused_col.hpp")] + [
     os.path.join(ROOT, "include", "ar.h")]
@@ -77,7 +77,7 @@ def build(verbose: bool = False, incremental: bool = False) -> str:
 # one family stays valid while only another family's sources change.
 COMMON = ["capi.cpp", "ar_internal.hpp", "device_common.hpp"]
 FAMILIES = {
-    "step": ["kernels.hip", "plan.cpp"],
+    "step": ["kernels.hip", "plan.cpp", "noalloc.hip"],
     "lo": ["fused_lo.hip"],
     "col": ["fused_col.hpp"] + ["fused_col_g%d.hip" % i for i in range(8)],
     "group": ["fused_group.hip"],

@@ -15,6 +15,10 @@ constexpr int kMaxRanges = 8;    // placement ranges per launch
 // it -- bytes, tiles, products with P -- fits in 64-bit arithmetic.
 constexpr int64_t kMaxRankElems = int64_t(1) << 46;
 constexpr int kFusedMaxP = 16;   // largest P of the register-resident fused kernel
+// Size of the device-resident scratch of ar_execute_noalloc (noalloc.hip):
+// the X and Y buffers of a step-wise plan with r > 0 take 2 * P rank
+// regions of the call's extent rounded up to 64 elements.
+constexpr int64_t kNoAllocScratchBytes = int64_t(64) << 20;
 
 enum Buf : int32_t { kBufNone = -1, kBufU = 0, kBufX = 1, kBufY = 2 };
 enum Kind : int32_t { kCopy = 0, kReduce = 1, kReduce2 = 2 };
@@ -208,6 +212,10 @@ int launch_fused_ring(const ColArgs& a, int dtype, int op, bool nt, int grid, vo
 // Second half of a split fused launch (broadcast.hip): block b's result,
 // stored on rank b by the reducing kernel, copied to the other P - 1 ranks.
 int launch_broadcast(const ColArgs& a, int dtype, bool nt, int grid, void* stream);
+// Device address of the allocation-free scratch (noalloc.hip) on `device`,
+// which must be the current device; looked up on the first call per device.
+// Returns a hipError_t value.
+int noalloc_scratch(int device, void** ptr);
 // Workgroups of a step launch over `total_tiles` wave tiles, and the tile size.
 int step_grid(int64_t total_tiles);
 int64_t step_tile_elems();

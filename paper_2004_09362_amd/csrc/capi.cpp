@@ -7,6 +7,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <array>
 #include <atomic>
 #include <cmath>
 #include <cstdint>
@@ -192,18 +193,18 @@ int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
 ar_status check_buffers(const ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool* all16) {
   const int32_t P = pl->s.P;
   const int64_t extent = ((batch - 1) * stride + pl->s.n) * 4;
-  std::vector<std::pair<uintptr_t, int32_t>> sorted;
-  sorted.reserve(P);
+  // on the stack (P <= 128): the allocation-free entry point uses this too
+  std::array<std::pair<uintptr_t, int32_t>, ar::kMaxP> sorted;
   *all16 = true;
   for (int32_t x = 0; x < P; ++x) {
     const uintptr_t p = reinterpret_cast<uintptr_t>(bufs[x]);
     if (p == 0) return fail(AR_ERR_INVALID_ARG, "rank buffer " + std::to_string(x) + " is NULL");
     if (p % 4 != 0) return fail(AR_ERR_INVALID_ARG, "rank buffer " + std::to_string(x) + " is not 4-byte aligned");
     if (p % 16 != 0) *all16 = false;
-    sorted.push_back({p, x});
+    sorted[size_t(x)] = {p, x};
   }
-  std::sort(sorted.begin(), sorted.end());
-  for (size_t i = 1; i < sorted.size(); ++i)
+  std::sort(sorted.begin(), sorted.begin() + P);
+  for (size_t i = 1; i < size_t(P); ++i)
     if (extent > 0 && sorted[i].first < sorted[i - 1].first + uintptr_t(extent))
       return fail(AR_ERR_ALIAS, "rank buffers " + std::to_string(sorted[i - 1].second) + " and " +
                                     std::to_string(sorted[i].second) + " overlap");
@@ -297,7 +298,7 @@ struct LaunchTimer {
 };
 
 ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool vec, hipStream_t stream,
-                       int device, LaunchTimer* tm) {
+                       int device, LaunchTimer* tm, bool noalloc) {
   const ar::Schedule& s = pl->s;
   ar::StepArgs a;
   std::memset(&a, 0, sizeof a);
@@ -313,11 +314,25 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
     // phase), one region per rank, X then Y.
     const int64_t rank_stride = round_up((batch - 1) * stride + s.n, 64);
     const size_t need = size_t(2) * s.P * size_t(rank_stride) * 4;
-    ar_status st = ensure_scratch(pl, need, device, stream);
-    if (st != AR_OK) return st;
+    char* base = nullptr;
+    if (noalloc) {
+      // the device's file-scope array (noalloc.hip), never an allocation
+      if (need > size_t(ar::kNoAllocScratchBytes))
+        return fail(AR_ERR_UNSUPPORTED, "the call needs " + std::to_string(need) +
+                                            " bytes of scratch; ar_execute_noalloc holds at most " +
+                                            std::to_string(ar::kNoAllocScratchBytes));
+      void* p = nullptr;
+      const int e = ar::noalloc_scratch(device, &p);
+      if (e != 0) return hip_fail(hipError_t(e), "hipGetSymbolAddress(scratch)");
+      base = static_cast<char*>(p);
+    } else {
+      ar_status st = ensure_scratch(pl, need, device, stream);
+      if (st != AR_OK) return st;
+      base = static_cast<char*>(pl->scratch);
+    }
     a.scratch_rank_stride = rank_stride;
-    a.scratch[0] = static_cast<char*>(pl->scratch);
-    a.scratch[1] = static_cast<char*>(pl->scratch) + size_t(s.P) * size_t(rank_stride) * 4;
+    a.scratch[0] = base;
+    a.scratch[1] = base + size_t(s.P) * size_t(rank_stride) * 4;
   }
   const int64_t max_len = a.q + (a.m ? 1 : 0);
   const int64_t tile = ar::step_tile_elems();
@@ -487,7 +502,7 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
 }
 
 ar_status execute_impl(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
-                       hipStream_t stream, LaunchTimer* tm) {
+                       hipStream_t stream, LaunchTimer* tm, bool noalloc = false) {
   if (!plan) return fail(AR_ERR_INVALID_ARG, "plan is NULL");
   if (!rank_buffers) return fail(AR_ERR_INVALID_ARG, "rank_buffers is NULL");
   if (batch < 1) return fail(AR_ERR_INVALID_ARG, "batch must be >= 1");
@@ -515,7 +530,7 @@ ar_status execute_impl(ar_plan* plan, void* const* rank_buffers, int64_t batch, 
     st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream, device, tm);
   } else {
     const bool vec = all16 && (batch == 1 || instance_stride % 4 == 0);
-    st = run_stepwise(plan, rank_buffers, batch, instance_stride, vec, stream, device, tm);
+    st = run_stepwise(plan, rank_buffers, batch, instance_stride, vec, stream, device, tm, noalloc);
   }
   if (st == AR_OK) {
     plan->last_stream = stream;
@@ -716,6 +731,11 @@ ar_status ar_plan_set_path(ar_plan* plan, ar_path path) {
 ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
                              hipStream_t stream) {
   return execute_impl(plan, rank_buffers, batch, instance_stride, stream, nullptr);
+}
+
+ar_status ar_execute_noalloc(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
+                             hipStream_t stream) {
+  return execute_impl(plan, rank_buffers, batch, instance_stride, stream, nullptr, true);
 }
 
 ar_status ar_execute(ar_plan* plan, void* const* rank_buffers, hipStream_t stream) {

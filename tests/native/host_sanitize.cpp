@@ -88,6 +88,14 @@ hipError_t hipStreamIsCapturing(hipStream_t, hipStreamCaptureStatus* st) {
   *st = fake::capturing ? hipStreamCaptureStatusActive : hipStreamCaptureStatusNone;
   return hipSuccess;
 }
+// the allocation-free entry point's device array (noalloc.hip): one fake
+// address, never an allocation
+namespace ar {
+int noalloc_scratch(int device, void** ptr) {
+  *ptr = device == 0 ? reinterpret_cast<void*>(uintptr_t(1) << 42) : nullptr;
+  return device == 0 ? 0 : int(hipErrorInvalidDevice);
+}
+}  // namespace ar
 hipError_t hipFree(void* p) {
   if (p) --fake::live_allocs;
   return hipSuccess;
@@ -570,6 +578,24 @@ static void execute_errors() {
   // a smaller call reuses the scratch
   const int64_t before = fake::total_allocs;
   EXPECT(ar_execute(pl, bufs.data(), stream_tag()) == AR_OK && fake::total_allocs == before, "scratch reuse");
+  // the allocation-free entry point: no allocation, the library's array as X / Y
+  {
+    const int64_t allocs = fake::total_allocs, live = fake::live_allocs;
+    fake::launches.clear();
+    fake::malloc_fails = true;  // any allocation attempt would fail the call
+    EXPECT(ar_execute_noalloc(pl, big.data(), 4, n, stream_tag()) == AR_OK && !fake::launches.empty(),
+           "allocation-free execute");
+    EXPECT(ar_execute_noalloc(pl, bufs.data(), 1, n, stream_tag()) == AR_OK, "allocation-free, smaller call");
+    fake::malloc_fails = false;
+    EXPECT(fake::total_allocs == allocs && fake::live_allocs == live, "the allocation-free execute allocated");
+    // beyond the array: 2 * 7 * round64(extent) * 4 bytes > 64 MiB
+    const int64_t many = (int64_t(64) << 20) / (2 * 7 * 4 * n) + 2;
+    std::vector<void*> huge = fake_buffers(7, many * n * 4);
+    fake::launches.clear();
+    EXPECT(ar_execute_noalloc(pl, huge.data(), many, n, stream_tag()) == AR_ERR_UNSUPPORTED &&
+               fake::launches.empty(), "allocation-free execute beyond the array");
+    EXPECT(std::strstr(ar_last_error_message(), "at most") != nullptr, "no size in the message");
+  }
   // a failed launch is reported as a HIP error and stops the execute
   fake::launches.clear();
   fake::launch_error = int(hipErrorLaunchFailure);
