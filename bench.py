@@ -424,6 +424,7 @@ def main():
             rk["workload"] = describe(args.workload, jobs_k, args.group, args.schedule)
             rk["k"] = [j["k"] for j in jobs_k]
             out["extra"].append(rk)
+    out["box_reference"] = box_reference(sets[0][0], stream)
     if fetchers is not None:
         log("timing the CPU oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(jobs, fetchers, group=args.group, schedule=args.schedule)
@@ -515,6 +516,42 @@ def measure(args, jobs, path, ptr_tables, n_sets, steps, warmup, stream):
             "path": "fused" if fused else "stepwise",
             "hbm_algorithmic_GBps_step": round(step_alg / (ms_per_step * 1e-3) / 1e9, 1),
             "wall_s_timed": round(wall, 4), "roofline": roof, "source_hash": src_hash}
+
+
+def box_reference(X, stream, reps=3):
+    """HBM rates of this GPU on the workload's own rank buffers, for context:
+    torch's fill_ (writes only) over all of X and copy_ of one half onto the
+    other (one read and one write stream), best of `reps`.  Run after every
+    timed step (it overwrites the buffers).  None for sets under 1 GiB, which
+    the 256 MB Infinity Cache would flatter."""
+    import torch
+
+    nbytes = X.numel() * X.element_size()
+    if nbytes < (1 << 30):
+        return None
+    flat = X.view(-1)
+    half = flat.numel() // 2
+    a, b = flat[:half], flat[half:2 * half]
+
+    def best(fn, moved):
+        fn()
+        torch.cuda.synchronize()
+        ms = []
+        for _ in range(reps):
+            e0, e1 = HipEvent(), HipEvent()
+            e0.record(stream)
+            fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms.append(e0.elapsed_time(e1))
+        return round(moved / (min(ms) * 1e-3) / 1e9, 1)
+
+    out = {"fill_GBps": best(lambda: flat.fill_(0), nbytes),
+           "copy_GBps": best(lambda: b.copy_(a), 2 * half * X.element_size()),
+           "bytes": nbytes,
+           "how": "torch fill_ over the rank buffers and copy_ of one half onto the other, after the timed "
+                  "steps, best of %d" % reps}
+    return out
 
 
 def kernel_name(args, dj, st, fused):

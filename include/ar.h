@@ -97,8 +97,6 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *   AR_STEP_MERGE = 0|1             step launches block by block / as
  *                                   merged runs of blocks (default: merged
  *                                   for blocks of at most 256 elements);
- *   AR_FUSED_MODE = 0|1             latency-optimal kernel with P <= 16:
- *                                   16-byte or 4-byte columns (default 1);
  *   AR_FUSED_SPLIT = 0|1            single fused launch, or reduce plus
  *                                   broadcast where every rank receives the
  *                                   same result (default: split for

@@ -11,6 +11,7 @@ from __future__ import annotations
 
 import ctypes
 import os
+import weakref
 from typing import Sequence
 
 import torch  # noqa: F401  (loads the HIP runtime torch was built with, before libar.so)
@@ -238,6 +239,8 @@ def ar_plan_set_path(plan: int, path: int):
 
 
 _TORCH_DTYPE = {AR_INT32: torch.int32, AR_FLOAT32: torch.float32}
+# per plan: the last call whose buffers passed the checks (see _ptr_table)
+_CHECKED: dict = {}
 
 
 def _ptr_table(plan: int, rank_buffers, batch: int = 1, instance_stride: int | None = None,
@@ -256,6 +259,15 @@ def _ptr_table(plan: int, rank_buffers, batch: int = 1, instance_stride: int | N
         st = ar_plan_stats(plan)
         info = _PLAN_INFO[plan] = (st.P, st.n, None)
     P, n, dt = info
+    # the same (live) tensor objects at the same addresses as this plan's last
+    # checked call -- what a loop of executes passes: only the addresses are
+    # re-read (weak references, so the plan keeps no buffer alive)
+    addrs = [b.data_ptr() if isinstance(b, torch.Tensor) else int(b) for b in bufs]
+    key = (tuple(addrs), batch, instance_stride, _on_gpu)
+    last = _CHECKED.get(plan)
+    if last is not None and last[0] == key and len(last[1]) == len(bufs) and \
+            all(r is None or r() is b for r, b in zip(last[1], bufs)):
+        return (ctypes.c_void_p * P)(*addrs)
     if len(bufs) != P:
         raise ArError(AR_ERR_INVALID_ARG, "rank buffers", "the plan has P=%d ranks, got %d buffers" % (P, len(bufs)))
     if batch < 1:
@@ -265,10 +277,8 @@ def _ptr_table(plan: int, rank_buffers, batch: int = 1, instance_stride: int | N
     want = _TORCH_DTYPE.get(dt)
     dev = None
     storage_elems = {}
-    addrs = []
     for x, b in enumerate(bufs):
         if not isinstance(b, torch.Tensor):
-            addrs.append(int(b))
             continue
         if extent > 0:
             if _on_gpu and not b.is_cuda:
@@ -292,7 +302,7 @@ def _ptr_table(plan: int, rank_buffers, batch: int = 1, instance_stride: int | N
                 raise ArError(AR_ERR_INVALID_ARG, "rank buffers",
                               "rank %d's tensor holds %d elements from its start, the call needs %d "
                               "((batch - 1) * instance_stride + n)" % (x, have - b.storage_offset(), extent))
-        addrs.append(b.data_ptr())
+    _CHECKED[plan] = (key, [weakref.ref(b) if isinstance(b, torch.Tensor) else None for b in bufs])
     return (ctypes.c_void_p * P)(*addrs)
 
 
@@ -383,6 +393,7 @@ def ar_plan_model_time(plan: int, alpha: float, beta: float, gamma: float) -> fl
 
 def ar_plan_destroy(plan: int):
     _PLAN_INFO.pop(plan, None)
+    _CHECKED.pop(plan, None)
     lib.ar_plan_destroy(plan)
 
 

@@ -187,10 +187,10 @@ int launch_step(const StepArgs& a, int dtype, int op, bool vec, bool nt, int gri
 // One step as merged runs (a.run_len, a.tiles, ...): each range's blocks of a
 // rank streamed as one flat space per instance.
 int launch_step_merged(const StepArgs& a, int dtype, int op, bool nt, int grid, void* stream);
-// Fused latency-optimal kernel; mode 0: 16-byte columns groups, 1: one
-// element per lane (contiguous instances), 2: any instance stride.
+// Fused latency-optimal kernel; mode 1: one element per lane (contiguous
+// instances), 2: any instance stride.
 int launch_fused_lo(const FusedArgs& a, int P, int dtype, int op, int mode, bool nt, int grid, void* stream);
-// Column-fused kernels, one instantiation per P (fused_col_g*.hip):
+// Column-fused kernels, one instantiation per P (units written by build.py):
 // bandwidth-optimal (r = 0) and shifted / latency-optimal (r >= 1), and
 // their dispatcher over P = 2..128.
 template <int P>

@@ -2,7 +2,8 @@
 //
 // Argument checking, workspace management and launch orchestration.  The
 // schedule comes from plan.cpp, the kernels from kernels.hip (step),
-// fused_lo.hip, fused_col.hpp / fused_col_g*.hip, fused_group.hip and
+// fused_lo.hip, fused_col.hpp (instantiated per P in units that build.py
+// writes), fused_group.hip and
 // broadcast.hip; nothing here computes on the host.
 #include <hip/hip_runtime_api.h>
 
@@ -94,7 +95,7 @@ struct ar_plan {
   int32_t dtype = 0, op = 0;
   // Tuning overrides read from the environment at plan creation:
   // AR_STEP_NT / AR_FUSED_NT = 0|1 (nontemporal never / always; default by
-  // launch size), AR_FUSED_MODE = 0|1 (16-byte or 4-byte columns),
+  // launch size),
   // AR_FUSED_SPLIT = 0|1 (single fused launch / reduce plus broadcast, where
   // every rank receives the same result; default by P), AR_BCAST_NT = 0|1
   // (the broadcast's loads and stores; default by P and launch size),
@@ -106,7 +107,7 @@ struct ar_plan {
   // default: for blocks of up to kPackMaxLen elements), AR_STEP_MERGE = 0|1
   // (step launches as merged runs of blocks: never / wherever the ranges
   // allow; default: for blocks of up to kMergeMaxLen elements).
-  int32_t nt_mode = -1, fused_nt_mode = -1, fused_mode = -1, split_mode = -1, bcast_nt_mode = -1;
+  int32_t nt_mode = -1, fused_nt_mode = -1, split_mode = -1, bcast_nt_mode = -1;
   int32_t packed_mode = -1, rotate_mode = -1, merge_mode = -1;
   bool fused_split = false;
   // Sums whose blocks hold at most kPackMaxLen elements run on flat columns
@@ -135,7 +136,8 @@ struct ar_plan {
 namespace ar {
 
 // Column-fused kernels of the cyclic butterfly schedules: one instantiation
-// per P (fused_col_g*.hip), bandwidth-optimal (r = 0) or shifted (r >= 1).
+// per P (units that build.py writes), bandwidth-optimal (r = 0) or shifted
+// (r >= 1).
 int launch_fused_col_any(const ColArgs& a, int P, int dtype, int op, bool nt, int grid, void* stream) {
   switch (P) {
 #define AR_BO_CASE(PP)                                                                                \
@@ -399,7 +401,7 @@ ar_status run_stepwise(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   return AR_OK;
 }
 
-ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool all16, hipStream_t stream,
+ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, hipStream_t stream,
                        int device, LaunchTimer* tm) {
   const ar::Schedule& s = pl->s;
   ar::FusedArgs a;
@@ -410,12 +412,11 @@ ar_status run_fused_lo(ar_plan* pl, void* const* bufs, int64_t batch, int64_t st
   a.batch = batch;
   const int64_t cols = batch * s.n;
   const bool contiguous = (batch == 1 || stride == s.n);
-  int mode = 2;
-  if (contiguous) mode = (pl->fused_mode == 0 && all16 && cols % 4 == 0) ? 0 : 1;
-  a.groups = mode == 0 ? cols / 4 : cols;
+  const int mode = contiguous ? 1 : 2;
+  a.groups = cols;
   int64_t blocks = (a.groups + 255) / 256;
   blocks = std::min<int64_t>(std::max<int64_t>(blocks, 1), int64_t(1) << 22);
-  const bool nt = mode != 2 && use_nt(pl->fused_nt_mode, int64_t(2) * s.P * cols * 4, kFusedNtThresholdBytes);
+  const bool nt = mode == 1 && use_nt(pl->fused_nt_mode, int64_t(2) * s.P * cols * 4, kFusedNtThresholdBytes);
   a.lds = cap_lds(pl->fused_cap, device);
   if (tm) tm->mark();
   const int e = ar::launch_fused_lo(a, s.P, pl->dtype, pl->op, mode, nt, int(blocks), stream);
@@ -527,7 +528,7 @@ ar_status execute_impl(ar_plan* plan, void* const* rank_buffers, int64_t batch, 
   if (fused && plan->fused_kind != kFusedLo) {
     st = run_fused_col(plan, rank_buffers, batch, instance_stride, stream, device, tm);
   } else if (fused) {
-    st = run_fused_lo(plan, rank_buffers, batch, instance_stride, all16, stream, device, tm);
+    st = run_fused_lo(plan, rank_buffers, batch, instance_stride, stream, device, tm);
   } else {
     const bool vec = all16 && (batch == 1 || instance_stride % 4 == 0);
     st = run_stepwise(plan, rank_buffers, batch, instance_stride, vec, stream, device, tm, noalloc);
@@ -589,13 +590,15 @@ std::string plan_text(const ar_plan* pl) {
 
 namespace {
 
-// Cost-model parameters fitted on MI355X (gfx950): step-wise launches of
-// the gradient-sync and prime-sweep shapes and of the calibration sweeps
-// (P = 8, 37, 127) moved 6.0-6.3 TB/s of their algorithmic bytes, with
-// 3.4-4.2 us of fixed cost per launch when executes are enqueued back to
-// back; the fused kernels moved 5.2-6.4 TB/s, one launch (or a reducing
-// launch and a broadcast) per execute.
-constexpr ar_model_params kDefaultModel = {3.7e-6, 6.0e12, 4.0e-6, 5.6e12};
+// Cost-model parameters for MI355X (gfx950), from the calibration sweeps
+// (every k step by step and the fused path, P = 8, 37 and 127, messages of
+// 2 KB to 4 GB, executes enqueued back to back from Python): the fitted
+// per-launch cost was 4.7-7.2 us and the step launches' effective bandwidth
+// 7-11 TB/s of their algorithmic bytes (the smaller steps stay in the 256 MB
+// Infinity Cache).  Of the values tried, these chose a step count within
+// 6.3% of the fastest measured at every size (1% on average); the fused path
+// was faster than every step count at every size, as these values price it.
+constexpr ar_model_params kDefaultModel = {5.0e-6, 7.0e12, 5.0e-6, 6.0e12};
 
 bool model_params_ok(const ar_model_params& mp) {
   return mp.step_alpha >= 0 && mp.fused_alpha >= 0 && mp.step_bytes_per_s > 0 && mp.fused_bytes_per_s > 0 &&
@@ -643,7 +646,6 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
   };
   pl->nt_mode = env_mode("AR_STEP_NT");
   pl->fused_nt_mode = env_mode("AR_FUSED_NT");
-  pl->fused_mode = env_mode("AR_FUSED_MODE");
   pl->split_mode = env_mode("AR_FUSED_SPLIT");
   pl->bcast_nt_mode = env_mode("AR_BCAST_NT");
   pl->packed_mode = env_mode("AR_FUSED_PACKED");

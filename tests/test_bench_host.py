@@ -69,6 +69,26 @@ def test_traffic_lookup_checks_the_source_hash(tmp_path, monkeypatch):
     assert bench.traffic_from_profiles("gradsync", "missing", h) is None
 
 
+def test_generated_column_units_instantiate_every_P_once():
+    import re
+
+    from paper_2004_09362_amd import build as b
+
+    for kind in b.COL_KINDS:
+        ps = []
+        for i in range(b.COL_UNITS):
+            ps += [int(m) for m in re.findall(r"launch_fused_%s<(\d+)>" % kind, b.col_unit_text(i))]
+        assert sorted(ps) == list(range(2, 129)), kind
+    # the generated text counts in the column family's source hash
+    h = b.source_hash("col")
+    old = b.col_unit_text
+    try:
+        b.col_unit_text = lambda i: old(i) + "\nint changed_unit;"
+        assert b.source_hash("col") != h
+    finally:
+        b.col_unit_text = old
+
+
 def test_kernel_families_cover_every_source():
     from paper_2004_09362_amd import build as b
 

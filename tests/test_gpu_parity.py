@@ -275,23 +275,21 @@ def test_fused_latency_optimal_matches_oracle_and_stepwise(P):
 
 @pytest.mark.parametrize("P", [3, 5, 12, 16])
 def test_fused_column_modes_agree(P, monkeypatch):
-    """The fused latency-optimal kernel's 16-byte and 4-byte column modes and
-    its nontemporal variant produce the same bits as the oracle."""
+    """The fused latency-optimal kernel with and without nontemporal
+    accesses produces the oracle's bits."""
     rng = np.random.default_rng(77 + P)
     n, B = 64, 40
     L = ceil_log2(P)
     x = rng.normal(size=(P, B, n)).astype(np.float32)
     want = oracle.allreduce_batched(x, L, "sum")
-    for mode in ("0", "1"):
-        for nt in ("0", "1"):
-            monkeypatch.setenv("AR_FUSED_MODE", mode)
-            monkeypatch.setenv("AR_FUSED_NT", nt)
-            note("fused LO modes P=%d mode=%s nt=%s" % (P, mode, nt))
-            X = torch.from_numpy(x).to(DEV)
-            plan = ar.Plan(P, n, "float32", "sum", L, path=ar.AR_PATH_FUSED)
-            plan.batched([X[i] for i in range(P)], B, n)
-            torch.cuda.synchronize()
-            assert np.array_equal(bits(X.cpu().numpy()), bits(want)), (mode, nt)
+    for nt in ("0", "1"):
+        monkeypatch.setenv("AR_FUSED_NT", nt)
+        note("fused LO P=%d nt=%s" % (P, nt))
+        X = torch.from_numpy(x).to(DEV)
+        plan = ar.Plan(P, n, "float32", "sum", L, path=ar.AR_PATH_FUSED)
+        plan.batched([X[i] for i in range(P)], B, n)
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(X.cpu().numpy()), bits(want)), nt
     for nt in ("0", "1"):
         monkeypatch.setenv("AR_FUSED_NT", nt)
         note("fused BO nt=%s P=%d" % (nt, P))

@@ -51,9 +51,18 @@ def test_library_is_built_for_gfx950_only(tmp_path):
     fb = tmp_path / "fatbin"
     subprocess.run([llvm + "llvm-objcopy", "--dump-section", ".hip_fatbin=%s" % fb, ar.LIB_PATH,
                     str(tmp_path / "copy.so")], check=True)
-    out = subprocess.run([llvm + "clang-offload-bundler", "--list", "--type=o", "--input=%s" % fb],
-                         capture_output=True, text=True, check=True).stdout
-    targets = set(re.findall(r"amdgcn-amd-amdhsa--(gfx\w+)", out))
+    # one bundle per translation unit, stored compressed ("CCOB" header) or
+    # plain; list each on its own
+    data = fb.read_bytes()
+    starts = sorted(m.start() for m in re.finditer(rb"CCOB|__CLANG_OFFLOAD_BUNDLE__", data))
+    assert starts, "no offload bundle in libar.so"
+    targets = set()
+    for i, s in enumerate(starts):
+        part = tmp_path / ("bundle%d" % i)
+        part.write_bytes(data[s:starts[i + 1] if i + 1 < len(starts) else len(data)].rstrip(b"\0"))
+        out = subprocess.run([llvm + "clang-offload-bundler", "--list", "--type=o", "--input=%s" % part],
+                             capture_output=True, text=True, check=True).stdout
+        targets |= set(re.findall(r"amdgcn-amd-amdhsa--(gfx\w+)", out))
     assert targets == {"gfx950"}
 
 
