@@ -268,7 +268,10 @@ ar_status ar_execute_batched(ar_plan* plan, void* const* rank_buffers, int64_t b
  * overlap on one GPU (other streams, other threads) race and must be
  * ordered by the caller.  Nothing in the array needs clearing: each call
  * writes every scratch element before reading it.  No hipMalloc, hipFree,
- * memset or host synchronisation; otherwise as ar_execute_batched. */
+ * memset or host synchronisation; otherwise as ar_execute_batched.  The
+ * first call on a device that needs the array looks up its address there
+ * (hipGetSymbolAddress, which may load the library's device code): make that
+ * call outside a graph capture. */
 ar_status ar_execute_noalloc(ar_plan* plan, void* const* rank_buffers, int64_t batch, int64_t instance_stride,
                              hipStream_t stream);
 

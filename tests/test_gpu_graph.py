@@ -62,3 +62,72 @@ def test_captured_execute_replays_exactly(P, n, B, k, group, schedule, path):
         torch.cuda.synchronize()
     del g
     plan.close()
+
+
+def test_graph_stays_valid_when_the_scratch_grows():
+    """A graph captured at batch 1 keeps working after an eager call with a
+    larger batch made the plan allocate a larger scratch: the old buffer is
+    kept until the plan is destroyed."""
+    P, n, k = 7, 1001, 5
+    rng = np.random.default_rng(4242)
+    plan = ar.Plan(P, n, "float32", "sum", k, path=ar.AR_PATH_STEPWISE)
+    assert plan.stats().workspace_bytes > 0
+    X1 = torch.empty((P, n), dtype=torch.float32, device=DEV)
+    b1 = [X1[i] for i in range(P)]
+    X1.copy_(torch.from_numpy(rng.normal(size=(P, n)).astype(np.float32)))
+    plan(b1)  # eager: scratch for batch 1
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            plan(b1)
+    torch.cuda.synchronize()
+    # eager call at batch 9: the plan's scratch grows
+    B = 9
+    x9 = rng.normal(size=(P, B, n)).astype(np.float32)
+    X9 = torch.from_numpy(x9.reshape(P, B * n)).to(DEV)
+    plan.batched([X9[i] for i in range(P)], B, n)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(X9.cpu().numpy().reshape(P, B, n)), bits(oracle.allreduce_batched(x9, k, "sum")))
+    for rep in range(3):
+        x = rng.normal(size=(P, n)).astype(np.float32)
+        X1.copy_(torch.from_numpy(x))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(X1.cpu().numpy()), bits(oracle.allreduce(x, k, "sum"))), rep
+    del g
+    plan.close()
+
+
+def test_growth_under_capture_is_refused():
+    """A captured call that would have to allocate more scratch is refused
+    (nothing enqueued) instead of allocating inside the capture."""
+    P, n, k = 7, 1001, 5
+    plan = ar.Plan(P, n, "float32", "sum", k, path=ar.AR_PATH_STEPWISE)
+    X1 = torch.ones((P, n), dtype=torch.float32, device=DEV)
+    plan([X1[i] for i in range(P)])  # eager: scratch for batch 1
+    torch.cuda.synchronize()
+    B = 4
+    X4 = torch.ones((P, B * n), dtype=torch.float32, device=DEV)
+    Y = torch.ones(1024, device=DEV)
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    status = None
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            try:
+                plan.batched([X4[i] for i in range(P)], B, n)
+            except ar.ArError as e:
+                status = e.status
+            Y.mul_(2.0)  # the capture holds this only
+    torch.cuda.synchronize()
+    assert status == ar.AR_ERR_UNSUPPORTED
+    g.replay()
+    torch.cuda.synchronize()
+    assert bool((X4 == 1).all()) and bool((Y == 2).all())  # captured work runs only on replay
+    del g
+    plan.close()

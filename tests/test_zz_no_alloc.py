@@ -106,3 +106,35 @@ def test_beyond_the_array_is_refused():
     torch.cuda.synchronize()
     assert bool((X == 1).all())  # nothing ran
     plan.close()
+
+
+def test_noalloc_under_graph_capture():
+    """The use it exists for: a step-wise plan with scratch captured into a
+    graph with no allocation before or during the capture (one eager call
+    looks up the device array first), replayed on fresh inputs."""
+    P, n, k = 37, 2000, 8
+    rng = np.random.default_rng(5150)
+    plan = ar.Plan(P, n, "float32", "sum", k, path=ar.AR_PATH_STEPWISE)
+    X = torch.empty((P, n), dtype=torch.float32, device=DEV)
+    bufs = [X[i] for i in range(P)]
+    x = rng.normal(size=(P, n)).astype(np.float32)
+    X.copy_(torch.from_numpy(x))
+    plan.noalloc(bufs, 1, n)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(X.cpu().numpy()), bits(oracle.allreduce(x, k, "sum")))
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        with torch.cuda.graph(g, stream=s):
+            plan.noalloc(bufs, 1, n)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        x = rng.normal(size=(P, n)).astype(np.float32)
+        X.copy_(torch.from_numpy(x))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(X.cpu().numpy()), bits(oracle.allreduce(x, k, "sum"))), rep
+    del g
+    plan.close()
