@@ -206,8 +206,9 @@ enum { AR_KIND_COPY = 0, AR_KIND_REDUCE = 1, AR_KIND_REDUCE2 = 2 };
  * between ranks, and computes the sizes.  No device memory is touched.
  *   P in [1, 128]; n in [0, 2^46]; k_steps in [ceil(log2 P), 2*ceil(log2 P)]
  *   (k_steps = 0 for P = 1), or AR_K_AUTO; dtype/op from the enums above.
- * Errors: AR_ERR_INVALID_ARG (range), AR_ERR_UNSUPPORTED (dtype/op),
- * AR_ERR_INTERNAL (consistency check failed).  *out_plan is set on AR_OK. */
+ * Errors: AR_ERR_INVALID_ARG (range), AR_ERR_UNSUPPORTED (dtype/op, or P
+ * above the compiled maximum of 128), AR_ERR_INTERNAL (consistency check
+ * failed).  *out_plan is set on AR_OK. */
 ar_status ar_plan_create(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_steps, ar_plan** out_plan);
 
 /* As ar_plan_create (which is group AR_GROUP_CYCLIC, schedule
@@ -237,8 +238,9 @@ ar_status ar_plan_set_path(ar_plan* plan, ar_path path);
  * NULL.  The first call on a plan that needs scratch (r > 0,
  * STEPWISE) allocates it on the current device; it is reused afterwards,
  * and a call that needs more (a larger batch or stride, another device)
- * allocates a larger one and keeps the old one until ar_plan_destroy, so
- * that graphs captured before stay valid.  A plan must not run on two
+ * allocates a larger one (at least twice the old on the same device, when
+ * that much is free) and keeps the old one until ar_plan_destroy, so that
+ * graphs captured before stay valid.  A plan must not run on two
  * streams at once (shared scratch).  An execute only enqueues kernels (no
  * memset, no synchronisation, no allocation once the scratch exists), so
  * after one call with the same device, batch and stride it may be captured

@@ -226,8 +226,18 @@ ar_status ensure_scratch(ar_plan* pl, size_t need, int device, hipStream_t strea
     return fail(AR_ERR_UNSUPPORTED, "the plan needs " + std::to_string(need) +
                                         " bytes of scratch, which cannot be allocated while the stream is captured; "
                                         "run one call with this device, batch and stride before capturing");
+  // Growth on the same device at least doubles the buffer, so that the
+  // buffers kept until destroy (below) add up to less than twice the last;
+  // if the doubled size cannot be had, exactly the need.
+  size_t want = need;
+  if (pl->scratch && pl->scratch_device == device) want = std::max(need, pl->scratch_bytes * 2);
   void* p = nullptr;
-  hipError_t e = hipMalloc(&p, need);
+  hipError_t e = hipMalloc(&p, want);
+  if (e != hipSuccess && want > need) {
+    (void)hipGetLastError();
+    want = need;
+    e = hipMalloc(&p, want);
+  }
   if (e != hipSuccess) {
     (void)hipGetLastError();
     return fail(AR_ERR_OUT_OF_MEMORY, "scratch of " + std::to_string(need) + " bytes: " + hipGetErrorString(e));
@@ -236,7 +246,7 @@ ar_status ensure_scratch(ar_plan* pl, size_t need, int device, hipStream_t strea
   // enqueued, and graphs captured earlier, may still use it
   if (pl->scratch) pl->retired.push_back({pl->scratch, pl->scratch_device});
   pl->scratch = p;
-  pl->scratch_bytes = need;
+  pl->scratch_bytes = want;
   pl->scratch_device = device;
   return AR_OK;
 }
@@ -628,6 +638,7 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
   *out_plan = nullptr;
   if (int(dtype) != AR_INT32 && int(dtype) != AR_FLOAT32) return fail(AR_ERR_UNSUPPORTED, "dtype must be int32 or float32");
   if (int(op) != AR_SUM && int(op) != AR_MAX) return fail(AR_ERR_UNSUPPORTED, "op must be sum or max");
+  if (P > ar::kMaxP) return fail(AR_ERR_UNSUPPORTED, "P above the compiled maximum of 128 ranks");
   if (int(group) != AR_GROUP_CYCLIC && int(group) != AR_GROUP_XOR) return fail(AR_ERR_INVALID_ARG, "unknown group");
   if (int(schedule) != AR_SCHEDULE_BUTTERFLY && int(schedule) != AR_SCHEDULE_RING)
     return fail(AR_ERR_INVALID_ARG, "unknown schedule");
@@ -954,7 +965,8 @@ ar_status ar_plan_create_auto(int32_t P, int64_t n, ar_dtype dtype, ar_op op, ar
     return fail(AR_ERR_INVALID_ARG, "unknown path");
   const ar_model_params& mp = params ? *params : kDefaultModel;
   if (!model_params_ok(mp)) return fail(AR_ERR_INVALID_ARG, "model alphas must be >= 0 and bandwidths > 0");
-  if (P < 1 || P > ar::kMaxP) return fail(AR_ERR_INVALID_ARG, "P must be in [1, 128]");
+  if (P > ar::kMaxP) return fail(AR_ERR_UNSUPPORTED, "P above the compiled maximum of 128 ranks");
+  if (P < 1) return fail(AR_ERR_INVALID_ARG, "P must be in [1, 128]");
   int32_t L = 0;
   while ((1 << L) < P) ++L;
   // Sec. 8: the number of steps that the model prices cheapest on the

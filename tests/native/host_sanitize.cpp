@@ -458,7 +458,7 @@ static void errors() {
   ar_plan* pl = nullptr;
   EXPECT(ar_plan_create(4, 100, AR_FLOAT32, AR_SUM, 2, nullptr) == AR_ERR_INVALID_ARG, "null out_plan");
   EXPECT(ar_plan_create(0, 100, AR_FLOAT32, AR_SUM, 0, &pl) == AR_ERR_INVALID_ARG && !pl, "P = 0");
-  EXPECT(ar_plan_create(129, 100, AR_FLOAT32, AR_SUM, 8, &pl) == AR_ERR_INVALID_ARG, "P = 129");
+  EXPECT(ar_plan_create(129, 100, AR_FLOAT32, AR_SUM, 8, &pl) == AR_ERR_UNSUPPORTED, "P = 129");
   EXPECT(ar_plan_create(5, -1, AR_FLOAT32, AR_SUM, 4, &pl) == AR_ERR_INVALID_ARG, "n = -1");
   EXPECT(ar_plan_create(5, (int64_t(1) << 46) + 1, AR_FLOAT32, AR_SUM, 4, &pl) == AR_ERR_INVALID_ARG, "n > 2^46");
   EXPECT(ar_plan_create(5, INT64_MAX, AR_FLOAT32, AR_SUM, 4, &pl) == AR_ERR_INVALID_ARG, "n = INT64_MAX");
@@ -595,6 +595,21 @@ static void execute_errors() {
     EXPECT(ar_execute_noalloc(pl, huge.data(), many, n, stream_tag()) == AR_ERR_UNSUPPORTED &&
                fake::launches.empty(), "allocation-free execute beyond the array");
     EXPECT(std::strstr(ar_last_error_message(), "at most") != nullptr, "no size in the message");
+  }
+  // growth one batch at a time: the scratch at least doubles, so batches 1..16
+  // allocate five buffers (1, 2, 4, 8 and 16 instances' worth), all kept until destroy
+  {
+    ar_plan* g = nullptr;
+    EXPECT(ar_plan_create(7, n, AR_FLOAT32, AR_SUM, 5, &g) == AR_OK, "create for growth");
+    ar_plan_set_path(g, AR_PATH_STEPWISE);
+    std::vector<void*> b16 = fake_buffers(7, 16 * n * 4, uintptr_t(1) << 43);
+    const int64_t a0 = fake::total_allocs, l0 = fake::live_allocs;
+    for (int64_t batch = 1; batch <= 16; ++batch)
+      EXPECT(ar_execute_batched(g, b16.data(), batch, n, stream_tag()) == AR_OK, "growth batch %lld", (long long)batch);
+    EXPECT(fake::total_allocs - a0 == 5 && fake::live_allocs - l0 == 5, "growth allocated %lld buffers",
+           (long long)(fake::total_allocs - a0));
+    ar_plan_destroy(g);
+    EXPECT(fake::live_allocs == l0, "growth buffers not freed by destroy");
   }
   // a failed launch is reported as a HIP error and stops the execute
   fake::launches.clear();

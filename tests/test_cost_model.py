@@ -215,7 +215,8 @@ def test_auto_k_rejections():
     refused(lambda: ar.ar_plan_create_auto(37, 100, "float32", "sum", params={"fused_alpha": -1.0}),
             ar.AR_ERR_INVALID_ARG)
     refused(lambda: ar.ar_plan_create_auto(12, 100, "float32", "sum", "xor"), ar.AR_ERR_INVALID_ARG)
-    refused(lambda: ar.ar_plan_create_auto(129, 100, "float32", "sum"), ar.AR_ERR_INVALID_ARG)
+    refused(lambda: ar.ar_plan_create_auto(129, 100, "float32", "sum"), ar.AR_ERR_UNSUPPORTED)
+    refused(lambda: ar.ar_plan_create_auto(0, 100, "float32", "sum"), ar.AR_ERR_INVALID_ARG)
     refused(lambda: ar.ar_plan_create_auto(1, 100, "float32", "sum", path=ar.AR_PATH_FUSED), ar.AR_ERR_UNSUPPORTED)
     refused(lambda: ar.ar_plan_create_ex(7, 100, "float32", "sum", ar.AR_K_AUTO, "cyclic", "ring"),
             ar.AR_ERR_INVALID_ARG)

@@ -106,13 +106,19 @@ def test_tables_int32_and_max(P, k, group, schedule):
     (7, 10, 1, 0, 6, ar.AR_GROUP_CYCLIC, ar.AR_SCHEDULE_RING),       # Ring needs k = 2(P-1)
     (7, 10, 1, 0, 6, 2, ar.AR_SCHEDULE_BUTTERFLY),                   # unknown group
     (7, 10, 1, 0, 6, ar.AR_GROUP_CYCLIC, 5),                         # unknown schedule
-    (129, 10, 1, 0, 256, ar.AR_GROUP_CYCLIC, ar.AR_SCHEDULE_RING),   # P too large
 ])
 def test_create_ex_rejects(args):
     h = ctypes.c_void_p()
     assert ar.lib.ar_plan_create_ex(*args, ctypes.byref(h)) == ar.AR_ERR_INVALID_ARG
     assert h.value is None
     assert ar.ar_last_error() != ""
+
+
+def test_create_ex_rejects_P_above_the_compiled_maximum():
+    h = ctypes.c_void_p()
+    args = (129, 10, 1, 0, 256, ar.AR_GROUP_CYCLIC, ar.AR_SCHEDULE_RING)
+    assert ar.lib.ar_plan_create_ex(*args, ctypes.byref(h)) == ar.AR_ERR_UNSUPPORTED
+    assert h.value is None and "128" in ar.ar_last_error()
 
 
 def test_create_ex_defaults_equal_create():

@@ -74,7 +74,7 @@ def test_status_strings():
 
 @pytest.mark.parametrize("args,status", [
     ((0, 10, "float32", "sum", 0), ar.AR_ERR_INVALID_ARG),
-    ((129, 10, "float32", "sum", 14), ar.AR_ERR_INVALID_ARG),
+    ((129, 10, "float32", "sum", 14), ar.AR_ERR_UNSUPPORTED),     # above the compiled maximum
     ((7, -1, "float32", "sum", 3), ar.AR_ERR_INVALID_ARG),
     ((7, 10, "float32", "sum", 2), ar.AR_ERR_INVALID_ARG),
     ((7, 10, "float32", "sum", 7), ar.AR_ERR_INVALID_ARG),
