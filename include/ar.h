@@ -21,7 +21,8 @@
  *
  * Conventions shared by all entry points:
  *   - Every function returns an ar_status; AR_OK is 0.  On failure nothing
- *     has been enqueued and ar_last_error() (per thread) describes it.
+ *     has been enqueued and ar_last_error_message() (per thread) describes
+ *     it.
  *   - Device pointers are plain HIP device addresses on the current device.
  *     Host arrays (the table of rank pointers) are read during the call only.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream)

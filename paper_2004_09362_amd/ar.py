@@ -148,7 +148,7 @@ def ar_status_string(s: int) -> str:
 
 def _check(st: int, where: str):
     if st != AR_OK:
-        raise ArError(st, where, ar_last_error())
+        raise ArError(st, where, ar_last_error_message())
 
 
 def _dtype_code(dtype) -> int:
