@@ -336,7 +336,7 @@ def copy_probe(nbytes, reps):
                       "GBps": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)}), flush=True)
 
 
-def main():
+def make_parser():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
@@ -353,7 +353,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="BYTES",
                     help="instead: time a plain device-to-device copy of BYTES (counter calibration)")
-    args = ap.parse_args()
+    return ap
+
+
+def main():
+    args = make_parser().parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the P ranks are virtual ranks held on a single MI355X, and "

@@ -128,6 +128,17 @@ def test_cpu_baseline_runs_the_oracle_on_a_sample():
     assert cb["value"] > 0 and "instances" in cb["sample"]
 
 
+def test_default_line_is_the_largest_single_gpu_config():
+    """With no arguments the line is the large workload (P = 127, n = 2^26),
+    k = 14 on the line and k = 10 under extra."""
+    args = bench.make_parser().parse_args([])
+    assert args.workload == "large" and args.k is None and args.gpus == 1
+    _, jobs = bench.jobs_for("large", None)
+    assert [(j["P"], j["n"], j["k"]) for j in jobs] == [(127, 1 << 26, 14)]
+    assert bench.EXTRA_K["large"] == [10]
+    assert bench.describe("large", jobs, "cyclic", "butterfly").startswith("large: P=127, n=67108864")
+
+
 def test_host_facts():
     f = bench.host_facts()
     assert f["nproc"] >= 1 and f["cpu_model"]
