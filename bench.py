@@ -575,7 +575,10 @@ def kernel_name(args, dj, st, fused):
     else:
         kname = "fused_mid_kernel<P=%d>" % dj["P"]
     if fused and st.fused_launches == 2:
-        kname += "+broadcast"  # the pair: reducing launch, then the broadcast
+        # the pair: reducing launch, then the broadcast (destination-major on
+        # the bench's contiguous, 16-byte aligned rank rows where the plan allows)
+        stream = st.fused_bcast_stream and dj["n"] % 4 == 0  # rows of the [P, batch * n] tensor 16-byte aligned
+        kname += "+broadcast_stream" if stream else "+broadcast"
     return kname
 
 

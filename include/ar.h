@@ -174,6 +174,14 @@ typedef struct {
                                         separate passes: a combine reads two blocks and
                                         writes one, a copy reads and writes one); equal
                                         to hbm_bytes_stepwise                            */
+  int32_t fused_bcast_stream;        /* FUSED path split into two launches: 1 when the
+                                        broadcast copies destination by destination
+                                        (flat columns, or blocks of at least 1024
+                                        elements) for calls whose instances are
+                                        contiguous (batch 1 or instance_stride = n) in
+                                        16-byte aligned rank buffers, with batch * n
+                                        below 2^32 - 1024; other calls, and 0 here, take
+                                        the tiled broadcast (the same bits)              */
 } ar_stats;
 
 /* One launch of the STEPWISE path: a list of placement ranges.  In a range,

@@ -58,6 +58,7 @@ class Stats(ctypes.Structure):
         ("workspace_bytes", ctypes.c_int64),
         ("group", ctypes.c_int32), ("schedule", ctypes.c_int32), ("fused_launches", ctypes.c_int32),
         ("fused_flat", ctypes.c_int32), ("exec_path", ctypes.c_int32), ("hbm_bytes_algorithmic", ctypes.c_int64),
+        ("fused_bcast_stream", ctypes.c_int32),
     ]
 
     def as_dict(self):

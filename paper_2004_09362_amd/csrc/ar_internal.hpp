@@ -212,6 +212,44 @@ int launch_fused_ring(const ColArgs& a, int dtype, int op, bool nt, int grid, vo
 // Second half of a split fused launch (broadcast.hip): block b's result,
 // stored on rank b by the reducing kernel, copied to the other P - 1 ranks.
 int launch_broadcast(const ColArgs& a, int dtype, bool nt, int grid, void* stream);
+
+// The same copy ordered destination by destination (broadcast.hip), for
+// contiguous instances in 16-byte aligned rank buffers.  A workgroup copies
+// one chunk of kStreamChunk consecutive columns of the batch's flat column
+// space (the byte offset in every rank buffer is 4 * column) to one
+// destination rank, one 16-byte store per thread; ids run slice by slice
+// (C chunks per slice), destination by destination, chunk by chunk.
+constexpr uint32_t kStreamBlock = 256;  // threads per workgroup, four columns each
+constexpr uint32_t kStreamChunk = 4 * kStreamBlock;
+// n / d without a branch: t = umulhi(n, mul), (t + ((n - t) >> s1)) >> s2;
+// for d = 1, mul = s1 = s2 = 0 (stream_div builds it from a FastDiv).
+struct StreamDiv {
+  uint32_t d, mul, s1, s2;
+};
+inline StreamDiv stream_div(uint32_t d) {
+  const FastDiv f = make_fastdiv(d);
+  return f.l == 0 ? StreamDiv{d, 0, 0, 0} : StreamDiv{d, f.m, 1, f.l - 1};
+}
+// Host reference of the device quotient (used by the tests).
+inline uint32_t stream_div_host(uint32_t n, const StreamDiv& d) {
+  const uint32_t t = uint32_t((uint64_t(n) * d.mul) >> 32);
+  return (t + ((n - t) >> d.s1)) >> d.s2;
+}
+// The scalars come first, so that a workgroup reads them in one batch of
+// kernel-argument loads before it looks up its two rank pointers.
+struct StreamArgs {
+  uint32_t P;
+  uint32_t cols;            // batch * n flat columns, < 2^32 - kStreamChunk
+  uint32_t n, q, m;         // instance length, n / P, n % P
+  uint32_t big;             // m * (q + 1): columns of an instance in its first m blocks (q + 1 each)
+  uint32_t flat;            // 1: every column's result is on rank 0; 0: block b's on rank b (q >= kStreamChunk)
+  uint32_t chunks;          // ceil(cols / kStreamChunk)
+  uint32_t id0;             // id of this launch's first workgroup (a multiple of C * P)
+  StreamDiv ndiv, q1div, qdiv;  // n, q + 1, q
+  StreamDiv cdiv, sdiv;     // C (a multiple of the XCD count), C * P
+  void* user[kMaxP];
+};
+int launch_broadcast_stream(const StreamArgs& a, bool nt, uint32_t grid, void* stream);
 // Device address of the allocation-free scratch (noalloc.hip) on `device`,
 // which must be the current device; looked up on the first call per device.
 // Returns a hipError_t value.

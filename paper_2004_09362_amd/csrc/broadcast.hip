@@ -3,26 +3,28 @@
 // For the schedules whose distribution phase hands every rank the same
 // result (bandwidth-optimal plans of Sec. 7 in either group, and the Ring of
 // Sec. 6), the column kernels can store block b's result on rank b alone;
-// this kernel then copies it to ranks b+1, ..., b+P-1.  The copy moves the
+// the broadcast then copies it to ranks b+1, ..., b+P-1.  The copy moves the
 // bytes the distribution phase moves, and one more read and write of each
 // block than the single fused launch.  It pays at large P: a launch that
 // reads P streams and writes P streams at once interleaves reads and writes
 // across hundreds of DRAM rows, while a reducing launch (P reads, one
-// write) and this one (one read, P - 1 writes) each stream in one
-// direction.  On MI355X at P = 127 the pair ran 8% faster than the single
-// launch (probes: reducing 6.4 TB/s, broadcasting 5.3 TB/s, fused 5.35
-// TB/s).
+// write) and the broadcast (one read, P - 1 writes) each stream in one
+// direction.  On MI355X at P = 127 the pair with the tiled broadcast ran 8%
+// faster than the single launch (reducing 6.4 TB/s, broadcasting 5.8 TB/s,
+// single launch 5.35 TB/s), and the destination-major broadcast (second
+// kernel below, 6.3-6.4 TB/s) gains another 3-4% where it applies.
 //
-// Layout and tiles as in the reducing launch (col_tile_column,
-// device_common.hpp): one wave per 64 columns of one block of one instance,
-// tiles laid on 256-byte boundaries of rank b's buffer, or one short block
-// of several instances per wave.  After a reducing launch on flat columns
-// (a.flat: batches of short blocks) every column's result is on rank 0, and
-// the waves take 64 consecutive flat columns each.  Loads and stores are
-// nontemporal (NT) or ordinary: from P = 96 ranks, streaming the P - 1
-// stores nontemporally at one resident workgroup per CU was 3-4% faster,
-// and on flat columns nontemporal stores were 1-11% faster at any P; below
-// P = 96 on block tiles, ordinary stores streamed as fast or faster.
+// broadcast_kernel, the tiled copy: layout and tiles as in the reducing
+// launch (col_tile_column, device_common.hpp): one wave per 64 columns of
+// one block of one instance, tiles laid on 256-byte boundaries of rank b's
+// buffer, or one short block of several instances per wave.  After a
+// reducing launch on flat columns (a.flat: batches of short blocks) every
+// column's result is on rank 0, and the waves take 64 consecutive flat
+// columns each.  Loads and stores are nontemporal (NT) or ordinary: from
+// P = 96 ranks, streaming the P - 1 stores nontemporally at one resident
+// workgroup per CU was 3-4% faster, and on flat columns nontemporal stores
+// were 1-11% faster at any P; below P = 96 on block tiles, ordinary stores
+// streamed as fast or faster.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -61,7 +63,81 @@ __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
   }
 }
 
+// Destination-major copy.  The kernel above writes the P - 1 destinations
+// of a column tile at once, so the stores in flight hit P - 1 rank buffers
+// 2^28 bytes apart and HBM writes them at 5.8 TB/s, where one address-ordered
+// stream of one 16-byte store per thread takes 6.85 TB/s.  Here workgroup
+// ids run slice by slice, destination by destination, chunk by chunk: the
+// workgroups in flight sweep one destination's buffer in address order, and
+// each thread stores 16 bytes once and exits.  A slice's source columns are
+// read from HBM once and then from L2 for the other destinations: workgroup
+// ids go round-robin over the XCDs, so with C chunks per slice a multiple of
+// the XCD count, chunk c of a slice runs on the same XCD for every
+// destination, and C is sized so that each XCD's share of a slice (1 MB)
+// stays in its 4 MB L2 while the destination bytes stream past.  At P = 127,
+// n = 2^26 it took 5.30-5.38 ms against 5.62-5.85 ms for the kernel above
+// (on the same boxes); with C not a multiple of the XCD count 6.9 ms, with
+// 2 MB per XCD 7.5 ms, and with its index arithmetic behind branches (each
+// branch deferring an argument load, a round trip per workgroup) 6.6 ms.
+// The chunks of a slice that fall in destination y's own block are skipped
+// (y holds that result already), and a chunk holds at most two blocks (the
+// host asks for blocks of at least kStreamChunk elements), or one root
+// (flat columns).
+__device__ __forceinline__ uint32_t sdiv(uint32_t n, const StreamDiv& d) {
+  const uint32_t t = __umulhi(n, d.mul);
+  return (t + ((n - t) >> d.s1)) >> d.s2;
+}
+
+// Root of flat column g: rank 0 on flat columns, else the block of g within
+// its instance.  No branches, so that the argument loads are not deferred
+// into them (each deferred load is a round trip in every workgroup).
+__device__ __forceinline__ uint32_t stream_root(const StreamArgs& a, uint32_t g) {
+  const uint32_t i = g - sdiv(g, a.ndiv) * a.n;
+  const uint32_t lo = sdiv(i, a.q1div), hi = a.m + sdiv(i - a.big, a.qdiv);
+  return a.flat ? 0u : (i < a.big ? lo : hi);
+}
+
+template <bool NT>
+__global__ __launch_bounds__(kStreamBlock) void broadcast_stream_kernel(const StreamArgs a) {
+  const uint32_t id = a.id0 + blockIdx.x;
+  const uint32_t s = sdiv(id, a.sdiv);
+  const uint32_t r = id - s * a.sdiv.d;
+  const uint32_t y = sdiv(r, a.cdiv);
+  const uint32_t chunk = s * a.cdiv.d + (r - y * a.cdiv.d);
+  const uint32_t first = chunk * kStreamChunk;
+  const uint32_t last = min(first + kStreamChunk, a.cols) - 1;
+  const uint32_t b0 = stream_root(a, first), b1 = stream_root(a, last);
+  if (chunk >= a.chunks || (b0 == y && b1 == y)) return;
+  const uint32_t g = first + threadIdx.x * 4u;
+  if (g >= a.cols) return;
+  int32_t* dst = static_cast<int32_t*>(a.user[y]);
+  const int32_t* s0 = static_cast<const int32_t*>(a.user[b0]);
+  if (b0 == b1 && g + 3 < a.cols) {
+    const i32x4 v = *reinterpret_cast<const i32x4*>(s0 + g);
+    if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<i32x4*>(dst + g));
+    else *reinterpret_cast<i32x4*>(dst + g) = v;
+    return;
+  }
+  // a chunk across a block boundary, or the tail of the column space
+  const int32_t* s1 = static_cast<const int32_t*>(a.user[b1]);
+#pragma unroll
+  for (uint32_t i = 0; i < 4; ++i) {
+    const uint32_t gi = g + i;
+    if (gi < a.cols) {
+      const uint32_t b = stream_root(a, gi);
+      if (b != y) st1<NT>(dst + gi, (b == b0 ? s0 : s1)[gi]);
+    }
+  }
+}
+
 }  // namespace
+
+int launch_broadcast_stream(const StreamArgs& a, bool nt, uint32_t grid, void* stream) {
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  if (nt) hipLaunchKernelGGL((broadcast_stream_kernel<true>), dim3(grid), dim3(kStreamBlock), 0, s, a);
+  else hipLaunchKernelGGL((broadcast_stream_kernel<false>), dim3(grid), dim3(kStreamBlock), 0, s, a);
+  return int(hipGetLastError());
+}
 
 int launch_broadcast(const ColArgs& a, int dtype, bool nt, int grid, void* stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);

@@ -279,6 +279,62 @@ uint32_t cap_lds(int32_t cap, int device) {
   return uint32_t(bytes);
 }
 
+// Chunks per slice of the destination-major broadcast on `device`: 256
+// chunks (1 MB) per XCD, times the XCD count, taken as the CU count over the
+// 32 CUs of a gfx950 XCD (8 on a whole MI355X, fewer on a partition).  The
+// CU count is cached per device like the LDS sizes above.
+uint32_t stream_slice_chunks(int device) {
+  static std::atomic<int32_t> cus[64];
+  int32_t c = (device >= 0 && device < 64) ? cus[device].load(std::memory_order_acquire) : 0;
+  if (c == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, device) != hipSuccess || v <= 0) {
+      (void)hipGetLastError();
+      v = 32;
+    }
+    c = v;
+    if (device >= 0 && device < 64) cus[device].store(c, std::memory_order_release);
+  }
+  return 256u * uint32_t(std::max<int32_t>(1, c / 32));
+}
+
+// Arguments of the destination-major broadcast (broadcast.hip) when the
+// call allows it: instances contiguous (batch 1 or stride n), every rank
+// buffer 16-byte aligned, the column space and the grid within 32-bit
+// counts, and on block tiles blocks of at least kStreamChunk elements (a
+// chunk then spans at most two roots).  False: the tiled broadcast runs.
+bool stream_bcast_args(const ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool flat, int device,
+                       ar::StreamArgs* sa) {
+  const ar::Schedule& s = pl->s;
+  if (batch > 1 && stride != s.n) return false;
+  const int64_t cols = batch * s.n;
+  if (cols < 1 || cols > int64_t(UINT32_MAX) - ar::kStreamChunk) return false;
+  if (!flat && s.n / s.P < int64_t(ar::kStreamChunk)) return false;
+  for (int32_t x = 0; x < s.P; ++x)
+    if (reinterpret_cast<uintptr_t>(bufs[x]) % 16 != 0) return false;
+  const uint32_t C = stream_slice_chunks(device);
+  const uint32_t chunks = uint32_t((cols + ar::kStreamChunk - 1) / ar::kStreamChunk);
+  const int64_t grid = (int64_t(chunks) + C - 1) / C * C * s.P;
+  if (grid > int64_t(UINT32_MAX) / ar::kStreamBlock) return false;  // work-items per launch below 2^32
+  std::memset(sa, 0, sizeof *sa);
+  for (int32_t x = 0; x < s.P; ++x) sa->user[x] = bufs[x];
+  sa->P = uint32_t(s.P);
+  sa->cols = uint32_t(cols);
+  sa->n = uint32_t(s.n);
+  sa->q = uint32_t(s.n / s.P);
+  sa->m = uint32_t(s.n % s.P);
+  sa->big = sa->m * (sa->q + 1);
+  sa->flat = flat ? 1 : 0;
+  sa->ndiv = ar::stream_div(uint32_t(s.n));
+  sa->q1div = ar::stream_div(sa->q + 1);
+  sa->qdiv = ar::stream_div(std::max<uint32_t>(sa->q, 1));
+  sa->cdiv = ar::stream_div(C);
+  sa->sdiv = ar::stream_div(C * uint32_t(s.P));
+  sa->chunks = chunks;
+  sa->id0 = 0;
+  return true;
+}
+
 bool use_nt(int32_t mode, int64_t bytes, int64_t threshold = kNtThresholdBytes) {
   return mode == 1 || (mode < 0 && bytes >= threshold);
 }
@@ -499,13 +555,19 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");
   if (tm) tm->mark();
   if (pl->fused_split) {
-    a.lds = cap_lds(pl->bcast_cap, device);
     // nontemporal stores from kBcastStreamMinP ranks up, and on flat columns
     // at any P (P = 37: 11% faster, P = 48-128: 1-3%)
     const bool bnt = pl->bcast_nt_mode == 1 ||
                      (pl->bcast_nt_mode < 0 && (s.P >= kBcastStreamMinP || flat_short) &&
                       int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes);
-    e = ar::launch_broadcast(a, pl->dtype, bnt, grid, stream);
+    ar::StreamArgs sa;
+    if (stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, device, &sa)) {
+      const uint32_t sgrid = (sa.chunks + sa.cdiv.d - 1) / sa.cdiv.d * sa.sdiv.d;
+      e = ar::launch_broadcast_stream(sa, bnt, sgrid, stream);
+    } else {
+      a.lds = cap_lds(pl->bcast_cap, device);
+      e = ar::launch_broadcast(a, pl->dtype, bnt, grid, stream);
+    }
     if (e != 0) return hip_fail(hipError_t(e), "broadcast kernel launch");
     if (tm) tm->mark();
   }
@@ -832,6 +894,8 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
                                      ? AR_PATH_FUSED
                                      : AR_PATH_STEPWISE;
   out->hbm_bytes_algorithmic = out->hbm_bytes_stepwise;
+  out->fused_bcast_stream =
+      s.P > 1 && plan->fused_split && (plan->fused_flat || s.n / s.P >= int64_t(ar::kStreamChunk)) ? 1 : 0;
   return AR_OK;
 }
 

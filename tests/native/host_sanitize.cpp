@@ -145,6 +145,7 @@ hipError_t hipDeviceGetAttribute(int* v, hipDeviceAttribute_t attr, int device) 
   if (device != 0) return hipErrorInvalidDevice;
   if (attr == hipDeviceAttributeMaxSharedMemoryPerMultiprocessor) *v = 160 * 1024;
   else if (attr == hipDeviceAttributeMaxSharedMemoryPerBlock) *v = 64 * 1024;
+  else if (attr == hipDeviceAttributeMultiprocessorCount) *v = 256;
   else return hipErrorInvalidValue;
   return hipSuccess;
 }
@@ -220,6 +221,27 @@ int launch_broadcast(const ColArgs& a, int, bool, int grid, void*) {
   check_col(a, a.P, "bcast");
   if (!a.split) fake::problem("broadcast without a split reduce", a.P);
   return record("broadcast", a.P, grid, a.total_tiles);
+}
+// The destination-major broadcast: every rank pointer 16-byte aligned, the
+// column space and the chunk count consistent, a chunk spanning at most two
+// roots (flat columns, or blocks of at least kStreamChunk elements), slices
+// of a multiple of 8 chunks (the fake device's 256 CUs: 8 XCDs), and a grid
+// of whole slices below 2^32 work-items.
+int launch_broadcast_stream(const StreamArgs& a, bool, uint32_t grid, void*) {
+  const int P = int(a.P);
+  if (P < 2 || P > kMaxP) fake::problem("stream broadcast P", P);
+  for (int x = 0; x < P && x < kMaxP; ++x)
+    if (a.user[x] == nullptr || reinterpret_cast<uintptr_t>(a.user[x]) % 16 != 0)
+      fake::problem("stream broadcast rank pointer null or not 16-byte aligned", P);
+  if (a.cols == 0 || uint64_t(a.cols) + kStreamChunk > UINT32_MAX) fake::problem("stream column count", P);
+  if (a.chunks != (a.cols + kStreamChunk - 1) / kStreamChunk) fake::problem("stream chunk count", P);
+  if (!a.flat && a.q < kStreamChunk) fake::problem("stream blocks shorter than a chunk", P);
+  if (a.n == 0 || a.cols % a.n != 0 || a.ndiv.d != a.n) fake::problem("stream instance length", P);
+  if (a.q != a.n / a.P || a.m != a.n % a.P || a.q1div.d != a.q + 1) fake::problem("stream block sizes", P);
+  if (a.cdiv.d != 2048 || a.sdiv.d != a.cdiv.d * a.P) fake::problem("stream slice size", P);
+  if (a.id0 != 0 || grid != (a.chunks + a.cdiv.d - 1) / a.cdiv.d * a.sdiv.d) fake::problem("stream grid", P);
+  if (uint64_t(grid) * 256 > UINT32_MAX) fake::problem("stream grid beyond 2^32 work-items", P);
+  return record("broadcast_stream", P, int(grid), a.chunks);
 }
 int launch_fused_lo(const FusedArgs& a, int P, int, int, int mode, bool, int grid, void*) {
   if (P < 2 || P > kFusedMaxP) fake::problem("register-resident kernel beyond its P", P);
@@ -454,6 +476,50 @@ static void exercise(int P, int64_t n, int k, int group, int sched, int dtype, i
   EXPECT(fake::live_allocs == 0, "%s: scratch not freed (%lld live)", what, (long long)fake::live_allocs);
 }
 
+// Which broadcast a split plan takes: the destination-major one for
+// contiguous instances in 16-byte aligned buffers with blocks of at least
+// kStreamChunk elements (or flat columns), the tiled one otherwise.
+static void broadcast_choice() {
+  struct Case {
+    int P;
+    int64_t n;
+    int k, group, batch;
+    int64_t stride_extra;
+    uintptr_t misalign;
+    const char* expect;
+  };
+  const Case cases[] = {
+      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream"},
+      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 3, 0, 0, "broadcast_stream"},
+      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 3, 5, 0, "broadcast"},       // gaps between instances
+      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 4, "broadcast"},       // a rank buffer off 16 bytes
+      {127, 1024 * 127 - 1, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast"},         // blocks of 1023 elements
+      {64, 1024 * 64, 12, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream"},
+      {128, 1024 * 128 + 7, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream"},
+      {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream"},             // flat columns, root rank 0
+      {127, 2304, 14, AR_GROUP_CYCLIC, 8, 3, 0, "broadcast"},
+  };
+  for (const Case& c : cases) {
+    ar_plan* pl = nullptr;
+    EXPECT(ar_plan_create_ex(c.P, c.n, AR_FLOAT32, AR_SUM, c.k, ar_group(c.group), AR_SCHEDULE_BUTTERFLY, &pl) ==
+               AR_OK, "broadcast choice: create P=%d n=%lld", c.P, (long long)c.n);
+    if (!pl) continue;
+    ar_stats s;
+    EXPECT(ar_plan_stats(pl, &s) == AR_OK && s.fused_launches == 2, "broadcast choice: P=%d n=%lld not split", c.P,
+           (long long)c.n);
+    const int64_t stride = c.n + c.stride_extra;
+    std::vector<void*> bufs = fake_buffers(c.P, ((c.batch - 1) * stride + c.n) * 4 + 64);
+    bufs[size_t(c.P / 2)] = reinterpret_cast<char*>(bufs[size_t(c.P / 2)]) + c.misalign;
+    fake::launches.clear();
+    EXPECT(ar_execute_batched(pl, bufs.data(), c.batch, stride, stream_tag()) == AR_OK && fake::launches.size() == 2 &&
+               std::strcmp(fake::launches[1].kind, c.expect) == 0,
+           "broadcast choice: P=%d n=%lld batch %d stride +%lld misalign %zu took %s, expected %s", c.P,
+           (long long)c.n, c.batch, (long long)c.stride_extra, size_t(c.misalign),
+           fake::launches.size() == 2 ? fake::launches[1].kind : "?", c.expect);
+    ar_plan_destroy(pl);
+  }
+}
+
 static void errors() {
   ar_plan* pl = nullptr;
   EXPECT(ar_plan_create(4, 100, AR_FLOAT32, AR_SUM, 2, nullptr) == AR_ERR_INVALID_ARG, "null out_plan");
@@ -678,6 +744,7 @@ int main(int argc, char** argv) {
     th.emplace_back([] {
       errors();
       execute_errors();
+      broadcast_choice();
     });
     for (int t = 0; t < nt; ++t) th.emplace_back([t, nt, pmax, &counts] { counts[size_t(t)] = sweep(1 + t, nt, pmax); });
     for (std::thread& x : th) x.join();
@@ -686,6 +753,7 @@ int main(int argc, char** argv) {
     const int pmax = argc > 1 ? std::atoi(argv[1]) : 128;
     errors();
     execute_errors();
+    broadcast_choice();
     plans = sweep(1, 1, pmax);
   }
   std::printf("%d plans, %d launch contract problems, %d failures\n", plans, fake::problems.load(), fails.load());

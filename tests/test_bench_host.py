@@ -99,6 +99,7 @@ def test_kernel_families_cover_every_source():
                                               "fused_mid_kernel<P=37>", "fused_xor_kernel<P=32,R=0>",
                                               "fused_ring_kernel")} == {"step", "lo", "col", "group"}
     assert b.kernel_families("fused_bo_kernel<P=127>+broadcast") == ["col", "bcast"]
+    assert b.kernel_families("fused_bo_kernel<P=127>+broadcast_stream") == ["col", "bcast"]
     assert b.source_hash(["col", "bcast"]) != b.source_hash("col")
 
 

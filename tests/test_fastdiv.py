@@ -1,6 +1,7 @@
-"""The precomputed 32-bit division used by the step kernel's work
-decomposition (host reference of the same arithmetic) against exact
-division, including edge divisors and numerators."""
+"""The precomputed 32-bit divisions used by the kernels' work decomposition
+(host references of the same arithmetic: the step and column kernels' form,
+and the broadcast's branch-free form) against exact division, including
+edge divisors and numerators."""
 import os
 import subprocess
 
@@ -17,8 +18,10 @@ int main() {
   const uint32_t edge_n[] = {0u, 1u, 2u, 3u, 255u, 256u, 65535u, 65536u, 0x7fffffffu, 0x80000000u, 0xfffffffeu, 0xffffffffu};
   auto check = [&](uint32_t n, uint32_t d) {
     ar::FastDiv f = ar::make_fastdiv(d);
+    ar::StreamDiv s = ar::stream_div(d);
     ++checks;
     if (ar::fastdiv_host(n, f) != n / d) { if (bad < 5) printf("n=%u d=%u\n", n, d); ++bad; }
+    if (ar::stream_div_host(n, s) != n / d || s.d != d) { if (bad < 5) printf("stream n=%u d=%u\n", n, d); ++bad; }
   };
   for (uint32_t d = 1; d <= 5000; ++d) {
     for (uint32_t n : edge_n) check(n, d);

@@ -107,6 +107,21 @@ def test_fused_path_for_every_plan_with_two_or_more_ranks():
     assert ei.value.status == ar.AR_ERR_UNSUPPORTED
 
 
+@pytest.mark.parametrize("P,n,k,group,want", [
+    (127, 1 << 26, 14, "cyclic", 1),          # split, blocks of 528 K elements
+    (127, 127 * 1024, 14, "cyclic", 1),       # blocks of exactly 1024
+    (127, 127 * 1024 - 1, 14, "cyclic", 0),   # one block of 1023: the tiled broadcast
+    (127, 2304, 14, "cyclic", 1),             # short blocks on flat columns (results on rank 0)
+    (128, 2304, 14, "xor", 1),
+    (127, 1 << 26, 10, "cyclic", 0),          # shifted: one launch, no broadcast
+    (37, 1 << 22, 12, "cyclic", 0),           # below the split's P
+])
+def test_destination_major_broadcast_choice(P, n, k, group, want):
+    st = ar.Plan(P, n, "float32", "sum", k, group=group).stats()
+    assert st.fused_bcast_stream == want
+    assert st.fused_launches == (2 if want else st.fused_launches)
+
+
 def test_execute_argument_errors_before_any_device_work():
     p = ar.Plan(3, 8, "int32", "sum", 2)
     tbl = (ctypes.c_void_p * 3)(0x10000, 0, 0x30000)
