@@ -106,6 +106,10 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *   AR_BCAST_NT = 0|1               nontemporal loads and stores in that
  *                                   broadcast (default: for large launches
  *                                   with P >= 96, or on flat columns);
+ *   AR_BCAST_STREAM = 0|1           that broadcast tiled by block always /
+ *                                   destination by destination wherever the
+ *                                   call allows it (see fused_bcast_stream;
+ *                                   default: the size rules given there);
  *   AR_FUSED_PACKED = 0|1           column launches other than the latency-
  *                                   optimal ones: a wave takes 64 columns of
  *                                   one block of one instance, or one block
@@ -175,13 +179,16 @@ typedef struct {
                                         writes one, a copy reads and writes one); equal
                                         to hbm_bytes_stepwise                            */
   int32_t fused_bcast_stream;        /* FUSED path split into two launches: 1 when the
-                                        broadcast copies destination by destination
-                                        (flat columns, or blocks of at least 1024
-                                        elements) for calls whose instances are
-                                        contiguous (batch 1 or instance_stride = n) in
-                                        16-byte aligned rank buffers, with batch * n
-                                        below 2^32 - 1024; other calls, and 0 here, take
-                                        the tiled broadcast (the same bits)              */
+                                        broadcast of one instance copies destination by
+                                        destination -- flat columns (short blocks) from
+                                        P = 64, or blocks of at least 1024 elements in
+                                        rank buffers of at least 256 MiB (AR_BCAST_STREAM
+                                        overrides the size rules) -- for calls whose
+                                        instances are contiguous (batch 1 or
+                                        instance_stride = n) in 16-byte aligned rank
+                                        buffers, with batch * n below 2^32 - 1024; other
+                                        calls, and 0 here, take the tiled broadcast (the
+                                        same bits)                                        */
 } ar_stats;
 
 /* One launch of the STEPWISE path: a list of placement ranges.  In a range,

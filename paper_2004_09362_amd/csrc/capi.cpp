@@ -42,6 +42,14 @@ constexpr int32_t kFlatSplitMinP = 33;
 // CU: 3-4% faster at P = 100-128 than cached stores at two workgroups per CU,
 // the same at P = 64, and 13% slower at P = 48.  Neither change helps alone.
 constexpr int32_t kBcastStreamMinP = 96;
+// The destination-major broadcast (broadcast.hip) by default: on flat
+// columns from this many ranks up (P = 64-128: 12-16% faster than the tiled
+// copy from 0.6 to 9.6 GB; P = 37 and 48: 0.5-7% slower), and on block
+// tiles where a rank's span of the call reaches kBcastStreamMinBytes (n =
+// 2^26 fp32: 1-14% faster at P = 64-128; at 64 MB per rank and below it
+// read its source from L2 no more, and ran up to 2x slower).
+constexpr int32_t kBcastStreamFlatMinP = 64;
+constexpr int64_t kBcastStreamMinBytes = int64_t(256) << 20;
 // Blocks of at most this many elements (many small instances) are packed:
 // a column-fused wave takes one block of 64 / max_len instances instead of 64
 // columns of one block of one instance, laid on 256-byte boundaries (which
@@ -107,7 +115,7 @@ struct ar_plan {
   // default: for blocks of up to kPackMaxLen elements), AR_STEP_MERGE = 0|1
   // (step launches as merged runs of blocks: never / wherever the ranges
   // allow; default: for blocks of up to kMergeMaxLen elements).
-  int32_t nt_mode = -1, fused_nt_mode = -1, split_mode = -1, bcast_nt_mode = -1;
+  int32_t nt_mode = -1, fused_nt_mode = -1, split_mode = -1, bcast_nt_mode = -1, bcast_stream_mode = -1;
   int32_t packed_mode = -1, rotate_mode = -1, merge_mode = -1;
   bool fused_split = false;
   // Sums whose blocks hold at most kPackMaxLen elements run on flat columns
@@ -312,8 +320,12 @@ bool stream_bcast_args(const ar_plan* pl, void* const* bufs, int64_t batch, int6
   if (!flat && s.n / s.P < int64_t(ar::kStreamChunk)) return false;
   for (int32_t x = 0; x < s.P; ++x)
     if (reinterpret_cast<uintptr_t>(bufs[x]) % 16 != 0) return false;
-  const uint32_t C = stream_slice_chunks(device);
+  // chunks per slice: 1 MB per XCD, or all chunks (rounded up to the XCD
+  // count) when there are fewer, so that no workgroup is launched for nothing
+  const uint32_t xcd_chunks = stream_slice_chunks(device);
   const uint32_t chunks = uint32_t((cols + ar::kStreamChunk - 1) / ar::kStreamChunk);
+  const uint32_t xcds = xcd_chunks / 256;
+  const uint32_t C = std::min(xcd_chunks, (chunks + xcds - 1) / xcds * xcds);
   const int64_t grid = (int64_t(chunks) + C - 1) / C * C * s.P;
   if (grid > int64_t(UINT32_MAX) / ar::kStreamBlock) return false;  // work-items per launch below 2^32
   std::memset(sa, 0, sizeof *sa);
@@ -561,7 +573,10 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
                      (pl->bcast_nt_mode < 0 && (s.P >= kBcastStreamMinP || flat_short) &&
                       int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes);
     ar::StreamArgs sa;
-    if (stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, device, &sa)) {
+    const bool want_stream =
+        pl->bcast_stream_mode == 1 ||
+        (pl->bcast_stream_mode < 0 && (a.flat ? s.P >= kBcastStreamFlatMinP : batch * s.n * 4 >= kBcastStreamMinBytes));
+    if (want_stream && stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, device, &sa)) {
       const uint32_t sgrid = (sa.chunks + sa.cdiv.d - 1) / sa.cdiv.d * sa.sdiv.d;
       e = ar::launch_broadcast_stream(sa, bnt, sgrid, stream);
     } else {
@@ -721,6 +736,7 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
   pl->fused_nt_mode = env_mode("AR_FUSED_NT");
   pl->split_mode = env_mode("AR_FUSED_SPLIT");
   pl->bcast_nt_mode = env_mode("AR_BCAST_NT");
+  pl->bcast_stream_mode = env_mode("AR_BCAST_STREAM");
   pl->packed_mode = env_mode("AR_FUSED_PACKED");
   pl->rotate_mode = env_mode("AR_FUSED_ROTATE");
   pl->merge_mode = env_mode("AR_STEP_MERGE");
@@ -894,8 +910,18 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
                                      ? AR_PATH_FUSED
                                      : AR_PATH_STEPWISE;
   out->hbm_bytes_algorithmic = out->hbm_bytes_stepwise;
-  out->fused_bcast_stream =
-      s.P > 1 && plan->fused_split && (plan->fused_flat || s.n / s.P >= int64_t(ar::kStreamChunk)) ? 1 : 0;
+  {
+    // the default choice for one instance (ar.h): flat columns from
+    // kBcastStreamFlatMinP ranks, blocks of at least kStreamChunk elements in
+    // rank buffers of at least kBcastStreamMinBytes
+    const bool flat = plan->fused_flat;
+    const bool allowed = flat || s.n / std::max<int32_t>(s.P, 1) >= int64_t(ar::kStreamChunk);
+    const bool by_size = flat ? s.P >= kBcastStreamFlatMinP : s.n * 4 >= kBcastStreamMinBytes;
+    out->fused_bcast_stream =
+        s.P > 1 && plan->fused_split && allowed && (plan->bcast_stream_mode == 1 || (plan->bcast_stream_mode < 0 && by_size))
+            ? 1
+            : 0;
+  }
   return AR_OK;
 }
 

@@ -225,8 +225,8 @@ int launch_broadcast(const ColArgs& a, int, bool, int grid, void*) {
 // The destination-major broadcast: every rank pointer 16-byte aligned, the
 // column space and the chunk count consistent, a chunk spanning at most two
 // roots (flat columns, or blocks of at least kStreamChunk elements), slices
-// of a multiple of 8 chunks (the fake device's 256 CUs: 8 XCDs), and a grid
-// of whole slices below 2^32 work-items.
+// of a multiple of 8 chunks (the fake device's 256 CUs: 8 XCDs), 2048 or
+// all the chunks, and a grid of whole slices below 2^32 work-items.
 int launch_broadcast_stream(const StreamArgs& a, bool, uint32_t grid, void*) {
   const int P = int(a.P);
   if (P < 2 || P > kMaxP) fake::problem("stream broadcast P", P);
@@ -238,7 +238,9 @@ int launch_broadcast_stream(const StreamArgs& a, bool, uint32_t grid, void*) {
   if (!a.flat && a.q < kStreamChunk) fake::problem("stream blocks shorter than a chunk", P);
   if (a.n == 0 || a.cols % a.n != 0 || a.ndiv.d != a.n) fake::problem("stream instance length", P);
   if (a.q != a.n / a.P || a.m != a.n % a.P || a.q1div.d != a.q + 1) fake::problem("stream block sizes", P);
-  if (a.cdiv.d != 2048 || a.sdiv.d != a.cdiv.d * a.P) fake::problem("stream slice size", P);
+  if (a.cdiv.d % 8 != 0 || a.cdiv.d > 2048 || (a.cdiv.d < 2048 && a.cdiv.d >= a.chunks + 8) ||
+      a.sdiv.d != a.cdiv.d * a.P)
+    fake::problem("stream slice size", P);
   if (a.id0 != 0 || grid != (a.chunks + a.cdiv.d - 1) / a.cdiv.d * a.sdiv.d) fake::problem("stream grid", P);
   if (uint64_t(grid) * 256 > UINT32_MAX) fake::problem("stream grid beyond 2^32 work-items", P);
   return record("broadcast_stream", P, int(grid), a.chunks);
@@ -477,8 +479,9 @@ static void exercise(int P, int64_t n, int k, int group, int sched, int dtype, i
 }
 
 // Which broadcast a split plan takes: the destination-major one for
-// contiguous instances in 16-byte aligned buffers with blocks of at least
-// kStreamChunk elements (or flat columns), the tiled one otherwise.
+// contiguous instances in 16-byte aligned buffers, on flat columns from 64
+// ranks or on blocks of at least kStreamChunk elements in rank spans of at
+// least 256 MiB; the tiled one otherwise.
 static void broadcast_choice() {
   struct Case {
     int P;
@@ -489,15 +492,18 @@ static void broadcast_choice() {
     const char* expect;
   };
   const Case cases[] = {
-      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream"},
-      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 3, 0, 0, "broadcast_stream"},
-      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 3, 5, 0, "broadcast"},       // gaps between instances
-      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 4, "broadcast"},       // a rank buffer off 16 bytes
-      {127, 1024 * 127 - 1, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast"},         // blocks of 1023 elements
-      {64, 1024 * 64, 12, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream"},
-      {128, 1024 * 128 + 7, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream"},
-      {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream"},             // flat columns, root rank 0
+      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream"},
+      {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream"},   // 256 MiB per rank over two instances
+      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 3, 5, 0, "broadcast"},          // gaps between instances
+      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 4, "broadcast"},          // a rank buffer off 16 bytes
+      {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast"},          // 128 MiB per rank
+      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast"},
+      {64, int64_t(1) << 26, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream"},
+      {128, int64_t(1) << 26, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream"},
+      {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream"},                // flat columns, root rank 0
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 3, 0, "broadcast"},
+      {128, 2304, 14, AR_GROUP_XOR, 4, 0, 0, "broadcast_stream"},
+      {48, 2304, 12, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast"},                        // flat, below 64 ranks
   };
   for (const Case& c : cases) {
     ar_plan* pl = nullptr;

@@ -2,11 +2,14 @@
 
 Plans whose ranks all receive one result (bandwidth-optimal in either group,
 the Ring) run fused at P >= 64 as a reducing launch plus a broadcast.  The
-broadcast is destination-major when the instances are contiguous and every
-rank buffer is 16-byte aligned, with blocks of at least 1024 elements (or
-flat columns, whose results all sit on rank 0); otherwise the tiled kernel
-copies each block from its root.  Both are checked bit for bit against the
-oracle on whole arrays, on sizes that span several 4 KB chunks per block,
+broadcast can run destination-major when the instances are contiguous and
+every rank buffer is 16-byte aligned, with blocks of at least 1024 elements
+(or flat columns, whose results all sit on rank 0); otherwise the tiled
+kernel copies each block from its root.  By default the library takes the
+destination-major copy only where it measured faster (flat columns from
+P = 64, rank buffers of 256 MiB and more); these tests set AR_BCAST_STREAM=1
+so that it runs at sizes the oracle checks whole, and compare both copies
+bit for bit with the oracle: sizes that span several 4 KB chunks per block,
 chunks across block and instance boundaries, and a ragged tail.
 """
 import sys
@@ -62,8 +65,9 @@ CASES = [
 
 
 @pytest.mark.parametrize("P,n,k,group,schedule,dtype,op", CASES)
-def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op):
+def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op, monkeypatch):
     """16-byte aligned rows: the destination-major broadcast."""
+    monkeypatch.setenv("AR_BCAST_STREAM", "1")
     rng = np.random.default_rng(P * 7 + n)
     x = draw(rng, P, n, dtype)
     plan = ar.Plan(P, n, dtype, op, k, group=group, schedule=schedule)
@@ -81,10 +85,11 @@ def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op):
 
 
 @pytest.mark.parametrize("P,n,k", [(127, 127 * 1024 + 77, 14), (64, 64 * 1030 + 1, 12)])
-def test_split_broadcast_contiguous_batch(P, n, k):
+def test_split_broadcast_contiguous_batch(P, n, k, monkeypatch):
     """Three contiguous instances (stride n) in one buffer per rank: chunks
     that straddle an instance boundary take the last block of one instance
     and the first of the next."""
+    monkeypatch.setenv("AR_BCAST_STREAM", "1")
     B = 3
     rng = np.random.default_rng(P + k)
     x = draw(rng, P, B * n, "float32")
@@ -98,11 +103,12 @@ def test_split_broadcast_contiguous_batch(P, n, k):
     plan.close()
 
 
-def test_tiled_and_stream_broadcasts_agree():
+def test_tiled_and_stream_broadcasts_agree(monkeypatch):
     """The same plan and input through both broadcasts: aligned rows
     (destination-major), one rank buffer 4 bytes off a 16-byte boundary and
     instances with gaps between them (both tiled); every result equals the
     oracle's bits, and the gaps are left untouched."""
+    monkeypatch.setenv("AR_BCAST_STREAM", "1")
     P, n, k = 127, 127 * 1024 + 501, 14
     rng = np.random.default_rng(2004)
     x = draw(rng, P, n, "float32")
@@ -136,6 +142,16 @@ def test_tiled_and_stream_broadcasts_agree():
     got2 = np.stack([h[:, j * stride:j * stride + n] for j in range(B)], axis=1)
     assert np.array_equal(bits(got2), bits(oracle.allreduce_batched(x2, k, "sum")))
     assert np.all(h[:, n:stride] == -7.0)
+    plan.close()
+    # the same aligned rows through the tiled copy
+    monkeypatch.setenv("AR_BCAST_STREAM", "0")
+    plan = ar.Plan(P, n, "float32", "sum", k)
+    assert plan.stats().fused_bcast_stream == 0
+    big, views = aligned_rows(x)
+    note("broadcasts agree: aligned, tiled P=%d n=%d" % (P, n))
+    plan(views)
+    torch.cuda.synchronize()
+    assert np.array_equal(bits(big[:, :n].cpu().numpy()), want)
     plan.close()
 
 

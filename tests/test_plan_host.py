@@ -108,18 +108,28 @@ def test_fused_path_for_every_plan_with_two_or_more_ranks():
 
 
 @pytest.mark.parametrize("P,n,k,group,want", [
-    (127, 1 << 26, 14, "cyclic", 1),          # split, blocks of 528 K elements
-    (127, 127 * 1024, 14, "cyclic", 1),       # blocks of exactly 1024
-    (127, 127 * 1024 - 1, 14, "cyclic", 0),   # one block of 1023: the tiled broadcast
+    (127, 1 << 26, 14, "cyclic", 1),          # split, 256 MiB rank buffers
+    (64, 1 << 26, 12, "cyclic", 1),
+    (128, 1 << 26, 14, "xor", 1),
+    (127, 1 << 25, 14, "cyclic", 0),          # 128 MiB rank buffers: the tiled broadcast
+    (127, 127 * 1024, 14, "cyclic", 0),
     (127, 2304, 14, "cyclic", 1),             # short blocks on flat columns (results on rank 0)
     (128, 2304, 14, "xor", 1),
+    (48, 2304, 12, "cyclic", 0),              # flat, below 64 ranks
     (127, 1 << 26, 10, "cyclic", 0),          # shifted: one launch, no broadcast
     (37, 1 << 22, 12, "cyclic", 0),           # below the split's P
 ])
-def test_destination_major_broadcast_choice(P, n, k, group, want):
+def test_destination_major_broadcast_choice(P, n, k, group, want, monkeypatch):
     st = ar.Plan(P, n, "float32", "sum", k, group=group).stats()
     assert st.fused_bcast_stream == want
     assert st.fused_launches == (2 if want else st.fused_launches)
+    # the override: never, or wherever the call allows it (split plans with
+    # flat columns or blocks of at least 1024 elements)
+    monkeypatch.setenv("AR_BCAST_STREAM", "0")
+    assert ar.Plan(P, n, "float32", "sum", k, group=group).stats().fused_bcast_stream == 0
+    monkeypatch.setenv("AR_BCAST_STREAM", "1")
+    allowed = st.fused_launches == 2 and (st.fused_flat == 1 or n // P >= 1024)
+    assert ar.Plan(P, n, "float32", "sum", k, group=group).stats().fused_bcast_stream == int(allowed)
 
 
 def test_execute_argument_errors_before_any_device_work():
