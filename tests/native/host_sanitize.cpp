@@ -504,6 +504,8 @@ static void broadcast_choice() {
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 3, 0, "broadcast"},
       {128, 2304, 14, AR_GROUP_XOR, 4, 0, 0, "broadcast_stream"},
       {48, 2304, 12, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast"},                        // flat, below 64 ranks
+      {127, 2304, 14, AR_GROUP_CYCLIC, 60000, 0, 0, "broadcast"},                   // grid above 2^32 work-items
+      {127, 2304, 14, AR_GROUP_CYCLIC, 56000, 0, 0, "broadcast_stream"},            // just below it
   };
   for (const Case& c : cases) {
     ar_plan* pl = nullptr;
