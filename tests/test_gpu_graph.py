@@ -28,8 +28,7 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("P,n,B,k,group,schedule,path", CASES)
-def test_captured_execute_replays_exactly(P, n, B, k, group, schedule, path):
+def _capture_and_replay(P, n, B, k, group, schedule, path):
     if not torch.cuda.is_available():
         pytest.fail("GPU tests need a GPU")
     rng = np.random.default_rng(P * 100 + k)
@@ -62,6 +61,25 @@ def test_captured_execute_replays_exactly(P, n, B, k, group, schedule, path):
         torch.cuda.synchronize()
     del g
     plan.close()
+
+
+@pytest.mark.parametrize("P,n,B,k,group,schedule,path", CASES)
+def test_captured_execute_replays_exactly(P, n, B, k, group, schedule, path):
+    _capture_and_replay(P, n, B, k, group, schedule, path)
+
+
+@pytest.mark.parametrize("P,n,B,k,group", [
+    (127, 127 * 1024 + 76, 1, 14, "cyclic"),    # block tiles (destination-major by the override)
+    (127, 2304, 24, 14, "cyclic"),              # flat columns, rank 0 holds the results
+    (128, 2304, 16, 14, "xor"),
+])
+def test_captured_split_with_the_destination_major_broadcast(P, n, B, k, group, monkeypatch):
+    """The reducing launch and the destination-major broadcast captured
+    together: replays on fresh inputs equal the oracle."""
+    monkeypatch.setenv("AR_BCAST_STREAM", "1")
+    st = ar.Plan(P, n, "float32", "sum", k, group=group).stats()
+    assert st.fused_launches == 2 and st.fused_bcast_stream == 1
+    _capture_and_replay(P, n, B, k, group, "butterfly", ar.AR_PATH_FUSED)
 
 
 def test_graph_stays_valid_when_the_scratch_grows():
