@@ -65,8 +65,8 @@ __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
 
 // Destination-major copy.  The kernel above writes the P - 1 destinations
 // of a column tile at once, so the stores in flight hit P - 1 rank buffers
-// 2^28 bytes apart and HBM writes them at 5.8 TB/s, where one address-ordered
-// stream of one 16-byte store per thread takes 6.85 TB/s.  Here workgroup
+// (256 MB apart at P = 127, n = 2^26) and HBM writes them at 5.8 TB/s, where
+// one address-ordered stream of one 16-byte store per thread takes 6.85 TB/s.  Here workgroup
 // ids run slice by slice, destination by destination, chunk by chunk: the
 // workgroups in flight sweep one destination's buffer in address order, and
 // each thread stores 16 bytes once and exits.  A slice's source columns are
@@ -75,7 +75,7 @@ __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
 // the XCD count, chunk c of a slice runs on the same XCD for every
 // destination, and C is sized so that each XCD's share of a slice (1 MB)
 // stays in its 4 MB L2 while the destination bytes stream past.  At P = 127,
-// n = 2^26 it took 5.30-5.38 ms against 5.62-5.85 ms for the kernel above
+// n = 2^26 it took 5.30-5.51 ms against 5.62-5.93 ms for the kernel above
 // (on the same boxes); with C not a multiple of the XCD count 6.9 ms, with
 // 2 MB per XCD 7.5 ms, and with its index arithmetic behind branches (each
 // branch deferring an argument load, a round trip per workgroup) 6.6 ms.
