@@ -457,6 +457,34 @@ def test_large_workload(k):
     check_full_size("large", 127, w["n"], k, "sum", w["seed"], w["dist"])
 
 
+def test_large_workload_ring():
+    """The Ring at the large shape (P = 127, n = 2^26, k = 252): the fused
+    chain's reducing launch and the destination-major broadcast; sampled
+    columns against the oracle's Ring replay, and every rank the same bits."""
+    w = synth.WORKLOADS["large"]
+    P, n, k = 127, w["n"], 2 * 126
+    note("large ring P=%d n=%d k=%d: fill" % (P, n, k))
+    X = synth.device_ranks(w["seed"], P, n, np.float32, w["dist"], DEV)
+    cols = sample_cols(n, P, per_block=16, seed=k)
+    ct = torch.from_numpy(cols).to(DEV)
+    xs = X[:, ct].cpu().numpy()
+    want = oracle.allreduce(xs, k, "sum", n=n, cols=cols, schedule="ring")
+    plan = ar.Plan(P, n, "float32", "sum", k, schedule="ring")
+    st = plan.stats()
+    assert st.fused_launches == 2 and st.fused_bcast_stream == 1
+    note("large ring P=%d n=%d k=%d: execute" % (P, n, k))
+    plan([X[i] for i in range(P)])
+    torch.cuda.synchronize()
+    got = X[:, ct].cpu().numpy()
+    assert np.array_equal(bits(got), bits(want))
+    assert_fp32_bound(got, xs)
+    for i in range(1, P):
+        assert torch.equal(X[0].view(torch.int32), X[i].view(torch.int32))
+    plan.close()
+    del X
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("P,group", [(17, "cyclic"), (24, "cyclic"), (37, "cyclic"), (64, "cyclic"), (127, "cyclic"),
                                      (32, "xor"), (128, "xor")])
 def test_latency_optimal_flat_columns_with_gaps(P, group):
