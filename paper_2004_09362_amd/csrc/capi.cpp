@@ -43,7 +43,7 @@ constexpr int32_t kFlatSplitMinP = 33;
 // the same at P = 64, and 13% slower at P = 48.  Neither change helps alone.
 constexpr int32_t kBcastStreamMinP = 96;
 // The destination-major broadcast (broadcast.hip) by default: on flat
-// columns from this many ranks up (P = 64-128: 12-16% faster than the tiled
+// columns from this many ranks up (P = 64-128: 7-16% faster than the tiled
 // copy from 0.6 to 9.6 GB; P = 37 and 48: 0.5-7% slower), and on block
 // tiles where a rank's span of the call reaches kBcastStreamMinBytes (n =
 // 2^26 fp32: 1-14% faster at P = 64-128; at 64 MB per rank and below it
@@ -107,6 +107,9 @@ struct ar_plan {
   // AR_FUSED_SPLIT = 0|1 (single fused launch / reduce plus broadcast, where
   // every rank receives the same result; default by P), AR_BCAST_NT = 0|1
   // (the broadcast's loads and stores; default by P and launch size),
+  // AR_BCAST_STREAM = 0|1 (the broadcast tiled by block / destination by
+  // destination wherever the call allows it; default by the size rules at
+  // kBcastStreamFlatMinP and kBcastStreamMinBytes),
   // AR_FUSED_PACKED = 0|1 (column tiles of one block of one instance / of
   // several instances, for blocks of up to 64 elements; default: packed for
   // batches whose blocks hold up to kPackMaxLen elements), AR_FUSED_ROTATE =
