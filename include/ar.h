@@ -106,10 +106,16 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *   AR_BCAST_NT = 0|1               nontemporal loads and stores in that
  *                                   broadcast (default: for large launches
  *                                   with P >= 96, or on flat columns);
- *   AR_BCAST_STREAM = 0|1           that broadcast tiled by block always /
+ *   AR_BCAST_STREAM = 0|1|2|3       that broadcast tiled by block always /
  *                                   destination by destination wherever the
  *                                   call allows it (see fused_bcast_stream;
- *                                   default: the size rules given there);
+ *                                   default: the size rules given there),
+ *                                   its chunks ordered by the default rule
+ *                                   (1: one contiguous region per XCD for
+ *                                   P >= 104 below 256 MiB per rank, else
+ *                                   interleaved over the XCDs), always
+ *                                   interleaved (2), or always in regions
+ *                                   (3);
  *   AR_FUSED_PACKED = 0|1           column launches other than the latency-
  *                                   optimal ones: a wave takes 64 columns of
  *                                   one block of one instance, or one block
@@ -182,7 +188,7 @@ typedef struct {
                                         broadcast of one instance copies destination by
                                         destination -- flat columns (short blocks) from
                                         P = 64, or blocks of at least 1024 elements in
-                                        rank buffers of at least 256 MiB (AR_BCAST_STREAM
+                                        rank buffers of at least 64 MiB (AR_BCAST_STREAM
                                         overrides the size rules) -- for calls whose
                                         instances are contiguous (batch 1 or
                                         instance_stride = n) in 16-byte aligned rank

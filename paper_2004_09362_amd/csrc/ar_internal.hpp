@@ -245,6 +245,9 @@ struct StreamArgs {
   uint32_t flat;            // 1: every column's result is on rank 0; 0: block b's on rank b (q >= kStreamChunk)
   uint32_t chunks;          // ceil(cols / kStreamChunk)
   uint32_t id0;             // id of this launch's first workgroup (a multiple of C * P)
+  uint32_t regions;         // 1: XCD x takes the x-th C / X chunks of a slice; 0: every X-th chunk
+  uint32_t xcd_shift;       // log2 of the XCD count X (a power of two; C is a multiple of X)
+  uint32_t per_xcd;         // C / X
   StreamDiv ndiv, q1div, qdiv;  // n, q + 1, q
   StreamDiv cdiv, sdiv;     // C (a multiple of the XCD count), C * P
   void* user[kMaxP];

@@ -79,10 +79,15 @@ __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
 // (on the same boxes); with C not a multiple of the XCD count 6.9 ms, with
 // 2 MB per XCD 7.5 ms, and with its index arithmetic behind branches (each
 // branch deferring an argument load, a round trip per workgroup) 6.6 ms.
-// The chunks of a slice that fall in destination y's own block are skipped
-// (y holds that result already), and a chunk holds at most two blocks (the
-// host asks for blocks of at least kStreamChunk elements), or one root
-// (flat columns).
+// Below 256 MB per rank the interleaved chunks often stopped hitting L2 at
+// P = 110-128 (P = 127, 64 MB per rank: 36% of the source reads went to
+// HBM); with a.regions XCD x instead takes the x-th contiguous C / X chunks
+// of each slice, which keeps its sources in L2 at the price of X write
+// streams 1 MB apart (P = 127: 1.45 against 1.60-1.87 ms at 64 MB per
+// rank, 5.74-5.80 against 5.45-5.51 ms at 256 MB).  The chunks of a slice that fall in
+// destination y's own block are skipped (y holds that result already), and
+// a chunk holds at most two blocks (the host asks for blocks of at least
+// kStreamChunk elements), or one root (flat columns).
 __device__ __forceinline__ uint32_t sdiv(uint32_t n, const StreamDiv& d) {
   const uint32_t t = __umulhi(n, d.mul);
   return (t + ((n - t) >> d.s1)) >> d.s2;
@@ -103,7 +108,9 @@ __global__ __launch_bounds__(kStreamBlock) void broadcast_stream_kernel(const St
   const uint32_t s = sdiv(id, a.sdiv);
   const uint32_t r = id - s * a.sdiv.d;
   const uint32_t y = sdiv(r, a.cdiv);
-  const uint32_t chunk = s * a.cdiv.d + (r - y * a.cdiv.d);
+  uint32_t c = r - y * a.cdiv.d;  // workgroup c of the slice runs on XCD c mod X
+  if (a.regions) c = (c & ((1u << a.xcd_shift) - 1u)) * a.per_xcd + (c >> a.xcd_shift);
+  const uint32_t chunk = s * a.cdiv.d + c;
   const uint32_t first = chunk * kStreamChunk;
   const uint32_t last = min(first + kStreamChunk, a.cols) - 1;
   const uint32_t b0 = stream_root(a, first), b1 = stream_root(a, last);

@@ -45,11 +45,21 @@ constexpr int32_t kBcastStreamMinP = 96;
 // The destination-major broadcast (broadcast.hip) by default: on flat
 // columns from this many ranks up (P = 64-128: 7-16% faster than the tiled
 // copy from 0.6 to 9.6 GB; P = 37 and 48: 0.5-7% slower), and on block
-// tiles where a rank's span of the call reaches kBcastStreamMinBytes (n =
-// 2^26 fp32: 1-14% faster at P = 64-128; at 64 MB per rank and below it
-// read its source from L2 no more, and ran up to 2x slower).
+// tiles where a rank's span of the call reaches kBcastRegionMinBytes.  The
+// XCDs take interleaved chunks from kBcastStreamMinBytes (P = 64-128, 256 MB
+// per rank: 7-18% faster than the tiled copy), and below it up to
+// kBcastRegionMinP - 1 ranks (P = 64-100 at 64 and 128 MB: 4-11% faster).
+// From kBcastRegionMinP ranks below 256 MB the interleaved chunks often read
+// their sources from L2 no more (P = 110-128 at 64 MB: 3-25% slower than
+// the tiled copy, up to 45% at 128 MB with rank buffers 2^27 bytes apart);
+// there each XCD takes a contiguous region of the slice instead, which ran
+// at 5.8-5.9 TB/s in every case measured (tiled: 5.4-6.3, in most cases
+// below).  Below 64 MB per rank the tiled copy was as fast or faster at
+// P = 100-127.
 constexpr int32_t kBcastStreamFlatMinP = 64;
 constexpr int64_t kBcastStreamMinBytes = int64_t(256) << 20;
+constexpr int64_t kBcastRegionMinBytes = int64_t(64) << 20;
+constexpr int32_t kBcastRegionMinP = 104;
 // Blocks of at most this many elements (many small instances) are packed:
 // a column-fused wave takes one block of 64 / max_len instances instead of 64
 // columns of one block of one instance, laid on 256-byte boundaries (which
@@ -107,9 +117,11 @@ struct ar_plan {
   // AR_FUSED_SPLIT = 0|1 (single fused launch / reduce plus broadcast, where
   // every rank receives the same result; default by P), AR_BCAST_NT = 0|1
   // (the broadcast's loads and stores; default by P and launch size),
-  // AR_BCAST_STREAM = 0|1 (the broadcast tiled by block / destination by
-  // destination wherever the call allows it; default by the size rules at
-  // kBcastStreamFlatMinP and kBcastStreamMinBytes),
+  // AR_BCAST_STREAM = 0|1|2|3 (the broadcast tiled by block / destination by
+  // destination wherever the call allows it, with the chunk order by size,
+  // interleaved, or in XCD regions; default by the size rules at
+  // kBcastStreamFlatMinP, kBcastRegionMinBytes, kBcastStreamMinBytes and
+  // kBcastRegionMinP),
   // AR_FUSED_PACKED = 0|1 (column tiles of one block of one instance / of
   // several instances, for blocks of up to 64 elements; default: packed for
   // batches whose blocks hold up to kPackMaxLen elements), AR_FUSED_ROTATE =
@@ -314,8 +326,8 @@ uint32_t stream_slice_chunks(int device) {
 // buffer 16-byte aligned, the column space and the grid within 32-bit
 // counts, and on block tiles blocks of at least kStreamChunk elements (a
 // chunk then spans at most two roots).  False: the tiled broadcast runs.
-bool stream_bcast_args(const ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool flat, int device,
-                       ar::StreamArgs* sa) {
+bool stream_bcast_args(const ar_plan* pl, void* const* bufs, int64_t batch, int64_t stride, bool flat, bool regions,
+                       int device, ar::StreamArgs* sa) {
   const ar::Schedule& s = pl->s;
   if (batch > 1 && stride != s.n) return false;
   const int64_t cols = batch * s.n;
@@ -347,6 +359,11 @@ bool stream_bcast_args(const ar_plan* pl, void* const* bufs, int64_t batch, int6
   sa->sdiv = ar::stream_div(C * uint32_t(s.P));
   sa->chunks = chunks;
   sa->id0 = 0;
+  uint32_t shift = 0;
+  while ((1u << shift) < xcds) ++shift;
+  sa->regions = regions && (1u << shift) == xcds ? 1 : 0;
+  sa->xcd_shift = shift;
+  sa->per_xcd = C / xcds;
   return true;
 }
 
@@ -577,9 +594,12 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
                       int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes);
     ar::StreamArgs sa;
     const bool want_stream =
-        pl->bcast_stream_mode == 1 ||
-        (pl->bcast_stream_mode < 0 && (a.flat ? s.P >= kBcastStreamFlatMinP : batch * s.n * 4 >= kBcastStreamMinBytes));
-    if (want_stream && stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, device, &sa)) {
+        pl->bcast_stream_mode >= 1 ||
+        (pl->bcast_stream_mode < 0 && (a.flat ? s.P >= kBcastStreamFlatMinP : batch * s.n * 4 >= kBcastRegionMinBytes));
+    const bool regions =
+        pl->bcast_stream_mode == 3 || (pl->bcast_stream_mode != 2 && !a.flat && s.P >= kBcastRegionMinP &&
+                                       batch * s.n * 4 < kBcastStreamMinBytes);
+    if (want_stream && stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, regions, device, &sa)) {
       const uint32_t sgrid = (sa.chunks + sa.cdiv.d - 1) / sa.cdiv.d * sa.sdiv.d;
       e = ar::launch_broadcast_stream(sa, bnt, sgrid, stream);
     } else {
@@ -739,7 +759,12 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
   pl->fused_nt_mode = env_mode("AR_FUSED_NT");
   pl->split_mode = env_mode("AR_FUSED_SPLIT");
   pl->bcast_nt_mode = env_mode("AR_BCAST_NT");
-  pl->bcast_stream_mode = env_mode("AR_BCAST_STREAM");
+  {
+    // 0: tiled; 1: destination-major, chunk order by size; 2 / 3: destination-major with
+    // interleaved chunks / XCD regions
+    const char* e = std::getenv("AR_BCAST_STREAM");
+    pl->bcast_stream_mode = e != nullptr && e[0] >= '0' && e[0] <= '3' && e[1] == 0 ? int32_t(e[0] - '0') : -1;
+  }
   pl->packed_mode = env_mode("AR_FUSED_PACKED");
   pl->rotate_mode = env_mode("AR_FUSED_ROTATE");
   pl->merge_mode = env_mode("AR_STEP_MERGE");
@@ -916,12 +941,12 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
   {
     // the default choice for one instance (ar.h): flat columns from
     // kBcastStreamFlatMinP ranks, blocks of at least kStreamChunk elements in
-    // rank buffers of at least kBcastStreamMinBytes
+    // rank buffers of at least kBcastRegionMinBytes
     const bool flat = plan->fused_flat;
     const bool allowed = flat || s.n / std::max<int32_t>(s.P, 1) >= int64_t(ar::kStreamChunk);
-    const bool by_size = flat ? s.P >= kBcastStreamFlatMinP : s.n * 4 >= kBcastStreamMinBytes;
+    const bool by_size = flat ? s.P >= kBcastStreamFlatMinP : s.n * 4 >= kBcastRegionMinBytes;
     out->fused_bcast_stream =
-        s.P > 1 && plan->fused_split && allowed && (plan->bcast_stream_mode == 1 || (plan->bcast_stream_mode < 0 && by_size))
+        s.P > 1 && plan->fused_split && allowed && (plan->bcast_stream_mode >= 1 || (plan->bcast_stream_mode < 0 && by_size))
             ? 1
             : 0;
   }

@@ -55,6 +55,7 @@ thread_local bool device_ok = true;
 thread_local bool malloc_fails = false;
 thread_local bool capturing = false;  // every stream reports an active graph capture
 thread_local int launch_error = 0;  // hipError_t value every launcher returns when set
+thread_local int last_regions = -1;  // XCD-region order of the last destination-major broadcast
 thread_local int64_t live_allocs = 0, total_allocs = 0;
 std::atomic<uintptr_t> next_addr{uintptr_t(1) << 44};
 thread_local hipError_t last = hipSuccess;
@@ -242,6 +243,8 @@ int launch_broadcast_stream(const StreamArgs& a, bool, uint32_t grid, void*) {
       a.sdiv.d != a.cdiv.d * a.P)
     fake::problem("stream slice size", P);
   if (a.id0 != 0 || grid != (a.chunks + a.cdiv.d - 1) / a.cdiv.d * a.sdiv.d) fake::problem("stream grid", P);
+  if (a.regions > 1 || a.xcd_shift != 3 || a.per_xcd * 8 != a.cdiv.d) fake::problem("stream XCD regions", P);
+  fake::last_regions = int(a.regions);
   if (uint64_t(grid) * 256 > UINT32_MAX) fake::problem("stream grid beyond 2^32 work-items", P);
   return record("broadcast_stream", P, int(grid), a.chunks);
 }
@@ -490,22 +493,28 @@ static void broadcast_choice() {
     int64_t stride_extra;
     uintptr_t misalign;
     const char* expect;
+    int regions;  // the destination-major copy's chunk order: 1 XCD regions, 0 interleaved, -1 tiled copy
   };
   const Case cases[] = {
-      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream"},
-      {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream"},   // 256 MiB per rank over two instances
-      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 3, 5, 0, "broadcast"},          // gaps between instances
-      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 4, "broadcast"},          // a rank buffer off 16 bytes
-      {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast"},          // 128 MiB per rank
-      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast"},
-      {64, int64_t(1) << 26, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream"},
-      {128, int64_t(1) << 26, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream"},
-      {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream"},                // flat columns, root rank 0
-      {127, 2304, 14, AR_GROUP_CYCLIC, 8, 3, 0, "broadcast"},
-      {128, 2304, 14, AR_GROUP_XOR, 4, 0, 0, "broadcast_stream"},
-      {48, 2304, 12, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast"},                        // flat, below 64 ranks
-      {127, 2304, 14, AR_GROUP_CYCLIC, 60000, 0, 0, "broadcast"},                   // grid above 2^32 work-items
-      {127, 2304, 14, AR_GROUP_CYCLIC, 56000, 0, 0, "broadcast_stream"},            // just below it
+      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
+      {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream", 0},   // 256 MiB per rank over two instances
+      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 3, 5, 0, "broadcast", -1},          // gaps between instances
+      {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 4, "broadcast", -1},          // a rank buffer off 16 bytes
+      {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 128 MiB per rank: XCD regions
+      {127, int64_t(1) << 24, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 64 MiB
+      {127, (int64_t(1) << 24) - 1024, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast", -1}, // just below 64 MiB
+      {100, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},   // below 104 ranks: interleaved
+      {104, int64_t(1) << 24, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
+      {64, int64_t(1) << 24, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
+      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast", -1},
+      {64, int64_t(1) << 26, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
+      {128, int64_t(1) << 26, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 0},
+      {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream", 0},                // flat columns, root rank 0
+      {127, 2304, 14, AR_GROUP_CYCLIC, 8, 3, 0, "broadcast", -1},
+      {128, 2304, 14, AR_GROUP_XOR, 4, 0, 0, "broadcast_stream", 0},
+      {48, 2304, 12, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast", -1},                        // flat, below 64 ranks
+      {127, 2304, 14, AR_GROUP_CYCLIC, 60000, 0, 0, "broadcast", -1},                   // grid above 2^32 work-items
+      {127, 2304, 14, AR_GROUP_CYCLIC, 56000, 0, 0, "broadcast_stream", 0},            // just below it
   };
   for (const Case& c : cases) {
     ar_plan* pl = nullptr;
@@ -519,11 +528,56 @@ static void broadcast_choice() {
     std::vector<void*> bufs = fake_buffers(c.P, ((c.batch - 1) * stride + c.n) * 4 + 64);
     bufs[size_t(c.P / 2)] = reinterpret_cast<char*>(bufs[size_t(c.P / 2)]) + c.misalign;
     fake::launches.clear();
+    fake::last_regions = -1;
     EXPECT(ar_execute_batched(pl, bufs.data(), c.batch, stride, stream_tag()) == AR_OK && fake::launches.size() == 2 &&
-               std::strcmp(fake::launches[1].kind, c.expect) == 0,
+               std::strcmp(fake::launches[1].kind, c.expect) == 0 && fake::last_regions == c.regions,
            "broadcast choice: P=%d n=%lld batch %d stride +%lld misalign %zu took %s, expected %s", c.P,
            (long long)c.n, c.batch, (long long)c.stride_extra, size_t(c.misalign),
            fake::launches.size() == 2 ? fake::launches[1].kind : "?", c.expect);
+    ar_plan_destroy(pl);
+  }
+}
+
+// AR_BCAST_STREAM = 2 / 3: the destination-major copy with interleaved chunks
+// / XCD regions wherever the call allows it, whatever the size; 1 with the
+// order by size; 0 the tiled copy.  Plans read the variable when they are
+// created: single-threaded only.
+static void broadcast_order_override() {
+  struct Case {
+    int P;
+    int64_t n;
+    int batch;
+    const char* env;
+    const char* expect;
+    int regions;
+  };
+  const Case cases[] = {
+      {127, int64_t(1) << 26, 1, "2", "broadcast_stream", 0}, {127, int64_t(1) << 26, 1, "3", "broadcast_stream", 1},
+      {127, int64_t(1) << 26, 1, "1", "broadcast_stream", 0}, {127, 127 * 1024 + 77, 1, "1", "broadcast_stream", 1},
+      {127, 127 * 1024 + 77, 1, "2", "broadcast_stream", 0},  {127, 127 * 1024 + 77, 1, "3", "broadcast_stream", 1},
+      {127, 127 * 1024 + 77, 1, "0", "broadcast", -1},         {127, 2304, 8, "1", "broadcast_stream", 0},
+      {127, 2304, 8, "3", "broadcast_stream", 1},              {48, 2304, 8, "2", "broadcast_stream", 0},
+      {127, 127 * 1024 + 77, 1, "7", "broadcast", -1},         // not a mode: the size rules
+  };
+  for (const Case& c : cases) {
+    setenv("AR_BCAST_STREAM", c.env, 1);
+    ar_plan* pl = nullptr;
+    EXPECT(ar_plan_create_ex(c.P, c.n, AR_FLOAT32, AR_SUM, c.P == 48 ? 12 : 14, AR_GROUP_CYCLIC,
+                             AR_SCHEDULE_BUTTERFLY, &pl) == AR_OK,
+           "broadcast order: create P=%d n=%lld", c.P, (long long)c.n);
+    unsetenv("AR_BCAST_STREAM");
+    if (!pl) continue;
+    ar_stats st;
+    EXPECT(ar_plan_stats(pl, &st) == AR_OK && st.fused_bcast_stream == (c.regions >= 0 ? 1 : 0),
+           "broadcast order: stats P=%d n=%lld env %s", c.P, (long long)c.n, c.env);
+    std::vector<void*> bufs = fake_buffers(c.P, c.batch * c.n * 4 + 64);
+    fake::launches.clear();
+    fake::last_regions = -1;
+    EXPECT(ar_execute_batched(pl, bufs.data(), c.batch, c.n, stream_tag()) == AR_OK && fake::launches.size() == 2 &&
+               std::strcmp(fake::launches[1].kind, c.expect) == 0 && fake::last_regions == c.regions,
+           "broadcast order: P=%d n=%lld batch %d env %s took %s (regions %d), expected %s (%d)", c.P,
+           (long long)c.n, c.batch, c.env, fake::launches.size() == 2 ? fake::launches[1].kind : "?",
+           fake::last_regions, c.expect, c.regions);
     ar_plan_destroy(pl);
   }
 }
@@ -762,6 +816,7 @@ int main(int argc, char** argv) {
     errors();
     execute_errors();
     broadcast_choice();
+    broadcast_order_override();
     plans = sweep(1, 1, pmax);
   }
   std::printf("%d plans, %d launch contract problems, %d failures\n", plans, fake::problems.load(), fails.load());

@@ -7,10 +7,12 @@ every rank buffer is 16-byte aligned, with blocks of at least 1024 elements
 (or flat columns, whose results all sit on rank 0); otherwise the tiled
 kernel copies each block from its root.  By default the library takes the
 destination-major copy only where it measured faster (flat columns from
-P = 64, rank buffers of 256 MiB and more); these tests set AR_BCAST_STREAM=1
-so that it runs at sizes the oracle checks whole, and compare both copies
-bit for bit with the oracle: sizes that span several 4 KB chunks per block,
-chunks across block and instance boundaries, and a ragged tail.
+P = 64, rank buffers of 64 MiB and more), its chunks interleaved over the
+XCDs from 256 MiB per rank and in one contiguous region per XCD below.
+These tests set AR_BCAST_STREAM (2: interleaved, 3: regions, 1: the order
+by size) so that it runs at sizes the oracle checks whole, and compare both
+copies bit for bit with the oracle: sizes that span several 4 KB chunks per
+block, chunks across block and instance boundaries, and a ragged tail.
 """
 import sys
 
@@ -64,17 +66,21 @@ CASES = [
 ]
 
 
+ORDERS = ["2", "3"]  # interleaved chunks, XCD regions
+
+
+@pytest.mark.parametrize("order", ORDERS)
 @pytest.mark.parametrize("P,n,k,group,schedule,dtype,op", CASES)
-def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op, monkeypatch):
+def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op, order, monkeypatch):
     """16-byte aligned rows: the destination-major broadcast."""
-    monkeypatch.setenv("AR_BCAST_STREAM", "1")
+    monkeypatch.setenv("AR_BCAST_STREAM", order)
     rng = np.random.default_rng(P * 7 + n)
     x = draw(rng, P, n, dtype)
     plan = ar.Plan(P, n, dtype, op, k, group=group, schedule=schedule)
     st = plan.stats()
     assert st.fused_launches == 2 and st.exec_path == ar.AR_PATH_FUSED and st.fused_bcast_stream == 1
     big, views = aligned_rows(x)
-    note("stream broadcast P=%d n=%d k=%d %s/%s %s %s" % (P, n, k, group, schedule, dtype, op))
+    note("stream broadcast P=%d n=%d k=%d %s/%s %s %s order %s" % (P, n, k, group, schedule, dtype, op, order))
     plan(views)
     torch.cuda.synchronize()
     got = big[:, :n].cpu().numpy()
@@ -84,18 +90,19 @@ def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op, monke
     plan.close()
 
 
+@pytest.mark.parametrize("order", ORDERS)
 @pytest.mark.parametrize("P,n,k", [(127, 127 * 1024 + 77, 14), (64, 64 * 1030 + 1, 12)])
-def test_split_broadcast_contiguous_batch(P, n, k, monkeypatch):
+def test_split_broadcast_contiguous_batch(P, n, k, order, monkeypatch):
     """Three contiguous instances (stride n) in one buffer per rank: chunks
     that straddle an instance boundary take the last block of one instance
     and the first of the next."""
-    monkeypatch.setenv("AR_BCAST_STREAM", "1")
+    monkeypatch.setenv("AR_BCAST_STREAM", order)
     B = 3
     rng = np.random.default_rng(P + k)
     x = draw(rng, P, B * n, "float32")
     big, views = aligned_rows(x)
     plan = ar.Plan(P, n, "float32", "sum", k)
-    note("stream broadcast batch P=%d n=%d B=%d k=%d" % (P, n, B, k))
+    note("stream broadcast batch P=%d n=%d B=%d k=%d order %s" % (P, n, B, k, order))
     plan.batched(views, B, n)
     torch.cuda.synchronize()
     got = big[:, :B * n].cpu().numpy().reshape(P, B, n)
@@ -155,9 +162,12 @@ def test_tiled_and_stream_broadcasts_agree(monkeypatch):
     plan.close()
 
 
-def test_flat_split_broadcast_small_instances():
+@pytest.mark.parametrize("order", ["1", "3"])
+def test_flat_split_broadcast_small_instances(order, monkeypatch):
     """Short blocks on flat columns (results on rank 0 before the broadcast):
-    40 instances of 2304 elements at P = 127, bandwidth-optimal, contiguous."""
+    40 instances of 2304 elements at P = 127, bandwidth-optimal, contiguous;
+    chunks interleaved (the default on flat columns) or in XCD regions."""
+    monkeypatch.setenv("AR_BCAST_STREAM", order)
     P, n, B, k = 127, 2304, 40, 14
     rng = np.random.default_rng(77)
     x = draw(rng, P, B * n, "float32")
@@ -165,7 +175,7 @@ def test_flat_split_broadcast_small_instances():
     plan = ar.Plan(P, n, "float32", "sum", k)
     st = plan.stats()
     assert st.fused_flat == 1 and st.fused_launches == 2 and st.fused_bcast_stream == 1
-    note("flat stream broadcast P=%d n=%d B=%d" % (P, n, B))
+    note("flat stream broadcast P=%d n=%d B=%d order %s" % (P, n, B, order))
     plan.batched(views, B, n)
     torch.cuda.synchronize()
     got = big[:, :B * n].cpu().numpy().reshape(P, B, n)

@@ -111,7 +111,9 @@ def test_fused_path_for_every_plan_with_two_or_more_ranks():
     (127, 1 << 26, 14, "cyclic", 1),          # split, 256 MiB rank buffers
     (64, 1 << 26, 12, "cyclic", 1),
     (128, 1 << 26, 14, "xor", 1),
-    (127, 1 << 25, 14, "cyclic", 0),          # 128 MiB rank buffers: the tiled broadcast
+    (127, 1 << 25, 14, "cyclic", 1),          # 128 MiB rank buffers: one region of chunks per XCD
+    (127, 1 << 24, 14, "cyclic", 1),          # 64 MiB
+    (127, (1 << 24) - 1024, 14, "cyclic", 0), # just below 64 MiB: the tiled broadcast
     (127, 127 * 1024, 14, "cyclic", 0),
     (127, 2304, 14, "cyclic", 1),             # short blocks on flat columns (results on rank 0)
     (128, 2304, 14, "xor", 1),
@@ -127,9 +129,12 @@ def test_destination_major_broadcast_choice(P, n, k, group, want, monkeypatch):
     # flat columns or blocks of at least 1024 elements)
     monkeypatch.setenv("AR_BCAST_STREAM", "0")
     assert ar.Plan(P, n, "float32", "sum", k, group=group).stats().fused_bcast_stream == 0
-    monkeypatch.setenv("AR_BCAST_STREAM", "1")
     allowed = st.fused_launches == 2 and (st.fused_flat == 1 or n // P >= 1024)
-    assert ar.Plan(P, n, "float32", "sum", k, group=group).stats().fused_bcast_stream == int(allowed)
+    for mode in ("1", "2", "3"):  # chunk order by size, interleaved, XCD regions
+        monkeypatch.setenv("AR_BCAST_STREAM", mode)
+        assert ar.Plan(P, n, "float32", "sum", k, group=group).stats().fused_bcast_stream == int(allowed)
+    monkeypatch.setenv("AR_BCAST_STREAM", "4")  # not a mode: the size rules
+    assert ar.Plan(P, n, "float32", "sum", k, group=group).stats().fused_bcast_stream == want
 
 
 def test_execute_argument_errors_before_any_device_work():
