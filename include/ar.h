@@ -111,9 +111,12 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   call allows it (see fused_bcast_stream;
  *                                   default: the size rules given there),
  *                                   its chunks ordered by the default rule
- *                                   (1: one contiguous region per XCD for
- *                                   P >= 104 below 256 MiB per rank, else
- *                                   interleaved over the XCDs), always
+ *                                   (1: one contiguous region of each slice
+ *                                   per XCD on flat columns from 16 MiB per
+ *                                   rank, on blocks that all start on the
+ *                                   4 KB chunk grid, and on other blocks
+ *                                   for P >= 104 below 256 MiB per rank;
+ *                                   else interleaved over the XCDs), always
  *                                   interleaved (2), or always in regions
  *                                   (3);
  *   AR_FUSED_PACKED = 0|1           column launches other than the latency-
@@ -186,10 +189,10 @@ typedef struct {
                                         to hbm_bytes_stepwise                            */
   int32_t fused_bcast_stream;        /* FUSED path split into two launches: 1 when the
                                         broadcast of one instance copies destination by
-                                        destination -- flat columns (short blocks) from
-                                        P = 64, or blocks of at least 1024 elements in
-                                        rank buffers of at least 64 MiB (AR_BCAST_STREAM
-                                        overrides the size rules) -- for calls whose
+                                        destination -- flat columns (short blocks), or
+                                        blocks of at least 1024 elements in rank buffers
+                                        of at least 2 MiB (AR_BCAST_STREAM overrides the
+                                        size rule) -- for calls whose
                                         instances are contiguous (batch 1 or
                                         instance_stride = n) in 16-byte aligned rank
                                         buffers, with batch * n below 2^32 - 1024; other

@@ -252,7 +252,9 @@ struct StreamArgs {
   StreamDiv cdiv, sdiv;     // C (a multiple of the XCD count), C * P
   void* user[kMaxP];
 };
-int launch_broadcast_stream(const StreamArgs& a, bool nt, uint32_t grid, void* stream);
+// straddle: some block or instance boundary falls inside a chunk (block
+// tiles with n % P != 0 or n / P not a multiple of kStreamChunk).
+int launch_broadcast_stream(const StreamArgs& a, bool nt, bool straddle, uint32_t grid, void* stream);
 // Device address of the allocation-free scratch (noalloc.hip) on `device`,
 // which must be the current device; looked up on the first call per device.
 // Returns a hipError_t value.

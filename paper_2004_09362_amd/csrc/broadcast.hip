@@ -65,29 +65,26 @@ __global__ __launch_bounds__(kBlock) void broadcast_kernel(const ColArgs a) {
 
 // Destination-major copy.  The kernel above writes the P - 1 destinations
 // of a column tile at once, so the stores in flight hit P - 1 rank buffers
-// (256 MB apart at P = 127, n = 2^26) and HBM writes them at 5.8 TB/s, where
-// one address-ordered stream of one 16-byte store per thread takes 6.85 TB/s.  Here workgroup
-// ids run slice by slice, destination by destination, chunk by chunk: the
-// workgroups in flight sweep one destination's buffer in address order, and
-// each thread stores 16 bytes once and exits.  A slice's source columns are
-// read from HBM once and then from L2 for the other destinations: workgroup
-// ids go round-robin over the XCDs, so with C chunks per slice a multiple of
-// the XCD count, chunk c of a slice runs on the same XCD for every
-// destination, and C is sized so that each XCD's share of a slice (1 MB)
-// stays in its 4 MB L2 while the destination bytes stream past.  At P = 127,
-// n = 2^26 it took 5.30-5.51 ms against 5.62-5.93 ms for the kernel above
-// (on the same boxes); with C not a multiple of the XCD count 6.9 ms, with
-// 2 MB per XCD 7.5 ms, and with its index arithmetic behind branches (each
-// branch deferring an argument load, a round trip per workgroup) 6.6 ms.
-// Below 256 MB per rank the interleaved chunks often stopped hitting L2 at
-// P = 110-128 (P = 127, 64 MB per rank: 36% of the source reads went to
-// HBM); with a.regions XCD x instead takes the x-th contiguous C / X chunks
-// of each slice, which keeps its sources in L2 at the price of X write
-// streams 1 MB apart (P = 127: 1.45 against 1.60-1.87 ms at 64 MB per
-// rank, 5.74-5.80 against 5.45-5.51 ms at 256 MB).  The chunks of a slice that fall in
-// destination y's own block are skipped (y holds that result already), and
-// a chunk holds at most two blocks (the host asks for blocks of at least
-// kStreamChunk elements), or one root (flat columns).
+// (256 MB apart at P = 127, n = 2^26) and HBM writes them at 5.8 TB/s.  Here
+// workgroup ids run slice by slice, destination by destination, chunk by
+// chunk: the workgroups in flight sweep one destination's buffer in address
+// order, and each thread copies 16 bytes once and exits.  A slice's source
+// columns are read from HBM once and then from L2 for the other
+// destinations: workgroup ids go round-robin over the XCDs, so with C chunks
+// per slice a multiple of the XCD count X, workgroup c of a slice runs on
+// XCD c mod X for every destination.  The chunk it copies is chunk c
+// (interleaved: 1 MB of each slice per XCD, in 4 KB pieces X chunks apart),
+// or with a.regions the ((c mod X) * C / X + c / X)-th (XCD x copies the x-th
+// contiguous C / X chunks: 256 KB of each slice).  Interleaved chunks stop
+// hitting L2 at P = 110-128 below 256 MB per rank (P = 127, 64 MB per rank:
+// 36% of the source reads went to HBM), where regions keep them; regions
+// also suit blocks on the chunk grid.  With C not a multiple of X the copy
+// took 1.3x the time, with 2 MB per XCD 1.4x, and with the index arithmetic
+// behind branches (each deferring an argument load, a round trip per
+// workgroup) 1.2x.  The chunks of a slice that fall in destination y's own
+// block are skipped (y holds that result already), and a chunk holds at most
+// two blocks (the host asks for blocks of at least kStreamChunk elements),
+// or one root (flat columns).
 __device__ __forceinline__ uint32_t sdiv(uint32_t n, const StreamDiv& d) {
   const uint32_t t = __umulhi(n, d.mul);
   return (t + ((n - t) >> d.s1)) >> d.s2;
@@ -102,7 +99,25 @@ __device__ __forceinline__ uint32_t stream_root(const StreamArgs& a, uint32_t g)
   return a.flat ? 0u : (i < a.big ? lo : hi);
 }
 
-template <bool NT>
+// First column after block b0 of the instance holding column `first`
+// (block b0 + 1 = P: the instance's end), for block tiles.
+__device__ __forceinline__ uint32_t stream_block_end(const StreamArgs& a, uint32_t first, uint32_t b0) {
+  const uint32_t i0 = first - sdiv(first, a.ndiv) * a.n;
+  return first - i0 + (b0 + 1) * a.q + min(b0 + 1, a.m);
+}
+
+// STRADDLE: some block or instance boundary is off the kStreamChunk grid,
+// so chunks can span two blocks; such a chunk is copied in whole 16-byte
+// groups, each element selected from its root's load (the elements of y's
+// own block are rewritten with the value y holds: the same bits).  Without
+// STRADDLE only the tail of the column space (and any chunk across a
+// boundary, which the host rules out) takes the element path.  Both kinds
+// are kept because the instructions on the plain path matter: a workgroup
+// does little besides its index arithmetic.  At P = 127, n = 2^26
+// (straddles) the element path took 5.37 ms, whole groups 4.82 ms, and whole
+// groups behind a separate plain path 4.94 ms; at P = 128 (none) the kernel
+// with the plain path first took 4.64 ms and the whole-group one 4.80 ms.
+template <bool NT, bool STRADDLE>
 __global__ __launch_bounds__(kStreamBlock) void broadcast_stream_kernel(const StreamArgs a) {
   const uint32_t id = a.id0 + blockIdx.x;
   const uint32_t s = sdiv(id, a.sdiv);
@@ -116,33 +131,55 @@ __global__ __launch_bounds__(kStreamBlock) void broadcast_stream_kernel(const St
   const uint32_t b0 = stream_root(a, first), b1 = stream_root(a, last);
   if (chunk >= a.chunks || (b0 == y && b1 == y)) return;
   const uint32_t g = first + threadIdx.x * 4u;
-  if (g >= a.cols) return;
   int32_t* dst = static_cast<int32_t*>(a.user[y]);
   const int32_t* s0 = static_cast<const int32_t*>(a.user[b0]);
-  if (b0 == b1 && g + 3 < a.cols) {
-    const i32x4 v = *reinterpret_cast<const i32x4*>(s0 + g);
-    if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<i32x4*>(dst + g));
-    else *reinterpret_cast<i32x4*>(dst + g) = v;
-    return;
+  if constexpr (STRADDLE) {
+    if (first + kStreamChunk <= a.cols) {
+      i32x4 v = *reinterpret_cast<const i32x4*>(s0 + g);
+      if (b0 != b1) {  // block b0 ends at column bnd of this chunk
+        const int32_t* s1 = static_cast<const int32_t*>(a.user[b1]);
+        const i32x4 w = *reinterpret_cast<const i32x4*>(s1 + g);
+        const uint32_t bnd = stream_block_end(a, first, b0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[i] = g + uint32_t(i) < bnd ? v[i] : w[i];
+      }
+      if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<i32x4*>(dst + g));
+      else *reinterpret_cast<i32x4*>(dst + g) = v;
+      return;
+    }
+  } else {
+    if (b0 == b1 && first + kStreamChunk <= a.cols) {
+      const i32x4 v = *reinterpret_cast<const i32x4*>(s0 + g);
+      if constexpr (NT) __builtin_nontemporal_store(v, reinterpret_cast<i32x4*>(dst + g));
+      else *reinterpret_cast<i32x4*>(dst + g) = v;
+      return;
+    }
   }
-  // a chunk across a block boundary, or the tail of the column space
+  // the chunk at the end of the column space (and, without STRADDLE, any
+  // chunk across a boundary): element by element
   const int32_t* s1 = static_cast<const int32_t*>(a.user[b1]);
+  const uint32_t bnd = a.flat ? a.cols : stream_block_end(a, first, b0);
+  const bool w0 = b0 != y, w1 = b1 != y;
 #pragma unroll
   for (uint32_t i = 0; i < 4; ++i) {
     const uint32_t gi = g + i;
-    if (gi < a.cols) {
-      const uint32_t b = stream_root(a, gi);
-      if (b != y) st1<NT>(dst + gi, (b == b0 ? s0 : s1)[gi]);
-    }
+    const bool lo = gi < bnd;
+    if (gi < a.cols && (lo ? w0 : w1)) st1<NT>(dst + gi, (lo ? s0 : s1)[gi]);
   }
 }
 
 }  // namespace
 
-int launch_broadcast_stream(const StreamArgs& a, bool nt, uint32_t grid, void* stream) {
+int launch_broadcast_stream(const StreamArgs& a, bool nt, bool straddle, uint32_t grid, void* stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  if (nt) hipLaunchKernelGGL((broadcast_stream_kernel<true>), dim3(grid), dim3(kStreamBlock), 0, s, a);
-  else hipLaunchKernelGGL((broadcast_stream_kernel<false>), dim3(grid), dim3(kStreamBlock), 0, s, a);
+  const dim3 g(grid), blk(kStreamBlock);
+  if (straddle) {
+    if (nt) hipLaunchKernelGGL((broadcast_stream_kernel<true, true>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((broadcast_stream_kernel<false, true>), g, blk, 0, s, a);
+  } else {
+    if (nt) hipLaunchKernelGGL((broadcast_stream_kernel<true, false>), g, blk, 0, s, a);
+    else hipLaunchKernelGGL((broadcast_stream_kernel<false, false>), g, blk, 0, s, a);
+  }
   return int(hipGetLastError());
 }
 

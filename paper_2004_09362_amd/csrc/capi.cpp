@@ -43,22 +43,24 @@ constexpr int32_t kFlatSplitMinP = 33;
 // the same at P = 64, and 13% slower at P = 48.  Neither change helps alone.
 constexpr int32_t kBcastStreamMinP = 96;
 // The destination-major broadcast (broadcast.hip) by default: on flat
-// columns from this many ranks up (P = 64-128: 7-16% faster than the tiled
-// copy from 0.6 to 9.6 GB; P = 37 and 48: 0.5-7% slower), and on block
-// tiles where a rank's span of the call reaches kBcastRegionMinBytes.  The
-// XCDs take interleaved chunks from kBcastStreamMinBytes (P = 64-128, 256 MB
-// per rank: 7-18% faster than the tiled copy), and below it up to
-// kBcastRegionMinP - 1 ranks (P = 64-100 at 64 and 128 MB: 4-11% faster).
-// From kBcastRegionMinP ranks below 256 MB the interleaved chunks often read
-// their sources from L2 no more (P = 110-128 at 64 MB: 3-25% slower than
-// the tiled copy, up to 45% at 128 MB with rank buffers 2^27 bytes apart);
-// there each XCD takes a contiguous region of the slice instead, which ran
-// at 5.8-5.9 TB/s in every case measured (tiled: 5.4-6.3, in most cases
-// below).  Below 64 MB per rank the tiled copy was as fast or faster at
-// P = 100-127.
-constexpr int32_t kBcastStreamFlatMinP = 64;
-constexpr int64_t kBcastStreamMinBytes = int64_t(256) << 20;
-constexpr int64_t kBcastRegionMinBytes = int64_t(64) << 20;
+// columns at any P, and on block tiles where a rank's span of the call
+// reaches kBcastStreamMinBytes (smaller spans not measured).  Measured
+// against the tiled copy (rank rows back to back), it took 6-24% less time
+// on block tiles at P = 64-128 and 2-256 MB per rank (5.7-7.2 TB/s against
+// 5.0-6.2), and 6-21% less on flat columns at P = 37-128 and 4.5-72 MB per
+// rank.  Its chunk order: XCD regions on flat columns from
+// kBcastFlatRegionMinBytes per rank (interleaved below, where short slices
+// left XCDs idle; within 2% either way above), and on block tiles whose
+// blocks all start on the chunk grid (P = 64 and 128 from 32 MB per rank:
+// 5-55% less time than interleaved; P = 64 below: up to 7% more); with
+// straddling chunks interleaved below kBcastRegionMinP ranks (P = 100:
+// 5-10% less time than regions) or from kBcastInterleaveMinBytes per rank
+// (P = 127 at 256 MB: 5%), and regions otherwise, where the interleaved
+// chunks read their sources from L2 no more (P = 127 below 256 MB per rank:
+// 1.1-2.0x the time of regions).
+constexpr int64_t kBcastStreamMinBytes = int64_t(2) << 20;
+constexpr int64_t kBcastFlatRegionMinBytes = int64_t(16) << 20;
+constexpr int64_t kBcastInterleaveMinBytes = int64_t(256) << 20;
 constexpr int32_t kBcastRegionMinP = 104;
 // Blocks of at most this many elements (many small instances) are packed:
 // a column-fused wave takes one block of 64 / max_len instances instead of 64
@@ -120,8 +122,8 @@ struct ar_plan {
   // AR_BCAST_STREAM = 0|1|2|3 (the broadcast tiled by block / destination by
   // destination wherever the call allows it, with the chunk order by size,
   // interleaved, or in XCD regions; default by the size rules at
-  // kBcastStreamFlatMinP, kBcastRegionMinBytes, kBcastStreamMinBytes and
-  // kBcastRegionMinP),
+  // kBcastStreamMinBytes, kBcastFlatRegionMinBytes, kBcastInterleaveMinBytes
+  // and kBcastRegionMinP),
   // AR_FUSED_PACKED = 0|1 (column tiles of one block of one instance / of
   // several instances, for blocks of up to 64 elements; default: packed for
   // batches whose blocks hold up to kPackMaxLen elements), AR_FUSED_ROTATE =
@@ -335,12 +337,19 @@ bool stream_bcast_args(const ar_plan* pl, void* const* bufs, int64_t batch, int6
   if (!flat && s.n / s.P < int64_t(ar::kStreamChunk)) return false;
   for (int32_t x = 0; x < s.P; ++x)
     if (reinterpret_cast<uintptr_t>(bufs[x]) % 16 != 0) return false;
-  // chunks per slice: 1 MB per XCD, or all chunks (rounded up to the XCD
-  // count) when there are fewer, so that no workgroup is launched for nothing
-  const uint32_t xcd_chunks = stream_slice_chunks(device);
+  // chunks per slice: at most 1 MB per XCD interleaved, 256 KB per XCD in
+  // regions (at 8-32 MB per rank 1 MB regions ran 3-50% slower; from 64 MB
+  // the sizes ran within a few percent), evened out over the slices and
+  // rounded up to the XCD count, so that the last slice is about as full as
+  // the others (a short last slice in regions leaves most XCDs idle)
+  const uint32_t xcds = stream_slice_chunks(device) / 256;
+  uint32_t shift = 0;
+  while ((1u << shift) < xcds) ++shift;
+  const bool reg = regions && (1u << shift) == xcds;
   const uint32_t chunks = uint32_t((cols + ar::kStreamChunk - 1) / ar::kStreamChunk);
-  const uint32_t xcds = xcd_chunks / 256;
-  const uint32_t C = std::min(xcd_chunks, (chunks + xcds - 1) / xcds * xcds);
+  const uint32_t cmax = (reg ? 64u : 256u) * xcds;
+  const uint32_t slices = (chunks + cmax - 1) / cmax;
+  const uint32_t C = ((chunks + slices - 1) / slices + xcds - 1) / xcds * xcds;
   const int64_t grid = (int64_t(chunks) + C - 1) / C * C * s.P;
   if (grid > int64_t(UINT32_MAX) / ar::kStreamBlock) return false;  // work-items per launch below 2^32
   std::memset(sa, 0, sizeof *sa);
@@ -359,9 +368,7 @@ bool stream_bcast_args(const ar_plan* pl, void* const* bufs, int64_t batch, int6
   sa->sdiv = ar::stream_div(C * uint32_t(s.P));
   sa->chunks = chunks;
   sa->id0 = 0;
-  uint32_t shift = 0;
-  while ((1u << shift) < xcds) ++shift;
-  sa->regions = regions && (1u << shift) == xcds ? 1 : 0;
+  sa->regions = reg ? 1 : 0;
   sa->xcd_shift = shift;
   sa->per_xcd = C / xcds;
   return true;
@@ -593,15 +600,19 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
                      (pl->bcast_nt_mode < 0 && (s.P >= kBcastStreamMinP || flat_short) &&
                       int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes);
     ar::StreamArgs sa;
+    const int64_t span = batch * s.n * 4;
     const bool want_stream =
-        pl->bcast_stream_mode >= 1 ||
-        (pl->bcast_stream_mode < 0 && (a.flat ? s.P >= kBcastStreamFlatMinP : batch * s.n * 4 >= kBcastRegionMinBytes));
-    const bool regions =
-        pl->bcast_stream_mode == 3 || (pl->bcast_stream_mode != 2 && !a.flat && s.P >= kBcastRegionMinP &&
-                                       batch * s.n * 4 < kBcastStreamMinBytes);
+        pl->bcast_stream_mode >= 1 || (pl->bcast_stream_mode < 0 && (a.flat || span >= kBcastStreamMinBytes));
+    // chunks can straddle two blocks when a block or instance boundary is
+    // not a multiple of the chunk
+    const bool straddle = !a.flat && (s.n % s.P != 0 || (s.n / s.P) % ar::kStreamChunk != 0);
+    bool regions;
+    if (pl->bcast_stream_mode == 2 || pl->bcast_stream_mode == 3) regions = pl->bcast_stream_mode == 3;
+    else if (a.flat) regions = span >= kBcastFlatRegionMinBytes;
+    else regions = !straddle || (s.P >= kBcastRegionMinP && span < kBcastInterleaveMinBytes);
     if (want_stream && stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, regions, device, &sa)) {
       const uint32_t sgrid = (sa.chunks + sa.cdiv.d - 1) / sa.cdiv.d * sa.sdiv.d;
-      e = ar::launch_broadcast_stream(sa, bnt, sgrid, stream);
+      e = ar::launch_broadcast_stream(sa, bnt, straddle, sgrid, stream);
     } else {
       a.lds = cap_lds(pl->bcast_cap, device);
       e = ar::launch_broadcast(a, pl->dtype, bnt, grid, stream);
@@ -939,12 +950,12 @@ ar_status ar_plan_stats(const ar_plan* plan, ar_stats* out) {
                                      : AR_PATH_STEPWISE;
   out->hbm_bytes_algorithmic = out->hbm_bytes_stepwise;
   {
-    // the default choice for one instance (ar.h): flat columns from
-    // kBcastStreamFlatMinP ranks, blocks of at least kStreamChunk elements in
-    // rank buffers of at least kBcastRegionMinBytes
+    // the default choice for one instance (ar.h): flat columns, and blocks
+    // of at least kStreamChunk elements in rank buffers of at least
+    // kBcastStreamMinBytes
     const bool flat = plan->fused_flat;
     const bool allowed = flat || s.n / std::max<int32_t>(s.P, 1) >= int64_t(ar::kStreamChunk);
-    const bool by_size = flat ? s.P >= kBcastStreamFlatMinP : s.n * 4 >= kBcastRegionMinBytes;
+    const bool by_size = flat || s.n * 4 >= kBcastStreamMinBytes;
     out->fused_bcast_stream =
         s.P > 1 && plan->fused_split && allowed && (plan->bcast_stream_mode >= 1 || (plan->bcast_stream_mode < 0 && by_size))
             ? 1

@@ -228,7 +228,7 @@ int launch_broadcast(const ColArgs& a, int, bool, int grid, void*) {
 // roots (flat columns, or blocks of at least kStreamChunk elements), slices
 // of a multiple of 8 chunks (the fake device's 256 CUs: 8 XCDs), 2048 or
 // all the chunks, and a grid of whole slices below 2^32 work-items.
-int launch_broadcast_stream(const StreamArgs& a, bool, uint32_t grid, void*) {
+int launch_broadcast_stream(const StreamArgs& a, bool, bool straddle, uint32_t grid, void*) {
   const int P = int(a.P);
   if (P < 2 || P > kMaxP) fake::problem("stream broadcast P", P);
   for (int x = 0; x < P && x < kMaxP; ++x)
@@ -239,12 +239,21 @@ int launch_broadcast_stream(const StreamArgs& a, bool, uint32_t grid, void*) {
   if (!a.flat && a.q < kStreamChunk) fake::problem("stream blocks shorter than a chunk", P);
   if (a.n == 0 || a.cols % a.n != 0 || a.ndiv.d != a.n) fake::problem("stream instance length", P);
   if (a.q != a.n / a.P || a.m != a.n % a.P || a.q1div.d != a.q + 1) fake::problem("stream block sizes", P);
-  if (a.cdiv.d % 8 != 0 || a.cdiv.d > 2048 || (a.cdiv.d < 2048 && a.cdiv.d >= a.chunks + 8) ||
-      a.sdiv.d != a.cdiv.d * a.P)
+  const uint32_t cmax = a.regions ? 512 : 2048;  // 256 KB / 1 MB per XCD and slice, 8 XCDs
+  const uint32_t slices = (a.chunks + a.cdiv.d - 1) / std::max<uint32_t>(a.cdiv.d, 1);
+  if (a.cdiv.d % 8 != 0 || a.cdiv.d > cmax || slices != (a.chunks + cmax - 1) / cmax ||
+      uint64_t(a.cdiv.d) * slices >= uint64_t(a.chunks) + 8 * slices || a.sdiv.d != a.cdiv.d * a.P)
     fake::problem("stream slice size", P);
   if (a.id0 != 0 || grid != (a.chunks + a.cdiv.d - 1) / a.cdiv.d * a.sdiv.d) fake::problem("stream grid", P);
   if (a.regions > 1 || a.xcd_shift != 3 || a.per_xcd * 8 != a.cdiv.d) fake::problem("stream XCD regions", P);
   fake::last_regions = int(a.regions);
+  {
+    // a chunk can straddle two blocks exactly when some block or instance boundary is off the chunk grid
+    bool off_grid = false;
+    if (!a.flat)
+      for (uint32_t b = 1; b <= a.P && !off_grid; ++b) off_grid = (b * a.q + std::min(b, a.m)) % kStreamChunk != 0;
+    if (straddle != off_grid) fake::problem("stream straddle flag", P);
+  }
   if (uint64_t(grid) * 256 > UINT32_MAX) fake::problem("stream grid beyond 2^32 work-items", P);
   return record("broadcast_stream", P, int(grid), a.chunks);
 }
@@ -502,19 +511,23 @@ static void broadcast_choice() {
       {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 4, "broadcast", -1},          // a rank buffer off 16 bytes
       {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 128 MiB per rank: XCD regions
       {127, int64_t(1) << 24, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 64 MiB
-      {127, (int64_t(1) << 24) - 1024, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast", -1}, // just below 64 MiB
+      {127, (int64_t(1) << 24) - 1024, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
+      {127, int64_t(1) << 19, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 2 MiB per rank
+      {127, (int64_t(1) << 19) - 1024, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast", -1}, // just below 2 MiB
+      {64, int64_t(1) << 19, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
       {100, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},   // below 104 ranks: interleaved
       {104, int64_t(1) << 24, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
-      {64, int64_t(1) << 24, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
+      {64, int64_t(1) << 24, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},     // blocks on the chunk grid: regions
       {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast", -1},
-      {64, int64_t(1) << 26, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
-      {128, int64_t(1) << 26, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 0},
+      {64, int64_t(1) << 26, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
+      {128, int64_t(1) << 26, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream", 0},                // flat columns, root rank 0
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 3, 0, "broadcast", -1},
       {128, 2304, 14, AR_GROUP_XOR, 4, 0, 0, "broadcast_stream", 0},
-      {48, 2304, 12, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast", -1},                        // flat, below 64 ranks
+      {48, 2304, 12, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream", 0},                  // flat, any P
+      {48, 2304, 12, AR_GROUP_CYCLIC, 8192, 0, 0, "broadcast_stream", 1},               // flat, 72 MiB per rank: regions
       {127, 2304, 14, AR_GROUP_CYCLIC, 60000, 0, 0, "broadcast", -1},                   // grid above 2^32 work-items
-      {127, 2304, 14, AR_GROUP_CYCLIC, 56000, 0, 0, "broadcast_stream", 0},            // just below it
+      {127, 2304, 14, AR_GROUP_CYCLIC, 56000, 0, 0, "broadcast_stream", 1},            // just below it
   };
   for (const Case& c : cases) {
     ar_plan* pl = nullptr;

@@ -6,13 +6,16 @@ broadcast can run destination-major when the instances are contiguous and
 every rank buffer is 16-byte aligned, with blocks of at least 1024 elements
 (or flat columns, whose results all sit on rank 0); otherwise the tiled
 kernel copies each block from its root.  By default the library takes the
-destination-major copy only where it measured faster (flat columns from
-P = 64, rank buffers of 64 MiB and more), its chunks interleaved over the
-XCDs from 256 MiB per rank and in one contiguous region per XCD below.
-These tests set AR_BCAST_STREAM (2: interleaved, 3: regions, 1: the order
-by size) so that it runs at sizes the oracle checks whole, and compare both
-copies bit for bit with the oracle: sizes that span several 4 KB chunks per
-block, chunks across block and instance boundaries, and a ragged tail.
+destination-major copy on flat columns and on rank buffers of 2 MiB and
+more, its chunks interleaved over the XCDs or in one contiguous region per
+XCD by shape.  A chunk across a block or instance boundary is copied as
+whole 16-byte groups, each element from its own root's load (the kernel for
+blocks off the 4 KB chunk grid), or element by element (the kernel for
+blocks on it, where only the tail takes that path).  These tests set
+AR_BCAST_STREAM (2: interleaved, 3: regions, 1: the default order) so that
+it runs at sizes the oracle checks whole, and compare both copies bit for
+bit with the oracle: sizes that span several 4 KB chunks per block, chunks
+across block and instance boundaries, and a ragged tail.
 """
 import sys
 

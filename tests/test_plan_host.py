@@ -113,11 +113,13 @@ def test_fused_path_for_every_plan_with_two_or_more_ranks():
     (128, 1 << 26, 14, "xor", 1),
     (127, 1 << 25, 14, "cyclic", 1),          # 128 MiB rank buffers: one region of chunks per XCD
     (127, 1 << 24, 14, "cyclic", 1),          # 64 MiB
-    (127, (1 << 24) - 1024, 14, "cyclic", 0), # just below 64 MiB: the tiled broadcast
+    (127, (1 << 24) - 1024, 14, "cyclic", 1),
+    (127, 1 << 19, 14, "cyclic", 1),          # 2 MiB
+    (127, (1 << 19) - 1024, 14, "cyclic", 0), # just below 2 MiB: the tiled broadcast
     (127, 127 * 1024, 14, "cyclic", 0),
     (127, 2304, 14, "cyclic", 1),             # short blocks on flat columns (results on rank 0)
     (128, 2304, 14, "xor", 1),
-    (48, 2304, 12, "cyclic", 0),              # flat, below 64 ranks
+    (48, 2304, 12, "cyclic", 1),              # flat, any P
     (127, 1 << 26, 10, "cyclic", 0),          # shifted: one launch, no broadcast
     (37, 1 << 22, 12, "cyclic", 0),           # below the split's P
 ])
