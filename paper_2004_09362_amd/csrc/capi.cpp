@@ -29,8 +29,15 @@ constexpr int64_t kFusedNtThresholdBytes = int64_t(128) << 20;
 // Plans whose ranks all receive the same result (bandwidth-optimal in either
 // group, the Ring) run fused as a reducing launch plus a broadcast from this
 // many ranks up (broadcast.hip): measured faster at P = 64 and 127, slower
-// at P = 24 and 48.
+// at P = 24 and 48 (with the tiled broadcast).  Block-tiled plans whose
+// instance spans kSplitMidMinBytes per rank split from kSplitMidMinP ranks:
+// with the destination-major broadcast the pair's launches summed to 5-11%
+// less time than the single launch at P = 32-56, n = 2^24 (the second launch
+// adds about 10 us per call); at n = 2^22 from 9% less to 5% more, and at
+// P = 24 the call took 2.5% longer.
 constexpr int32_t kSplitMinP = 64;
+constexpr int32_t kSplitMidMinP = 32;
+constexpr int64_t kSplitMidMinBytes = int64_t(64) << 20;
 // Flat short-block sums in the rank-slot kernel (not the XOR group's) split
 // from this many ranks up: their single launch streams 5.0-5.6 TB/s there and
 // the pair up to 6.0 (P = 37: 7%, P = 48: 15% faster with caps 4 and 2 and a
@@ -800,7 +807,8 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
     pl->fused_flat = kind && op_ok && (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && max_len <= kPackMaxLen));
   }
   const bool rank_slots = pl->fused_flat && pl->fused_kind != kFusedXor;
-  const int32_t split_min = rank_slots ? kFlatSplitMinP : kSplitMinP;
+  const int32_t split_min =
+      rank_slots ? kFlatSplitMinP : (pl->s.n * 4 >= kSplitMidMinBytes ? kSplitMidMinP : kSplitMinP);
   pl->fused_split = one_result && (pl->split_mode == 1 || (pl->split_mode < 0 && pl->s.P >= split_min));
   {
     const int32_t P = pl->s.P;
