@@ -184,3 +184,29 @@ def test_flat_split_broadcast_small_instances(order, monkeypatch):
     got = big[:, :B * n].cpu().numpy().reshape(P, B, n)
     assert np.array_equal(bits(got), bits(oracle.allreduce_batched(x.reshape(P, B, n), k, "sum")))
     plan.close()
+
+
+@pytest.mark.parametrize("order", ORDERS)
+@pytest.mark.parametrize("P,k,group,schedule", [
+    (2, 2, "cyclic", "butterfly"), (3, 4, "cyclic", "butterfly"), (5, 6, "cyclic", "butterfly"),
+    (8, 6, "xor", "butterfly"), (16, 30, "cyclic", "ring"), (17, 10, "cyclic", "butterfly")])
+def test_split_forced_at_small_p(P, k, group, schedule, order, monkeypatch):
+    """Few destinations: the split forced (AR_FUSED_SPLIT=1) with the
+    destination-major copy, blocks of at least 1024 elements off the chunk
+    grid, three contiguous instances and a ragged tail."""
+    monkeypatch.setenv("AR_FUSED_SPLIT", "1")
+    monkeypatch.setenv("AR_BCAST_STREAM", order)
+    n, B = P * 1500 + 7, 3
+    rng = np.random.default_rng(P * 31 + k)
+    x = draw(rng, P, B * n, "float32")
+    big, views = aligned_rows(x)
+    plan = ar.Plan(P, n, "float32", "sum", k, group=group, schedule=schedule)
+    st = plan.stats()
+    assert st.fused_launches == 2 and st.fused_bcast_stream == 1
+    note("forced split P=%d n=%d B=%d k=%d %s/%s order %s" % (P, n, B, k, group, schedule, order))
+    plan.batched(views, B, n)
+    torch.cuda.synchronize()
+    got = big[:, :B * n].cpu().numpy().reshape(P, B, n)
+    want = oracle.allreduce_batched(x.reshape(P, B, n), k, "sum", group=group, schedule=schedule)
+    assert np.array_equal(bits(got), bits(want))
+    plan.close()
