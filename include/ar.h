@@ -105,8 +105,10 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   least 64 MiB, and for P >= 33 in the
  *                                   rank-slot kernel on short blocks);
  *   AR_BCAST_NT = 0|1               nontemporal loads and stores in that
- *                                   broadcast (default: for large launches
- *                                   with P >= 96, or on flat columns);
+ *                                   broadcast (default, for launches of 128
+ *                                   MiB and more: the tiled copy with
+ *                                   P >= 96 or on flat columns; the
+ *                                   destination-major copy always);
  *   AR_BCAST_STREAM = 0|1|2|3       that broadcast tiled by block always /
  *                                   destination by destination wherever the
  *                                   call allows it (see fused_bcast_stream;

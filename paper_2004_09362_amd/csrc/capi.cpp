@@ -601,11 +601,11 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
   if (e != 0) return hip_fail(hipError_t(e), "column-fused kernel launch");
   if (tm) tm->mark();
   if (pl->fused_split) {
-    // nontemporal stores from kBcastStreamMinP ranks up, and on flat columns
-    // at any P (P = 37: 11% faster, P = 48-128: 1-3%)
+    // the tiled copy: nontemporal stores from kBcastStreamMinP ranks up, and
+    // on flat columns at any P (P = 37: 11% faster, P = 48-128: 1-3%)
+    const bool big = int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes;
     const bool bnt = pl->bcast_nt_mode == 1 ||
-                     (pl->bcast_nt_mode < 0 && (s.P >= kBcastStreamMinP || flat_short) &&
-                      int64_t(s.P) * s.n * batch * 4 >= kFusedNtThresholdBytes);
+                     (pl->bcast_nt_mode < 0 && (s.P >= kBcastStreamMinP || flat_short) && big);
     ar::StreamArgs sa;
     const int64_t span = batch * s.n * 4;
     const bool want_stream =
@@ -619,7 +619,13 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
     else regions = !straddle || (s.P >= kBcastRegionMinP && span < kBcastInterleaveMinBytes);
     if (want_stream && stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, regions, device, &sa)) {
       const uint32_t sgrid = (sa.chunks + sa.cdiv.d - 1) / sa.cdiv.d * sa.sdiv.d;
-      e = ar::launch_broadcast_stream(sa, bnt, straddle, sgrid, stream);
+      // the destination-major copy: nontemporal at any P (launches of
+      // kFusedNtThresholdBytes and more).  Alone, its cached stores were up
+      // to 6% faster on some shapes (P = 64 at 16 MB per rank, flat columns),
+      // but the pair then took 0.3-10% longer: the next reducing launch pays
+      // for the cached lines (P = 32-128, 4-256 MB per rank, flat and block)
+      const bool snt = pl->bcast_nt_mode == 1 || (pl->bcast_nt_mode < 0 && big);
+      e = ar::launch_broadcast_stream(sa, snt, straddle, sgrid, stream);
     } else {
       a.lds = cap_lds(pl->bcast_cap, device);
       e = ar::launch_broadcast(a, pl->dtype, bnt, grid, stream);
