@@ -66,6 +66,8 @@ CASES = [
     (127, 127 * 1500 + 126, 14, "cyclic", "butterfly", "float32", "max"),
     (128, 128 * 1024 + 5, 14, "xor", "butterfly", "float32", "sum"),
     (100, 100 * 1100 + 3, 198, "cyclic", "ring", "float32", "sum"),
+    (64, 64 * 1024 + 63, 12, "cyclic", "butterfly", "float32", "sum"),  # blocks of 1024-1025: a straddle per block
+    (37, 2049 * 1024 + 5, 12, "cyclic", "butterfly", "int32", "sum"),   # 2050 chunks: five evened-out slices
 ]
 
 
@@ -75,8 +77,10 @@ ORDERS = ["2", "3"]  # interleaved chunks, XCD regions
 @pytest.mark.parametrize("order", ORDERS)
 @pytest.mark.parametrize("P,n,k,group,schedule,dtype,op", CASES)
 def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op, order, monkeypatch):
-    """16-byte aligned rows: the destination-major broadcast."""
+    """16-byte aligned rows: the destination-major broadcast (the split
+    forced, for P = 37)."""
     monkeypatch.setenv("AR_BCAST_STREAM", order)
+    monkeypatch.setenv("AR_FUSED_SPLIT", "1")
     rng = np.random.default_rng(P * 7 + n)
     x = draw(rng, P, n, dtype)
     plan = ar.Plan(P, n, dtype, op, k, group=group, schedule=schedule)
