@@ -133,7 +133,8 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   plans:
  *                                   never / always on flat columns as above
  *                                   (default: when blocks hold at most 64
- *                                   elements);
+ *                                   elements, and for shifted sums at odd
+ *                                   P >= 97);
  *   AR_FUSED_CAP = N or N,M         resident workgroups per CU of the fused
  *                                   launch (and of the broadcast); 0 is no
  *                                   cap (default: per kernel and P);
@@ -179,10 +180,11 @@ typedef struct {
                                         at least 64 MiB; P >= 33 for sums with short
                                         blocks outside the XOR group)                    */
   int32_t fused_flat;                /* FUSED path with short blocks (sums; max in the
-                                        bandwidth-optimal, Ring and XOR plans): 1 when it
-                                        runs on flat columns (the rank-slot kernel, or
-                                        the XOR group's kernel without the block) for
-                                        batches of fewer than 2^32 - 64 columns           */
+                                        bandwidth-optimal, Ring and XOR plans), or
+                                        shifted sums at odd P >= 97: 1 when it runs on
+                                        flat columns (the rank-slot kernel, or the XOR
+                                        group's kernel without the block) for batches of
+                                        fewer than 2^32 - 64 columns                     */
   int32_t exec_path;                 /* path ar_execute takes: AR_PATH_STEPWISE or
                                         AR_PATH_FUSED (AR_PATH_AUTO resolved); 0 when
                                         there is nothing to run (P = 1)                  */

@@ -77,6 +77,15 @@ constexpr int32_t kBcastRegionMinP = 104;
 // blocks of 33, 1.6x for the Ring at P = 24; within 4% of them for
 // bandwidth-optimal P = 24 and shifted P = 37 with blocks of 4-9.
 constexpr int64_t kPackMaxLen = 64;
+// Shifted sums (0 < r < L) on long blocks take the rank-slot kernel at odd P
+// from this many ranks: there the block-tiled shifted kernel holds all P
+// starred sums at one wave per SIMD (256 VGPRs plus 24-153 AGPRs), the
+// rank-slot kernel, which keeps only the sums its r needs, two.  Measured on
+// n = 2^24-2^26 fp32: 1-10% less time at P = 99, 111, 125 and 127 (the large
+// workload at k = 10: 5%), within 2.4% either way at P = 87, 3-9% more at
+// P = 33-81 (odd or even) and 1-5% more at even P = 72-100; mixed at P = 120
+// and faster at P = 128 (its kernel at three waves) by 3-5%.
+constexpr int32_t kRotShiftedMinP = 97;
 // Step launches whose blocks hold at most this many elements stream each
 // range's run of blocks as one flat space per rank (step_merged_kernel):
 // short blocks otherwise leave most lanes of the 1 KB block tiles idle.
@@ -810,7 +819,10 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
     // the XOR group, whose flat kernel then takes each lane's block
     const bool op_ok = pl->op == AR_SUM || pl->fused_kind == kFusedRing || pl->fused_kind == kFusedXor ||
                        (pl->fused_kind == kFusedCol && pl->s.r == 0);
-    pl->fused_flat = kind && op_ok && (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && max_len <= kPackMaxLen));
+    const bool odd_shifted = pl->fused_kind == kFusedCol && pl->s.r > 0 && pl->op == AR_SUM &&
+                             pl->s.P >= kRotShiftedMinP && pl->s.P % 2 == 1;
+    pl->fused_flat = kind && op_ok &&
+                     (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && (max_len <= kPackMaxLen || odd_shifted)));
   }
   const bool rank_slots = pl->fused_flat && pl->fused_kind != kFusedXor;
   const int32_t split_min =
