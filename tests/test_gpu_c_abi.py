@@ -32,6 +32,8 @@ CASES = [
     (37, 4101, 3, 4200, -1, "float32", "sum", STEPWISE, 1),
     (127, 9219, 1, 9219, 14, "float32", "sum", AUTO, 0),
     (127, 9219, 1, 9219, 10, "float32", "sum", STEPWISE, 0),
+    (127, 524295, 1, 524295, 14, "float32", "sum", AUTO, 0),  # 2 MiB per rank: split, destination-major copy
+    (127, 524295, 1, 524295, 10, "float32", "sum", AUTO, 0),  # shifted at odd P: the rank-slot kernel
 ]
 
 
