@@ -84,8 +84,15 @@ constexpr int64_t kPackMaxLen = 64;
 // n = 2^24-2^26 fp32: 1-10% less time at P = 99, 111, 125 and 127 (the large
 // workload at k = 10: 5%), within 2.4% either way at P = 87, 3-9% more at
 // P = 33-81 (odd or even) and 1-5% more at even P = 72-100; mixed at P = 120
-// and faster at P = 128 (its kernel at three waves) by 3-5%.
+// and faster at P = 128 (its kernel at three waves) by 3-5%.  Also at
+// P = kRotShiftedSmallMinP-kRotShiftedSmallMaxP with instances of at most
+// kRotShiftedSmallMaxBytes per rank: 1-5% less time at P = 24, 33, 34, 37,
+// 47 and 48 with 8-32 MB per rank (the prime_sweep shape, P = 37 at 16 MB:
+// 4-5% at k = 7-11), 1-10% more at 64 MB; at P = 64-93 within 2.4% either
+// way up to 32 MB.
 constexpr int32_t kRotShiftedMinP = 97;
+constexpr int32_t kRotShiftedSmallMinP = 24, kRotShiftedSmallMaxP = 48;
+constexpr int64_t kRotShiftedSmallMaxBytes = int64_t(32) << 20;
 // Step launches whose blocks hold at most this many elements stream each
 // range's run of blocks as one flat space per rank (step_merged_kernel):
 // short blocks otherwise leave most lanes of the 1 KB block tiles idle.
@@ -819,10 +826,13 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
     // the XOR group, whose flat kernel then takes each lane's block
     const bool op_ok = pl->op == AR_SUM || pl->fused_kind == kFusedRing || pl->fused_kind == kFusedXor ||
                        (pl->fused_kind == kFusedCol && pl->s.r == 0);
-    const bool odd_shifted = pl->fused_kind == kFusedCol && pl->s.r > 0 && pl->op == AR_SUM &&
-                             pl->s.P >= kRotShiftedMinP && pl->s.P % 2 == 1;
+    const bool shifted_sum = pl->fused_kind == kFusedCol && pl->s.r > 0 && pl->op == AR_SUM;
+    const bool rot_shifted =
+        shifted_sum && ((pl->s.P >= kRotShiftedMinP && pl->s.P % 2 == 1) ||
+                        (pl->s.P >= kRotShiftedSmallMinP && pl->s.P <= kRotShiftedSmallMaxP &&
+                         pl->s.n * 4 <= kRotShiftedSmallMaxBytes));
     pl->fused_flat = kind && op_ok &&
-                     (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && (max_len <= kPackMaxLen || odd_shifted)));
+                     (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && (max_len <= kPackMaxLen || rot_shifted)));
   }
   const bool rank_slots = pl->fused_flat && pl->fused_kind != kFusedXor;
   const int32_t split_min =
