@@ -133,9 +133,11 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   plans:
  *                                   never / always on flat columns as above
  *                                   (default: when blocks hold at most 64
- *                                   elements, and for shifted sums at odd
- *                                   P >= 97 or at P = 24-48 with n * e up
- *                                   to 32 MiB);
+ *                                   elements; shifted sums at odd P >= 97
+ *                                   or at P = 24-48 with n * e up to
+ *                                   32 MiB; bandwidth-optimal and Ring
+ *                                   plans from P = 33 with n * e below
+ *                                   256 MiB);
  *   AR_FUSED_CAP = N or N,M         resident workgroups per CU of the fused
  *                                   launch (and of the broadcast); 0 is no
  *                                   cap (default: per kernel and P);
@@ -181,9 +183,9 @@ typedef struct {
                                         at least 64 MiB; P >= 33 for sums with short
                                         blocks outside the XOR group)                    */
   int32_t fused_flat;                /* FUSED path with short blocks (sums; max in the
-                                        bandwidth-optimal, Ring and XOR plans), or
-                                        shifted sums at odd P >= 97 or at P = 24-48
-                                        with n * e up to 32 MiB: 1 when it runs on
+                                        bandwidth-optimal, Ring and XOR plans), and on
+                                        long blocks the AR_FUSED_ROTATE defaults: 1
+                                        when it runs on
                                         flat columns (the rank-slot kernel, or the XOR
                                         group's kernel without the block) for batches of
                                         fewer than 2^32 - 64 columns                     */

@@ -93,6 +93,18 @@ constexpr int64_t kPackMaxLen = 64;
 constexpr int32_t kRotShiftedMinP = 97;
 constexpr int32_t kRotShiftedSmallMinP = 24, kRotShiftedSmallMaxP = 48;
 constexpr int64_t kRotShiftedSmallMaxBytes = int64_t(32) << 20;
+// Plans whose ranks all receive one result (bandwidth-optimal, the Ring)
+// take the rank-slot kernel on long blocks too where it splits (from
+// kFlatSplitMinP ranks: the reducing launch stores to rank 0, the flat
+// broadcast copies) and below kRotOneMaxBytes per rank instance.  Against
+// the block-tiled kernels (split from P = 32 at 64 MiB and from P = 64),
+// sums and max took 3-9% less time at P = 37 and 127 with 16-128 MB per
+// rank (the Ring at P = 127: 3-5%), within 1.7% either way at P = 64-100;
+// at 256 MB (P = 127) 0.7% more.  Unsplit, at P = 8-32, the two were
+// within 4% either way with no consistent sign (the gradient-sync shape,
+// P = 24 at 64 MB: 4% more), so those keep block tiles.
+constexpr int32_t kRotOneMinP = 33;
+constexpr int64_t kRotOneMaxBytes = int64_t(256) << 20;
 // Step launches whose blocks hold at most this many elements stream each
 // range's run of blocks as one flat space per rank (step_merged_kernel):
 // short blocks otherwise leave most lanes of the 1 KB block tiles idle.
@@ -831,8 +843,11 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
         shifted_sum && ((pl->s.P >= kRotShiftedMinP && pl->s.P % 2 == 1) ||
                         (pl->s.P >= kRotShiftedSmallMinP && pl->s.P <= kRotShiftedSmallMaxP &&
                          pl->s.n * 4 <= kRotShiftedSmallMaxBytes));
-    pl->fused_flat = kind && op_ok &&
-                     (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && (max_len <= kPackMaxLen || rot_shifted)));
+    const bool rot_one = (pl->fused_kind == kFusedRing || (pl->fused_kind == kFusedCol && pl->s.r == 0)) &&
+                         pl->s.P >= kRotOneMinP && pl->s.n * 4 < kRotOneMaxBytes;
+    pl->fused_flat =
+        kind && op_ok &&
+        (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && (max_len <= kPackMaxLen || rot_shifted || rot_one)));
   }
   const bool rank_slots = pl->fused_flat && pl->fused_kind != kFusedXor;
   const int32_t split_min =

@@ -506,19 +506,19 @@ static void broadcast_choice() {
   };
   const Case cases[] = {
       {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
-      {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream", 0},   // 256 MiB per rank over two instances
+      {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream", 1},   // rank slots below 256 MiB per instance: flat, regions
       {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 3, 5, 0, "broadcast", -1},          // gaps between instances
       {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 4, "broadcast", -1},          // a rank buffer off 16 bytes
       {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 128 MiB per rank: XCD regions
       {127, int64_t(1) << 24, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 64 MiB
       {127, (int64_t(1) << 24) - 1024, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
-      {127, int64_t(1) << 19, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 2 MiB per rank
-      {127, (int64_t(1) << 19) - 1024, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast", -1}, // just below 2 MiB
-      {64, int64_t(1) << 19, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
-      {100, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},   // below 104 ranks: interleaved
+      {127, int64_t(1) << 19, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},   // 2 MiB per rank: flat, interleaved
+      {127, (int64_t(1) << 19) - 1024, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
+      {64, int64_t(1) << 19, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
+      {100, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
       {104, int64_t(1) << 24, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
       {64, int64_t(1) << 24, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},     // blocks on the chunk grid: regions
-      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast", -1},
+      {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
       {64, int64_t(1) << 26, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
       {128, int64_t(1) << 26, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream", 0},                // flat columns, root rank 0
@@ -566,11 +566,11 @@ static void broadcast_order_override() {
   };
   const Case cases[] = {
       {127, int64_t(1) << 26, 1, "2", "broadcast_stream", 0}, {127, int64_t(1) << 26, 1, "3", "broadcast_stream", 1},
-      {127, int64_t(1) << 26, 1, "1", "broadcast_stream", 0}, {127, 127 * 1024 + 77, 1, "1", "broadcast_stream", 1},
+      {127, int64_t(1) << 26, 1, "1", "broadcast_stream", 0}, {127, 127 * 1024 + 77, 1, "1", "broadcast_stream", 0},
       {127, 127 * 1024 + 77, 1, "2", "broadcast_stream", 0},  {127, 127 * 1024 + 77, 1, "3", "broadcast_stream", 1},
       {127, 127 * 1024 + 77, 1, "0", "broadcast", -1},         {127, 2304, 8, "1", "broadcast_stream", 0},
       {127, 2304, 8, "3", "broadcast_stream", 1},              {48, 2304, 8, "2", "broadcast_stream", 0},
-      {127, 127 * 1024 + 77, 1, "7", "broadcast", -1},         // not a mode: the size rules
+      {127, 127 * 1024 + 77, 1, "7", "broadcast_stream", 0},   // not a mode: the default rules (flat columns)
   };
   for (const Case& c : cases) {
     setenv("AR_BCAST_STREAM", c.env, 1);

@@ -68,17 +68,21 @@ def test_captured_execute_replays_exactly(P, n, B, k, group, schedule, path):
     _capture_and_replay(P, n, B, k, group, schedule, path)
 
 
-@pytest.mark.parametrize("P,n,B,k,group", [
-    (127, 127 * 1024 + 76, 1, 14, "cyclic"),    # block tiles (destination-major by the override)
-    (127, 2304, 24, 14, "cyclic"),              # flat columns, rank 0 holds the results
-    (128, 2304, 16, 14, "xor"),
+@pytest.mark.parametrize("P,n,B,k,group,rotate", [
+    (127, 127 * 1024 + 76, 1, 14, "cyclic", "0"),   # block tiles (destination-major by the override)
+    (127, 127 * 1024 + 76, 1, 14, "cyclic", None),  # the default rank slots below 256 MiB
+    (127, 2304, 24, 14, "cyclic", None),            # flat columns, rank 0 holds the results
+    (128, 2304, 16, 14, "xor", None),
 ])
-def test_captured_split_with_the_destination_major_broadcast(P, n, B, k, group, monkeypatch):
+def test_captured_split_with_the_destination_major_broadcast(P, n, B, k, group, rotate, monkeypatch):
     """The reducing launch and the destination-major broadcast captured
     together: replays on fresh inputs equal the oracle."""
     monkeypatch.setenv("AR_BCAST_STREAM", "1")
+    if rotate is not None:
+        monkeypatch.setenv("AR_FUSED_ROTATE", rotate)
     st = ar.Plan(P, n, "float32", "sum", k, group=group).stats()
     assert st.fused_launches == 2 and st.fused_bcast_stream == 1
+    assert st.fused_flat == int(rotate is None)
     _capture_and_replay(P, n, B, k, group, "butterfly", ar.AR_PATH_FUSED)
 
 

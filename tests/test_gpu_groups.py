@@ -304,13 +304,18 @@ def test_single_rank_other_schedules():
         assert np.array_equal(X.cpu().numpy(), x)
 
 
+@pytest.mark.parametrize("layout", ["0", "default"])
 @pytest.mark.parametrize("P,k,schedule", [(48, 12, "butterfly"), (40, 78, "ring"), (33, 12, "butterfly")])
-def test_split_from_32_ranks_at_64_mib(P, k, schedule):
-    """Block-tiled one-result plans from P = 32 with 64 MiB rank buffers run
-    as a reducing launch plus the destination-major broadcast: the full-size
-    vector against the oracle on sampled columns, and the whole vector
-    against the step-wise path."""
+def test_split_from_32_ranks_at_64_mib(P, k, schedule, layout, monkeypatch):
+    """One-result plans from P = 32 with 64 MiB rank buffers run as a
+    reducing launch plus the destination-major broadcast, on block tiles
+    (AR_FUSED_ROTATE=0, split from 32 ranks at this size) and on the
+    default rank slots (split from 33): the full-size vector against the
+    oracle on sampled columns, and the whole vector against the step-wise
+    path."""
+    if layout == "0":
+        monkeypatch.setenv("AR_FUSED_ROTATE", "0")
     w = synth.WORKLOADS["gradsync"]
     st = ar.Plan(P, w["n"], "float32", "sum", k, path=ar.AR_PATH_FUSED, schedule=schedule).stats()
-    assert st.fused_launches == 2 and st.fused_bcast_stream == 1
+    assert st.fused_launches == 2 and st.fused_bcast_stream == 1 and st.fused_flat == int(layout == "default")
     full_size("split P=%d %s" % (P, schedule), P, w["n"], k, "cyclic", schedule, w["seed"], w["dist"])

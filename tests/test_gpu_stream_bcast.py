@@ -11,9 +11,11 @@ more, its chunks interleaved over the XCDs or in one contiguous region per
 XCD by shape.  A chunk across a block or instance boundary is copied as
 whole 16-byte groups, each element from its own root's load (the kernel for
 blocks off the 4 KB chunk grid), or element by element (the kernel for
-blocks on it, where only the tail takes that path).  These tests set
-AR_BCAST_STREAM (2: interleaved, 3: regions, 1: the default order) so that
-it runs at sizes the oracle checks whole, and compare both copies bit for
+blocks on it, where only the tail takes that path).  Below 256 MiB per rank the
+one-result plans take flat columns by default from P = 8 up; the tests run
+each case on block tiles too (AR_FUSED_ROTATE=0), which the defaults keep
+for larger buffers.  They set AR_BCAST_STREAM (2: interleaved, 3: regions,
+1: the default order) so that the copy runs at sizes the oracle checks whole, and compare both copies bit for
 bit with the oracle: sizes that span several 4 KB chunks per block, chunks
 across block and instance boundaries, and a ragged tail.
 """
@@ -72,22 +74,35 @@ CASES = [
 
 
 ORDERS = ["2", "3"]  # interleaved chunks, XCD regions
+LAYOUTS = ["0", "default"]  # block tiles (AR_FUSED_ROTATE=0), the default (flat columns from P = 8)
 
 
+def set_layout(layout, monkeypatch):
+    if layout == "default":
+        monkeypatch.delenv("AR_FUSED_ROTATE", raising=False)
+    else:
+        monkeypatch.setenv("AR_FUSED_ROTATE", layout)
+
+
+@pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("order", ORDERS)
 @pytest.mark.parametrize("P,n,k,group,schedule,dtype,op", CASES)
-def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op, order, monkeypatch):
+def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op, order, layout, monkeypatch):
     """16-byte aligned rows: the destination-major broadcast (the split
     forced, for P = 37)."""
     monkeypatch.setenv("AR_BCAST_STREAM", order)
     monkeypatch.setenv("AR_FUSED_SPLIT", "1")
+    set_layout(layout, monkeypatch)
     rng = np.random.default_rng(P * 7 + n)
     x = draw(rng, P, n, dtype)
     plan = ar.Plan(P, n, dtype, op, k, group=group, schedule=schedule)
     st = plan.stats()
     assert st.fused_launches == 2 and st.exec_path == ar.AR_PATH_FUSED and st.fused_bcast_stream == 1
+    if group == "cyclic":
+        assert st.fused_flat == int(layout == "default")
     big, views = aligned_rows(x)
-    note("stream broadcast P=%d n=%d k=%d %s/%s %s %s order %s" % (P, n, k, group, schedule, dtype, op, order))
+    note("stream broadcast P=%d n=%d k=%d %s/%s %s %s order %s layout %s flat %d"
+         % (P, n, k, group, schedule, dtype, op, order, layout, st.fused_flat))
     plan(views)
     torch.cuda.synchronize()
     got = big[:, :n].cpu().numpy()
@@ -97,19 +112,23 @@ def test_split_broadcast_aligned_rows(P, n, k, group, schedule, dtype, op, order
     plan.close()
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("order", ORDERS)
 @pytest.mark.parametrize("P,n,k", [(127, 127 * 1024 + 77, 14), (64, 64 * 1030 + 1, 12)])
-def test_split_broadcast_contiguous_batch(P, n, k, order, monkeypatch):
+def test_split_broadcast_contiguous_batch(P, n, k, order, layout, monkeypatch):
     """Three contiguous instances (stride n) in one buffer per rank: chunks
     that straddle an instance boundary take the last block of one instance
     and the first of the next."""
     monkeypatch.setenv("AR_BCAST_STREAM", order)
+    set_layout(layout, monkeypatch)
     B = 3
     rng = np.random.default_rng(P + k)
     x = draw(rng, P, B * n, "float32")
     big, views = aligned_rows(x)
     plan = ar.Plan(P, n, "float32", "sum", k)
-    note("stream broadcast batch P=%d n=%d B=%d k=%d order %s" % (P, n, B, k, order))
+    st = plan.stats()
+    assert st.fused_launches == 2 and st.fused_bcast_stream == 1 and st.fused_flat == int(layout == "default")
+    note("stream broadcast batch P=%d n=%d B=%d k=%d order %s layout %s" % (P, n, B, k, order, layout))
     plan.batched(views, B, n)
     torch.cuda.synchronize()
     got = big[:, :B * n].cpu().numpy().reshape(P, B, n)
@@ -121,8 +140,10 @@ def test_tiled_and_stream_broadcasts_agree(monkeypatch):
     """The same plan and input through both broadcasts: aligned rows
     (destination-major), one rank buffer 4 bytes off a 16-byte boundary and
     instances with gaps between them (both tiled); every result equals the
-    oracle's bits, and the gaps are left untouched."""
+    oracle's bits, and the gaps are left untouched.  Block tiles
+    (AR_FUSED_ROTATE=0), whose boundary chunks straddle two roots."""
     monkeypatch.setenv("AR_BCAST_STREAM", "1")
+    monkeypatch.setenv("AR_FUSED_ROTATE", "0")
     P, n, k = 127, 127 * 1024 + 501, 14
     rng = np.random.default_rng(2004)
     x = draw(rng, P, n, "float32")
@@ -190,16 +211,18 @@ def test_flat_split_broadcast_small_instances(order, monkeypatch):
     plan.close()
 
 
+@pytest.mark.parametrize("layout", LAYOUTS)
 @pytest.mark.parametrize("order", ORDERS)
 @pytest.mark.parametrize("P,k,group,schedule", [
     (2, 2, "cyclic", "butterfly"), (3, 4, "cyclic", "butterfly"), (5, 6, "cyclic", "butterfly"),
     (8, 6, "xor", "butterfly"), (16, 30, "cyclic", "ring"), (17, 10, "cyclic", "butterfly")])
-def test_split_forced_at_small_p(P, k, group, schedule, order, monkeypatch):
+def test_split_forced_at_small_p(P, k, group, schedule, order, layout, monkeypatch):
     """Few destinations: the split forced (AR_FUSED_SPLIT=1) with the
     destination-major copy, blocks of at least 1024 elements off the chunk
     grid, three contiguous instances and a ragged tail."""
     monkeypatch.setenv("AR_FUSED_SPLIT", "1")
     monkeypatch.setenv("AR_BCAST_STREAM", order)
+    set_layout(layout, monkeypatch)
     n, B = P * 1500 + 7, 3
     rng = np.random.default_rng(P * 31 + k)
     x = draw(rng, P, B * n, "float32")

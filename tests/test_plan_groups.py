@@ -184,24 +184,36 @@ def test_random_plans_reproduce_oracle(case):
     assert st_.bytes_pulled_total == st_.blocks_pulled_per_rank * n * 4
 
 
-@pytest.mark.parametrize("P,n,k,group,schedule,launches", [
-    (128, 128 * 18, 14, "xor", "butterfly", 2),      # Recursive Halving, flat columns: reduce, then broadcast
-    (64, 64 * 18, 12, "xor", "butterfly", 2),
-    (32, 32 * 18, 10, "xor", "butterfly", 1),        # below 64 ranks: one launch
-    (128, 128 * 18, 10, "xor", "butterfly", 1),      # hybrid: the ranks receive different results
-    (127, 127 * 18, 14, "cyclic", "butterfly", 2),   # rank slots, split
-    (127, 127 * 18, 252, "cyclic", "ring", 2),
-    (127, 127 * 18, 11, "cyclic", "butterfly", 1),   # shifted: the ranks receive different results
-    (37, 37 * 18, 12, "cyclic", "butterfly", 2),     # rank slots split from 33 ranks up
-    (32, 32 * 18, 10, "cyclic", "butterfly", 1),
-    (37, 37 * 100, 12, "cyclic", "butterfly", 1),    # block tiles split from 64 ranks up
-    (127, 127 * 100, 14, "cyclic", "butterfly", 2),  # blocks of 100: block tiles, split
-    (127, 127 * 100, 252, "cyclic", "ring", 2),
+@pytest.mark.parametrize("P,n,k,group,schedule,launches,flat", [
+    (128, 128 * 18, 14, "xor", "butterfly", 2, 1),      # Recursive Halving, flat columns: reduce, then broadcast
+    (64, 64 * 18, 12, "xor", "butterfly", 2, 1),
+    (32, 32 * 18, 10, "xor", "butterfly", 1, 1),        # below 64 ranks: one launch
+    (128, 128 * 18, 10, "xor", "butterfly", 1, 1),      # hybrid: the ranks receive different results
+    (127, 127 * 18, 14, "cyclic", "butterfly", 2, 1),   # rank slots, split
+    (127, 127 * 18, 252, "cyclic", "ring", 2, 1),
+    (127, 127 * 18, 11, "cyclic", "butterfly", 1, 1),   # shifted: the ranks receive different results
+    (37, 37 * 18, 12, "cyclic", "butterfly", 2, 1),     # rank slots split from 33 ranks up
+    (32, 32 * 18, 10, "cyclic", "butterfly", 1, 1),
+    (37, 37 * 100, 12, "cyclic", "butterfly", 2, 1),    # long blocks below 256 MiB: rank slots too
+    (127, 127 * 100, 14, "cyclic", "butterfly", 2, 1),
+    (127, 127 * 100, 252, "cyclic", "ring", 2, 1),
+    (4, 4 * 100, 4, "cyclic", "butterfly", 1, 0),       # unsplit, below 33 ranks: block tiles
+    (24, 1 << 24, 10, "cyclic", "butterfly", 1, 0),
+    (24, 1 << 24, 46, "cyclic", "ring", 1, 0),
+    (32, 1 << 24, 10, "cyclic", "butterfly", 2, 0),     # block tiles split from 32 ranks at 64 MiB
+    (33, 1 << 24, 12, "cyclic", "butterfly", 2, 1),
+    (127, 1 << 26, 14, "cyclic", "butterfly", 2, 0),    # 256 MiB per rank: block tiles, split
+    (37, 1 << 26, 12, "cyclic", "butterfly", 2, 0),     # block tiles split from 32 ranks at 64 MiB
+    (24, 1 << 26, 10, "cyclic", "butterfly", 1, 0),
+    (37, 1 << 22, 8, "cyclic", "butterfly", 1, 1),      # shifted sums at P = 24-48 up to 32 MiB: rank slots
+    (37, 1 << 24, 8, "cyclic", "butterfly", 1, 0),
+    (127, 1 << 26, 10, "cyclic", "butterfly", 1, 1),    # shifted sums at odd P >= 97: rank slots
+    (126, 1 << 26, 10, "cyclic", "butterfly", 1, 0),
 ])
-def test_default_split_of_one_result_plans(P, n, k, group, schedule, launches):
+def test_default_split_of_one_result_plans(P, n, k, group, schedule, launches, flat):
     st = ar.Plan(P, n, "float32", "sum", k, group=group, schedule=schedule).stats()
     assert st.fused_launches == launches
-    assert st.fused_flat == int(n // P <= 64)
+    assert st.fused_flat == flat
     assert st.hbm_bytes_fused == (2 * P + (launches == 2)) * n * 4
 
 

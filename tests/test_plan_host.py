@@ -107,23 +107,28 @@ def test_fused_path_for_every_plan_with_two_or_more_ranks():
     assert ei.value.status == ar.AR_ERR_UNSUPPORTED
 
 
-@pytest.mark.parametrize("P,n,k,group,want", [
-    (127, 1 << 26, 14, "cyclic", 1),          # split, 256 MiB rank buffers
-    (64, 1 << 26, 12, "cyclic", 1),
-    (128, 1 << 26, 14, "xor", 1),
-    (127, 1 << 25, 14, "cyclic", 1),          # 128 MiB rank buffers: one region of chunks per XCD
-    (127, 1 << 24, 14, "cyclic", 1),          # 64 MiB
-    (127, (1 << 24) - 1024, 14, "cyclic", 1),
-    (127, 1 << 19, 14, "cyclic", 1),          # 2 MiB
-    (127, (1 << 19) - 1024, 14, "cyclic", 0), # just below 2 MiB: the tiled broadcast
-    (127, 127 * 1024, 14, "cyclic", 0),
-    (127, 2304, 14, "cyclic", 1),             # short blocks on flat columns (results on rank 0)
-    (128, 2304, 14, "xor", 1),
-    (48, 2304, 12, "cyclic", 1),              # flat, any P
-    (127, 1 << 26, 10, "cyclic", 0),          # shifted: one launch, no broadcast
-    (37, 1 << 22, 12, "cyclic", 0),           # below the split's P
+@pytest.mark.parametrize("P,n,k,group,rotate,want", [
+    (127, 1 << 26, 14, "cyclic", None, 1),          # split, 256 MiB rank buffers: block tiles
+    (64, 1 << 26, 12, "cyclic", None, 1),
+    (128, 1 << 26, 14, "xor", None, 1),
+    (127, 1 << 25, 14, "cyclic", None, 1),          # below 256 MiB: rank slots (flat columns)
+    (127, 1 << 25, 14, "cyclic", "0", 1),           # block tiles, 128 MiB: one region of chunks per XCD
+    (127, 1 << 24, 14, "cyclic", "0", 1),           # 64 MiB
+    (127, (1 << 24) - 1024, 14, "cyclic", "0", 1),
+    (127, 1 << 19, 14, "cyclic", "0", 1),           # 2 MiB
+    (127, (1 << 19) - 1024, 14, "cyclic", "0", 0),  # just below 2 MiB: the tiled broadcast
+    (127, 127 * 1024, 14, "cyclic", "0", 0),
+    (127, (1 << 19) - 1024, 14, "cyclic", None, 1), # the same on rank slots: flat, any size
+    (127, 2304, 14, "cyclic", None, 1),             # short blocks on flat columns (results on rank 0)
+    (128, 2304, 14, "xor", None, 1),
+    (48, 2304, 12, "cyclic", None, 1),              # flat, any P
+    (127, 1 << 26, 10, "cyclic", None, 0),          # shifted: one launch, no broadcast
+    (37, 1 << 22, 12, "cyclic", "0", 0),            # block tiles below the split's P
+    (37, 1 << 22, 12, "cyclic", None, 1),           # rank slots split from 33 ranks
 ])
-def test_destination_major_broadcast_choice(P, n, k, group, want, monkeypatch):
+def test_destination_major_broadcast_choice(P, n, k, group, rotate, want, monkeypatch):
+    if rotate is not None:
+        monkeypatch.setenv("AR_FUSED_ROTATE", rotate)
     st = ar.Plan(P, n, "float32", "sum", k, group=group).stats()
     assert st.fused_bcast_stream == want
     assert st.fused_launches == (2 if want else st.fused_launches)
@@ -250,8 +255,11 @@ def test_plan_sizes_match_oracle_counts(P):
         # elements, the rank-slot kernel), from P = 64 up on block tiles
         assert split == (P >= 33 and k == 2 * ceil_log2(P))
         assert st.fused_flat == int(P >= 2 and k > ceil_log2(P))
+        # blocks of 100 elements: the rank-slot kernel, split, from P = 33 up; block tiles below
         big = ar.Plan(P, 100 * P + 3, "float32", "sum", k).stats()
-        assert (big.fused_launches == 2) == (P >= 64 and k == 2 * ceil_log2(P))
+        assert (big.fused_launches == 2) == (P >= 33 and k == 2 * ceil_log2(P))
+        if k == 2 * ceil_log2(P) and P > 1:
+            assert big.fused_flat == int(P >= 33)
         assert st.hbm_bytes_fused == ((2 * P + split) * st.n * 4 if P > 1 else 0)
         # per-launch pulls equal the oracle's per-step pulls
         launches = [l for l in plan.launches() if l[0] != 2]
