@@ -15,6 +15,9 @@ constexpr int kMaxRanges = 8;    // placement ranges per launch
 // it -- bytes, tiles, products with P -- fits in 64-bit arithmetic.
 constexpr int64_t kMaxRankElems = int64_t(1) << 46;
 constexpr int kFusedMaxP = 16;   // largest P of the register-resident fused kernel
+// P range in which the rank-slot kernel also takes shifted max plans (the
+// library instantiates those only there)
+constexpr int kRotMaxShiftedMinP = 24, kRotMaxShiftedMaxP = 48;
 // Size of the device-resident scratch of ar_execute_noalloc (noalloc.hip):
 // the X and Y buffers of a step-wise plan with r > 0 take 2 * P rank
 // regions of the call's extent rounded up to 64 elements.

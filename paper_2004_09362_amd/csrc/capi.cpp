@@ -833,16 +833,19 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
     const int64_t max_len = pl->s.P > 0 ? pl->s.n / pl->s.P + (pl->s.n % pl->s.P ? 1 : 0) : 0;
     const bool kind = pl->fused_kind == kFusedRing || pl->fused_kind == kFusedXor ||
                       (pl->fused_kind == kFusedCol && pl->s.r < pl->s.L);
-    // max: the rank-slot kernel's bandwidth-optimal fold and Ring (its
-    // shifted max plans keep packed tiles, saving their instantiations), and
-    // the XOR group, whose flat kernel then takes each lane's block
+    // max: the rank-slot kernel's bandwidth-optimal fold and Ring, its
+    // shifted plans at P = kRotMaxShiftedMinP-kRotMaxShiftedMaxP (elsewhere
+    // they keep block or packed tiles, saving their instantiations), and the
+    // XOR group, whose flat kernel then takes each lane's block
+    const bool max_mid_p = pl->s.P >= ar::kRotMaxShiftedMinP && pl->s.P <= ar::kRotMaxShiftedMaxP;
     const bool op_ok = pl->op == AR_SUM || pl->fused_kind == kFusedRing || pl->fused_kind == kFusedXor ||
-                       (pl->fused_kind == kFusedCol && pl->s.r == 0);
-    const bool shifted_sum = pl->fused_kind == kFusedCol && pl->s.r > 0 && pl->op == AR_SUM;
+                       (pl->fused_kind == kFusedCol && (pl->s.r == 0 || max_mid_p));
+    const bool shifted = pl->fused_kind == kFusedCol && pl->s.r > 0;
+    const bool small_p = pl->s.P >= kRotShiftedSmallMinP && pl->s.P <= kRotShiftedSmallMaxP &&
+                         pl->s.n * 4 <= kRotShiftedSmallMaxBytes;
     const bool rot_shifted =
-        shifted_sum && ((pl->s.P >= kRotShiftedMinP && pl->s.P % 2 == 1) ||
-                        (pl->s.P >= kRotShiftedSmallMinP && pl->s.P <= kRotShiftedSmallMaxP &&
-                         pl->s.n * 4 <= kRotShiftedSmallMaxBytes));
+        shifted && ((pl->op == AR_SUM && pl->s.P >= kRotShiftedMinP && pl->s.P % 2 == 1) ||
+                    (small_p && (pl->op == AR_SUM || max_mid_p)));
     const bool rot_one = (pl->fused_kind == kFusedRing || (pl->fused_kind == kFusedCol && pl->s.r == 0)) &&
                          pl->s.P >= kRotOneMinP && pl->s.n * 4 < kRotOneMaxBytes;
     pl->fused_flat =

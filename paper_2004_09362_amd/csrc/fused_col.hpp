@@ -339,16 +339,20 @@ int launch_rot_rr(const ColArgs& a, int grid, hipStream_t s) {
 }
 
 // Sums at every r; max (op 1) for the bandwidth-optimal fold and the Ring,
-// whose ranks all receive one result.  Shifted max plans with short blocks
-// keep the packed tiles, which saves most of the max instantiations.
+// whose ranks all receive one result, and at every r for P in
+// [kRotMaxShiftedMinP, kRotMaxShiftedMaxP].  Elsewhere shifted max plans
+// keep the block or packed tiles, which saves most of the max
+// instantiations.
 template <int P>
 int launch_fused_rot(const ColArgs& a, int dtype, int op, bool ring, int grid, void* stream) {
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const dim3 g(grid), blk(kBlock);
-  if (op == 1) {  // max: the bandwidth-optimal fold and the Ring only
+  if (op == 1) {
     if (ring) {
       if (dtype == 0) hipLaunchKernelGGL((fused_rot_kernel<P, -1, int32_t, 1>), g, blk, a.lds, s, a);
       else hipLaunchKernelGGL((fused_rot_kernel<P, -1, float, 1>), g, blk, a.lds, s, a);
+    } else if constexpr (P >= kRotMaxShiftedMinP && P <= kRotMaxShiftedMaxP) {
+      return dtype == 0 ? launch_rot_rr<P, 0, int32_t, 1>(a, grid, s) : launch_rot_rr<P, 0, float, 1>(a, grid, s);
     } else {
       if (a.r != 0) return int(hipErrorInvalidValue);
       if (dtype == 0) hipLaunchKernelGGL((fused_rot_kernel<P, 0, int32_t, 1>), g, blk, a.lds, s, a);

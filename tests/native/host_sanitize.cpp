@@ -196,7 +196,8 @@ int launch_fused_mid(const ColArgs& a, int, int, bool, int grid, void*) {
 template <int P>
 int launch_fused_rot(const ColArgs& a, int, int op, bool, int grid, void*) {
   check_col(a, P, "rot");
-  if (!a.flat || (op != 0 && a.r != 0)) fake::problem("rank-slot kernel off flat columns, or a shifted max", P);
+  if (!a.flat || (op != 0 && a.r != 0 && (P < kRotMaxShiftedMinP || P > kRotMaxShiftedMaxP)))
+    fake::problem("rank-slot kernel off flat columns, or a shifted max outside its P range", P);
   return record("fused_rot", P, grid, a.total_tiles);
 }
 

@@ -29,7 +29,7 @@ from test_gpu_parity import DEV, bits, note
 
 pytestmark = pytest.mark.gpu
 
-# P, n, batch, instance stride, k, group, schedule, op ("isum": int32 sum)
+# P, n, batch, instance stride, k, group, schedule, op ("isum", "imax": int32 sum, max)
 CASES = [
     (5, 23, 37, 29, 6, "cyclic", "butterfly", "sum"),        # bandwidth-optimal, blocks of 4-5, 12 per wave
     (24, 100, 50, 104, 10, "cyclic", "butterfly", "sum"),    # bandwidth-optimal, blocks of 4-5
@@ -65,6 +65,9 @@ CASES = [
     (32, 200, 13, 200, 10, "xor", "butterfly", "max"),       # XOR max, flat: each lane's block orders the pairs
     (32, 200, 13, 200, 7, "xor", "butterfly", "max"),        # XOR max, hybrid r = 3
     (128, 2000, 5, 2003, 14, "xor", "butterfly", "max"),     # XOR max, flat, split
+    (37, 300, 20, 301, 9, "cyclic", "butterfly", "max"),     # shifted max at P = 24-48: rank slots
+    (48, 4000, 3, 4003, 8, "cyclic", "butterfly", "imax"),   # int32 shifted max, blocks of 83-84
+    (24, 1700, 4, 1703, 9, "cyclic", "butterfly", "imax"),   # r = 4 = L - 1
 ]
 
 SETTINGS = [  # AR_FUSED_ROTATE, AR_FUSED_PACKED (None: unset, the default)
@@ -77,14 +80,14 @@ def test_packed_and_blocked_tiles_agree_with_oracle(P, n, B, stride, k, group, s
     if not torch.cuda.is_available():
         pytest.fail("GPU tests need a GPU")
     rng = np.random.default_rng(P * 1000 + n + k)
-    dtype = "int32" if op == "isum" else "float32"
-    if op == "isum":
-        op = "sum"
+    dtype = "int32" if op in ("isum", "imax") else "float32"
+    if dtype == "int32":
+        op = op[1:]
         x = rng.integers(-2**31, 2**31, size=(P, B, stride), dtype=np.int64).astype(np.int32)
     else:
         x = rng.normal(size=(P, B, stride)).astype(np.float32)
     want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, op, group=group, schedule=schedule)
-    if dtype == "int32":  # wrapping sum, exact whatever the order
+    if dtype == "int32" and op == "sum":  # wrapping sum, exact whatever the order
         s64 = x[:, :, :n].astype(np.int64).sum(axis=0)
         assert np.array_equal(want, np.broadcast_to(((s64 + 2**31) % 2**32 - 2**31).astype(np.int32), want.shape))
     if op == "max":
@@ -146,9 +149,9 @@ def test_random_batches_with_the_split_forced_either_way(P, n, B, stride, k, gro
     if not torch.cuda.is_available():
         pytest.fail("GPU tests need a GPU")
     rng = np.random.default_rng(P * 11 + n + k)
-    dtype = "int32" if op == "isum" else "float32"
-    if op == "isum":
-        op = "sum"
+    dtype = "int32" if op in ("isum", "imax") else "float32"
+    if dtype == "int32":
+        op = op[1:]
         x = rng.integers(-2**31, 2**31, size=(P, B, stride), dtype=np.int64).astype(np.int32)
     else:
         x = rng.normal(size=(P, B, stride)).astype(np.float32)
@@ -170,6 +173,7 @@ def test_random_batches_with_the_split_forced_either_way(P, n, B, stride, k, gro
 @pytest.mark.parametrize("P,n,B,k,group,schedule", [
     (32, 200, 13, 10, "xor", "butterfly"), (32, 200, 13, 7, "xor", "butterfly"), (128, 2000, 5, 14, "xor", "butterfly"),
     (24, 100, 17, 10, "cyclic", "butterfly"), (24, 100, 17, 46, "cyclic", "ring"), (127, 1000, 9, 14, "cyclic", "butterfly"),
+    (37, 300, 9, 8, "cyclic", "butterfly"), (48, 4000, 3, 9, "cyclic", "butterfly"),  # shifted max in rank slots
 ])
 def test_max_of_signed_zeros_follows_the_schedules_operand_order(P, n, B, k, group, schedule, monkeypatch):
     """Inputs of +0.0 and -0.0 only: a max of two zeros returns the kept
@@ -215,9 +219,9 @@ def test_stepwise_merged_runs_agree_with_oracle(P, n, B, stride, k, group, sched
     if not torch.cuda.is_available():
         pytest.fail("GPU tests need a GPU")
     rng = np.random.default_rng(P * 7 + n + k)
-    dtype = "int32" if op == "isum" else "float32"
-    if op == "isum":
-        op = "sum"
+    dtype = "int32" if op in ("isum", "imax") else "float32"
+    if dtype == "int32":
+        op = op[1:]
         x = rng.integers(-2**31, 2**31, size=(P, B, stride), dtype=np.int64).astype(np.int32)
     else:
         x = rng.normal(size=(P, B, stride)).astype(np.float32)

@@ -217,9 +217,26 @@ def test_default_split_of_one_result_plans(P, n, k, group, schedule, launches, f
     assert st.hbm_bytes_fused == (2 * P + (launches == 2)) * n * 4
 
 
+@pytest.mark.parametrize("P,n,k,flat", [
+    (37, 1 << 22, 8, 1),       # shifted max at P = 24-48 up to 32 MiB: rank slots, as for sums
+    (37, 1 << 22, 11, 1),
+    (24, 1 << 21, 7, 1),
+    (37, 1 << 24, 8, 0),       # 64 MiB: block tiles
+    (49, 1 << 22, 8, 0),       # outside the P range of the shifted max instantiations
+    (127, 1 << 26, 10, 0),     # shifted sums there take rank slots, max keeps block tiles
+    (37, 1 << 22, 12, 1),      # bandwidth-optimal: rank slots from 33 ranks below 256 MiB
+])
+def test_default_layout_of_max_plans(P, n, k, flat):
+    for dtype in ("float32", "int32"):
+        st = ar.Plan(P, n, dtype, "max", k).stats()
+        assert st.fused_flat == flat, (P, n, k, dtype)
+
+
 @pytest.mark.parametrize("P,k,group,schedule,flat", [
     (24, 10, "cyclic", "butterfly", 1), (127, 14, "cyclic", "butterfly", 1), (24, 46, "cyclic", "ring", 1),
-    (24, 7, "cyclic", "butterfly", 0), (32, 10, "xor", "butterfly", 1), (32, 7, "xor", "butterfly", 1),
+    (24, 7, "cyclic", "butterfly", 1), (48, 8, "cyclic", "butterfly", 1),  # shifted max at P = 24-48: rank slots
+    (23, 7, "cyclic", "butterfly", 0), (49, 8, "cyclic", "butterfly", 0), (127, 10, "cyclic", "butterfly", 0),
+    (32, 10, "xor", "butterfly", 1), (32, 7, "xor", "butterfly", 1),
     (12, 4, "cyclic", "butterfly", 0),
 ])
 def test_max_with_short_blocks_on_flat_columns(P, k, group, schedule, flat):
