@@ -17,7 +17,10 @@ rank-slot kernel that rotates each lane's column by its block, the XOR
 group's plans with the block left out (it only orders the operands of a
 halving pair, which a sum does not see).  It is checked forced on and off, with
 either tiling, on blocks of every length up to 70 elements (longer blocks
-leave most stages of the rotation network unused by a whole wave).
+leave most stages of the rotation network unused by a whole wave), and on
+seeded random plans with long blocks (65 to about 600 elements), where the
+defaults take the rank-slot kernel for some shapes and block tiles for the
+rest.
 """
 import numpy as np
 import pytest
@@ -138,6 +141,60 @@ def test_random_short_block_batches(P, n, B, stride, k, group, schedule, op, mon
     elements), batch sizes and strides, under the default and with flat
     columns forced on and off: the oracle's bits every time."""
     test_packed_and_blocked_tiles_agree_with_oracle(P, n, B, stride, k, group, schedule, op, monkeypatch)
+
+
+def _random_long_cases(count, seed):
+    """Like _random_cases, with blocks of 65 to about 600 elements."""
+    rng = np.random.default_rng(seed)
+    out = []
+    while len(out) < count:
+        group = ["cyclic", "cyclic", "xor", "ring"][rng.integers(4)]
+        P = int(2 ** rng.integers(1, 8)) if group == "xor" else int(rng.integers(2, 129))
+        L = max(0, (P - 1).bit_length())
+        if group == "ring":
+            k, schedule, group = 2 * (P - 1), "ring", "cyclic"
+        else:
+            k, schedule = int(rng.integers(L, 2 * L + 1)), "butterfly"
+        n = P * int(rng.integers(65, 600)) + int(rng.integers(0, P))
+        B = int(rng.integers(1, 4))
+        stride = n + int(rng.integers(0, 5))
+        op = ["sum", "isum", "max", "imax"][rng.integers(4)]
+        out.append((P, n, B, stride, k, group, schedule, op))
+    return out
+
+
+@pytest.mark.parametrize("P,n,B,stride,k,group,schedule,op", _random_long_cases(24, 20261205))
+def test_random_long_block_batches(P, n, B, stride, k, group, schedule, op, monkeypatch):
+    """Seeded random plans with long blocks (65 to about 600 elements),
+    under the default (rank slots where the size rules pick them, block
+    tiles elsewhere) and with flat columns forced on and off: the oracle's
+    bits every time, gaps untouched."""
+    if not torch.cuda.is_available():
+        pytest.fail("GPU tests need a GPU")
+    rng = np.random.default_rng(P * 13 + n + k)
+    dtype = "int32" if op in ("isum", "imax") else "float32"
+    if dtype == "int32":
+        op = op[1:]
+        x = rng.integers(-2**31, 2**31, size=(P, B, stride), dtype=np.int64).astype(np.int32)
+    else:
+        x = rng.normal(size=(P, B, stride)).astype(np.float32)
+    want = oracle.allreduce_batched(np.ascontiguousarray(x[:, :, :n]), k, op, group=group, schedule=schedule)
+    for rotate in (None, "0", "1"):
+        if rotate is None:
+            monkeypatch.delenv("AR_FUSED_ROTATE", raising=False)
+        else:
+            monkeypatch.setenv("AR_FUSED_ROTATE", rotate)
+        plan = ar.Plan(P, n, dtype, op, k, path=ar.AR_PATH_FUSED, group=group, schedule=schedule)
+        st = plan.stats()
+        note("long blocks rotate=%s %s/%s P=%d n=%d B=%d k=%d %s %s: flat %d, launches %d"
+             % (rotate, group, schedule, P, n, B, k, dtype, op, st.fused_flat, st.fused_launches))
+        X = torch.from_numpy(x).to(DEV)
+        plan.batched([X[i] for i in range(P)], B, stride)
+        torch.cuda.synchronize()
+        got = X.cpu().numpy()
+        plan.close()
+        assert np.array_equal(bits(got[:, :, :n]), bits(want)), rotate
+        assert np.array_equal(bits(got[:, :, n:]), bits(x[:, :, n:])), rotate
 
 
 @pytest.mark.parametrize("P,n,B,stride,k,group,schedule,op", _random_cases(24, 20261204))
