@@ -89,7 +89,9 @@ constexpr int64_t kPackMaxLen = 64;
 // kRotShiftedSmallMaxBytes per rank: 1-5% less time at P = 24, 33, 34, 37,
 // 47 and 48 with 8-32 MB per rank (the prime_sweep shape, P = 37 at 16 MB:
 // 4-5% at k = 7-11), 1-10% more at 64 MB; at P = 64-93 within 2.4% either
-// way up to 32 MB.
+// way up to 32 MB.  Shifted max plans take this second rule as well (their
+// rank-slot kernels exist at P = 24-48 only): 4-7% less time at P = 37 and
+// 48 with 16 MB per rank, 2.6% more at P = 24 with 32 MB.
 constexpr int32_t kRotShiftedMinP = 97;
 constexpr int32_t kRotShiftedSmallMinP = 24, kRotShiftedSmallMaxP = 48;
 constexpr int64_t kRotShiftedSmallMaxBytes = int64_t(32) << 20;
