@@ -115,7 +115,7 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   default: the size rules given there),
  *                                   its chunks ordered by the default rule
  *                                   (1: one contiguous region of each slice
- *                                   per XCD on flat columns from 16 MiB per
+ *                                   per XCD on flat columns above 16 MiB per
  *                                   rank, on blocks that all start on the
  *                                   4 KB chunk grid, and on other blocks
  *                                   for P >= 104 below 256 MiB per rank;

@@ -55,9 +55,11 @@ constexpr int32_t kBcastStreamMinP = 96;
 // against the tiled copy (rank rows back to back), it took 6-24% less time
 // on block tiles at P = 64-128 and 2-256 MB per rank (5.7-7.2 TB/s against
 // 5.0-6.2), and 6-21% less on flat columns at P = 37-128 and 4.5-72 MB per
-// rank.  Its chunk order: XCD regions on flat columns from
-// kBcastFlatRegionMinBytes per rank (interleaved below, where short slices
-// left XCDs idle; within 2% either way above), and on block tiles whose
+// rank.  Its chunk order: XCD regions on flat columns above
+// kBcastFlatInterleaveMaxBytes per rank (interleaved up to it, where short
+// slices left XCDs idle, and at exactly 16 MiB, two full slices, 1-5% less
+// time than regions at P = 37-127; regions 1-4% less at 20, 28 and 32 MiB,
+// within 2% either way at 24 MiB and above), and on block tiles whose
 // blocks all start on the chunk grid (P = 64 and 128 from 32 MB per rank:
 // 5-55% less time than interleaved; P = 64 below: up to 7% more); with
 // straddling chunks interleaved below kBcastRegionMinP ranks (P = 100:
@@ -66,7 +68,7 @@ constexpr int32_t kBcastStreamMinP = 96;
 // chunks read their sources from L2 no more (P = 127 below 256 MB per rank:
 // 1.1-2.0x the time of regions).
 constexpr int64_t kBcastStreamMinBytes = int64_t(2) << 20;
-constexpr int64_t kBcastFlatRegionMinBytes = int64_t(16) << 20;
+constexpr int64_t kBcastFlatInterleaveMaxBytes = int64_t(16) << 20;
 constexpr int64_t kBcastInterleaveMinBytes = int64_t(256) << 20;
 constexpr int32_t kBcastRegionMinP = 104;
 // Blocks of at most this many elements (many small instances) are packed:
@@ -159,7 +161,7 @@ struct ar_plan {
   // AR_BCAST_STREAM = 0|1|2|3 (the broadcast tiled by block / destination by
   // destination wherever the call allows it, with the chunk order by size,
   // interleaved, or in XCD regions; default by the size rules at
-  // kBcastStreamMinBytes, kBcastFlatRegionMinBytes, kBcastInterleaveMinBytes
+  // kBcastStreamMinBytes, kBcastFlatInterleaveMaxBytes, kBcastInterleaveMinBytes
   // and kBcastRegionMinP),
   // AR_FUSED_PACKED = 0|1 (column tiles of one block of one instance / of
   // several instances, for blocks of up to 64 elements; default: packed for
@@ -645,7 +647,7 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
     const bool straddle = !a.flat && (s.n % s.P != 0 || (s.n / s.P) % ar::kStreamChunk != 0);
     bool regions;
     if (pl->bcast_stream_mode == 2 || pl->bcast_stream_mode == 3) regions = pl->bcast_stream_mode == 3;
-    else if (a.flat) regions = span >= kBcastFlatRegionMinBytes;
+    else if (a.flat) regions = span > kBcastFlatInterleaveMaxBytes;
     else regions = !straddle || (s.P >= kBcastRegionMinP && span < kBcastInterleaveMinBytes);
     if (want_stream && stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, regions, device, &sa)) {
       const uint32_t sgrid = (sa.chunks + sa.cdiv.d - 1) / sa.cdiv.d * sa.sdiv.d;

@@ -492,9 +492,10 @@ static void exercise(int P, int64_t n, int k, int group, int sched, int dtype, i
 }
 
 // Which broadcast a split plan takes: the destination-major one for
-// contiguous instances in 16-byte aligned buffers, on flat columns from 64
-// ranks or on blocks of at least kStreamChunk elements in rank spans of at
-// least 256 MiB; the tiled one otherwise.
+// contiguous instances in 16-byte aligned buffers, on flat columns at any P
+// or on blocks of at least kStreamChunk elements in rank spans of at least
+// 2 MiB; the tiled one otherwise.  On flat columns its chunks go in XCD
+// regions above 16 MiB per rank, interleaved up to it.
 static void broadcast_choice() {
   struct Case {
     int P;
@@ -508,6 +509,8 @@ static void broadcast_choice() {
   const Case cases[] = {
       {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
       {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream", 1},   // rank slots below 256 MiB per instance: flat, regions
+      {37, int64_t(1) << 22, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},    // flat, exactly 16 MiB: interleaved
+      {37, (int64_t(1) << 22) + 1024, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},  // just above: regions
       {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 3, 5, 0, "broadcast", -1},          // gaps between instances
       {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 4, "broadcast", -1},          // a rank buffer off 16 bytes
       {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},   // 128 MiB per rank: XCD regions
