@@ -117,7 +117,8 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   (1: one contiguous region of each slice
  *                                   per XCD on flat columns above 16 MiB per
  *                                   rank, on blocks that all start on the
- *                                   4 KB chunk grid, and on other blocks
+ *                                   4 KB chunk grid for P >= 104 or from
+ *                                   32 MiB per rank, and on other blocks
  *                                   for P >= 104 below 256 MiB per rank;
  *                                   else interleaved over the XCDs), always
  *                                   interleaved (2), or always in regions

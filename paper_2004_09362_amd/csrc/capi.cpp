@@ -60,8 +60,10 @@ constexpr int32_t kBcastStreamMinP = 96;
 // slices left XCDs idle, and at exactly 16 MiB, two full slices, 1-5% less
 // time than regions at P = 37-127; regions 1-4% less at 20, 28 and 32 MiB,
 // within 2% either way at 24 MiB and above), and on block tiles whose
-// blocks all start on the chunk grid (P = 64 and 128 from 32 MB per rank:
-// 5-55% less time than interleaved; P = 64 below: up to 7% more); with
+// blocks all start on the chunk grid from kBcastRegionMinP ranks or from
+// kBcastAlignedRegionMinBytes per rank (P = 128 at 8-32 MiB: 35-38% less
+// time than interleaved; P = 64 at 32-256 MiB and P = 32 at 64 MiB: 3-5%
+// less; P = 16-64 at 8-16 MiB: 1-8% more, so interleaved there); with
 // straddling chunks interleaved below kBcastRegionMinP ranks (P = 100:
 // 5-10% less time than regions) or from kBcastInterleaveMinBytes per rank
 // (P = 127 at 256 MB: 5%), and regions otherwise, where the interleaved
@@ -70,6 +72,7 @@ constexpr int32_t kBcastStreamMinP = 96;
 constexpr int64_t kBcastStreamMinBytes = int64_t(2) << 20;
 constexpr int64_t kBcastFlatInterleaveMaxBytes = int64_t(16) << 20;
 constexpr int64_t kBcastInterleaveMinBytes = int64_t(256) << 20;
+constexpr int64_t kBcastAlignedRegionMinBytes = int64_t(32) << 20;
 constexpr int32_t kBcastRegionMinP = 104;
 // Blocks of at most this many elements (many small instances) are packed:
 // a column-fused wave takes one block of 64 / max_len instances instead of 64
@@ -161,8 +164,8 @@ struct ar_plan {
   // AR_BCAST_STREAM = 0|1|2|3 (the broadcast tiled by block / destination by
   // destination wherever the call allows it, with the chunk order by size,
   // interleaved, or in XCD regions; default by the size rules at
-  // kBcastStreamMinBytes, kBcastFlatInterleaveMaxBytes, kBcastInterleaveMinBytes
-  // and kBcastRegionMinP),
+  // kBcastStreamMinBytes, kBcastFlatInterleaveMaxBytes, kBcastInterleaveMinBytes,
+  // kBcastAlignedRegionMinBytes and kBcastRegionMinP),
   // AR_FUSED_PACKED = 0|1 (column tiles of one block of one instance / of
   // several instances, for blocks of up to 64 elements; default: packed for
   // batches whose blocks hold up to kPackMaxLen elements), AR_FUSED_ROTATE =
@@ -648,7 +651,8 @@ ar_status run_fused_col(ar_plan* pl, void* const* bufs, int64_t batch, int64_t s
     bool regions;
     if (pl->bcast_stream_mode == 2 || pl->bcast_stream_mode == 3) regions = pl->bcast_stream_mode == 3;
     else if (a.flat) regions = span > kBcastFlatInterleaveMaxBytes;
-    else regions = !straddle || (s.P >= kBcastRegionMinP && span < kBcastInterleaveMinBytes);
+    else if (!straddle) regions = s.P >= kBcastRegionMinP || span >= kBcastAlignedRegionMinBytes;
+    else regions = s.P >= kBcastRegionMinP && span < kBcastInterleaveMinBytes;
     if (want_stream && stream_bcast_args(pl, bufs, batch, stride, a.flat != 0, regions, device, &sa)) {
       const uint32_t sgrid = (sa.chunks + sa.cdiv.d - 1) / sa.cdiv.d * sa.sdiv.d;
       // the destination-major copy: nontemporal at any P (launches of

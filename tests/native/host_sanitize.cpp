@@ -525,6 +525,10 @@ static void broadcast_choice() {
       {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
       {64, int64_t(1) << 26, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
       {128, int64_t(1) << 26, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},
+      {128, int64_t(1) << 21, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},      // aligned blocks, P >= 104: regions
+      {64, int64_t(1) << 22, 12, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 0},       // aligned, 16 MiB: interleaved
+      {64, int64_t(1) << 23, 12, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},       // aligned, 32 MiB: regions
+      {32, int64_t(1) << 24, 10, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},       // gradient-sync shape, 64 MiB
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream", 0},                // flat columns, root rank 0
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 3, 0, "broadcast", -1},
       {128, 2304, 14, AR_GROUP_XOR, 4, 0, 0, "broadcast_stream", 0},
