@@ -111,6 +111,11 @@ constexpr int64_t kRotShiftedSmallMaxBytes = int64_t(32) << 20;
 // within 4% either way with no consistent sign (the gradient-sync shape,
 // P = 24 at 64 MB: 4% more), so those keep block tiles.
 constexpr int32_t kRotOneMinP = 33;
+// The XOR group's sums, whose flat kernel leaves the block out, run on flat
+// columns on long blocks as well (Recursive Halving and the hybrids; not
+// Recursive Doubling, r = L, where block tiles were 1% faster at P = 32):
+// 1-7% less time at P = 8-128 with 16-64 MB per rank (P = 32 hybrids: 4%;
+// P = 128 at 16 MB, split: 7%), the same or better at every shape measured.
 constexpr int64_t kRotOneMaxBytes = int64_t(256) << 20;
 // Step launches whose blocks hold at most this many elements stream each
 // range's run of blocks as one flat space per rank (step_merged_kernel):
@@ -856,9 +861,11 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
                     (small_p && (pl->op == AR_SUM || max_mid_p)));
     const bool rot_one = (pl->fused_kind == kFusedRing || (pl->fused_kind == kFusedCol && pl->s.r == 0)) &&
                          pl->s.P >= kRotOneMinP && pl->s.n * 4 < kRotOneMaxBytes;
+    const bool xor_long = pl->fused_kind == kFusedXor && pl->op == AR_SUM && pl->s.r < pl->s.L;
     pl->fused_flat =
         kind && op_ok &&
-        (pl->rotate_mode == 1 || (pl->rotate_mode < 0 && (max_len <= kPackMaxLen || rot_shifted || rot_one)));
+        (pl->rotate_mode == 1 ||
+         (pl->rotate_mode < 0 && (max_len <= kPackMaxLen || rot_shifted || rot_one || xor_long)));
   }
   const bool rank_slots = pl->fused_flat && pl->fused_kind != kFusedXor;
   const int32_t split_min =

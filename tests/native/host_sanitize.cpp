@@ -496,17 +496,20 @@ static void exercise(int P, int64_t n, int k, int group, int sched, int dtype, i
 // or on blocks of at least kStreamChunk elements in rank spans of at least
 // 2 MiB; the tiled one otherwise.  On flat columns its chunks go in XCD
 // regions above 16 MiB per rank, interleaved up to it.
+struct BcastCase {
+  int P;
+  int64_t n;
+  int k, group, batch;
+  int64_t stride_extra;
+  uintptr_t misalign;
+  const char* expect;
+  int regions;  // the destination-major copy's chunk order: 1 XCD regions, 0 interleaved, -1 tiled copy
+};
+
+static void check_broadcast_case(const BcastCase& c);
+
 static void broadcast_choice() {
-  struct Case {
-    int P;
-    int64_t n;
-    int k, group, batch;
-    int64_t stride_extra;
-    uintptr_t misalign;
-    const char* expect;
-    int regions;  // the destination-major copy's chunk order: 1 XCD regions, 0 interleaved, -1 tiled copy
-  };
-  const Case cases[] = {
+  const BcastCase cases[] = {
       {127, int64_t(1) << 26, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
       {127, int64_t(1) << 25, 14, AR_GROUP_CYCLIC, 2, 0, 0, "broadcast_stream", 1},   // rank slots below 256 MiB per instance: flat, regions
       {37, int64_t(1) << 22, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},    // flat, exactly 16 MiB: interleaved
@@ -525,9 +528,9 @@ static void broadcast_choice() {
       {127, 1024 * 127 + 333, 14, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},
       {64, int64_t(1) << 26, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},
       {128, int64_t(1) << 26, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},
-      {128, int64_t(1) << 21, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},      // aligned blocks, P >= 104: regions
-      {64, int64_t(1) << 22, 12, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 0},       // aligned, 16 MiB: interleaved
-      {64, int64_t(1) << 23, 12, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},       // aligned, 32 MiB: regions
+      {128, int64_t(1) << 21, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 0},      // XOR sums on flat columns: 8 MiB
+      {64, int64_t(1) << 22, 12, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 0},       // 16 MiB: interleaved
+      {64, int64_t(1) << 23, 12, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},       // 32 MiB: regions
       {32, int64_t(1) << 24, 10, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},       // gradient-sync shape, 64 MiB
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 0, 0, "broadcast_stream", 0},                // flat columns, root rank 0
       {127, 2304, 14, AR_GROUP_CYCLIC, 8, 3, 0, "broadcast", -1},
@@ -537,26 +540,46 @@ static void broadcast_choice() {
       {127, 2304, 14, AR_GROUP_CYCLIC, 60000, 0, 0, "broadcast", -1},                   // grid above 2^32 work-items
       {127, 2304, 14, AR_GROUP_CYCLIC, 56000, 0, 0, "broadcast_stream", 1},            // just below it
   };
-  for (const Case& c : cases) {
-    ar_plan* pl = nullptr;
-    EXPECT(ar_plan_create_ex(c.P, c.n, AR_FLOAT32, AR_SUM, c.k, ar_group(c.group), AR_SCHEDULE_BUTTERFLY, &pl) ==
-               AR_OK, "broadcast choice: create P=%d n=%lld", c.P, (long long)c.n);
-    if (!pl) continue;
-    ar_stats s;
-    EXPECT(ar_plan_stats(pl, &s) == AR_OK && s.fused_launches == 2, "broadcast choice: P=%d n=%lld not split", c.P,
-           (long long)c.n);
-    const int64_t stride = c.n + c.stride_extra;
-    std::vector<void*> bufs = fake_buffers(c.P, ((c.batch - 1) * stride + c.n) * 4 + 64);
-    bufs[size_t(c.P / 2)] = reinterpret_cast<char*>(bufs[size_t(c.P / 2)]) + c.misalign;
-    fake::launches.clear();
-    fake::last_regions = -1;
-    EXPECT(ar_execute_batched(pl, bufs.data(), c.batch, stride, stream_tag()) == AR_OK && fake::launches.size() == 2 &&
-               std::strcmp(fake::launches[1].kind, c.expect) == 0 && fake::last_regions == c.regions,
-           "broadcast choice: P=%d n=%lld batch %d stride +%lld misalign %zu took %s, expected %s", c.P,
-           (long long)c.n, c.batch, (long long)c.stride_extra, size_t(c.misalign),
-           fake::launches.size() == 2 ? fake::launches[1].kind : "?", c.expect);
-    ar_plan_destroy(pl);
-  }
+  for (const BcastCase& c : cases) check_broadcast_case(c);
+}
+
+static void check_broadcast_case(const BcastCase& c) {
+  ar_plan* pl = nullptr;
+  EXPECT(ar_plan_create_ex(c.P, c.n, AR_FLOAT32, AR_SUM, c.k, ar_group(c.group), AR_SCHEDULE_BUTTERFLY, &pl) ==
+             AR_OK, "broadcast choice: create P=%d n=%lld", c.P, (long long)c.n);
+  if (!pl) return;
+  ar_stats s;
+  EXPECT(ar_plan_stats(pl, &s) == AR_OK && s.fused_launches == 2, "broadcast choice: P=%d n=%lld not split", c.P,
+         (long long)c.n);
+  const int64_t stride = c.n + c.stride_extra;
+  std::vector<void*> bufs = fake_buffers(c.P, ((c.batch - 1) * stride + c.n) * 4 + 64);
+  bufs[size_t(c.P / 2)] = reinterpret_cast<char*>(bufs[size_t(c.P / 2)]) + c.misalign;
+  fake::launches.clear();
+  fake::last_regions = -1;
+  EXPECT(ar_execute_batched(pl, bufs.data(), c.batch, stride, stream_tag()) == AR_OK && fake::launches.size() == 2 &&
+             std::strcmp(fake::launches[1].kind, c.expect) == 0 && fake::last_regions == c.regions,
+         "broadcast choice: P=%d n=%lld batch %d stride +%lld misalign %zu took %s, expected %s", c.P,
+         (long long)c.n, c.batch, (long long)c.stride_extra, size_t(c.misalign),
+         fake::launches.size() == 2 ? fake::launches[1].kind : "?", c.expect);
+  ar_plan_destroy(pl);
+}
+
+// Block tiles (AR_FUSED_ROTATE=0) whose blocks all start on the chunk grid:
+// XCD regions from 104 ranks or from 32 MiB per rank, interleaved chunks
+// below.  Plans read the variable when they are created: single-threaded
+// only.
+static void broadcast_block_order() {
+  const BcastCase cases[] = {
+      {128, int64_t(1) << 21, 14, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},      // P >= 104: regions
+      {64, int64_t(1) << 22, 12, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 0},       // 16 MiB: interleaved
+      {64, int64_t(1) << 23, 12, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},       // 32 MiB: regions
+      {32, int64_t(1) << 24, 10, AR_GROUP_XOR, 1, 0, 0, "broadcast_stream", 1},       // 64 MiB
+      {64, int64_t(1) << 22, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 0},    // cyclic, 16 MiB
+      {64, int64_t(1) << 24, 12, AR_GROUP_CYCLIC, 1, 0, 0, "broadcast_stream", 1},    // cyclic, 64 MiB
+  };
+  setenv("AR_FUSED_ROTATE", "0", 1);
+  for (const BcastCase& c : cases) check_broadcast_case(c);
+  unsetenv("AR_FUSED_ROTATE");
 }
 
 // AR_BCAST_STREAM = 2 / 3: the destination-major copy with interleaved chunks
@@ -838,6 +861,7 @@ int main(int argc, char** argv) {
     execute_errors();
     broadcast_choice();
     broadcast_order_override();
+    broadcast_block_order();
     plans = sweep(1, 1, pmax);
   }
   std::printf("%d plans, %d launch contract problems, %d failures\n", plans, fake::problems.load(), fails.load());
