@@ -138,7 +138,7 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *                                   or at P = 24-48 with n * e up to
  *                                   32 MiB; bandwidth-optimal and Ring
  *                                   plans from P = 33 with n * e below
- *                                   256 MiB; XOR-group sums other than
+ *                                   256 MiB; XOR-group plans other than
  *                                   Recursive Doubling at any length);
  *   AR_FUSED_CAP = N or N,M         resident workgroups per CU of the fused
  *                                   launch (and of the broadcast); 0 is no

@@ -111,11 +111,13 @@ constexpr int64_t kRotShiftedSmallMaxBytes = int64_t(32) << 20;
 // within 4% either way with no consistent sign (the gradient-sync shape,
 // P = 24 at 64 MB: 4% more), so those keep block tiles.
 constexpr int32_t kRotOneMinP = 33;
-// The XOR group's sums, whose flat kernel leaves the block out, run on flat
-// columns on long blocks as well (Recursive Halving and the hybrids; not
-// Recursive Doubling, r = L, where block tiles were 1% faster at P = 32):
-// 1-7% less time at P = 8-128 with 16-64 MB per rank (P = 32 hybrids: 4%;
-// P = 128 at 16 MB, split: 7%), the same or better at every shape measured.
+// The XOR group's plans run on flat columns on long blocks as well
+// (Recursive Halving and the hybrids; Recursive Doubling, r = L, keeps block
+// tiles: 1% faster for sums and 14% for max at P = 32).  Sums, whose flat
+// kernel leaves the block out, took 1-7% less time at P = 8-128 with
+// 16-64 MB per rank (P = 32 hybrids: 4%; P = 128 at 16 MB, split: 7%), max,
+// whose flat kernel orders each pair by the lane's block, 0-6% less; the
+// same or better at every shape measured.
 constexpr int64_t kRotOneMaxBytes = int64_t(256) << 20;
 // Step launches whose blocks hold at most this many elements stream each
 // range's run of blocks as one flat space per rank (step_merged_kernel):
@@ -861,7 +863,7 @@ ar_status create_plan(int32_t P, int64_t n, ar_dtype dtype, ar_op op, int32_t k_
                     (small_p && (pl->op == AR_SUM || max_mid_p)));
     const bool rot_one = (pl->fused_kind == kFusedRing || (pl->fused_kind == kFusedCol && pl->s.r == 0)) &&
                          pl->s.P >= kRotOneMinP && pl->s.n * 4 < kRotOneMaxBytes;
-    const bool xor_long = pl->fused_kind == kFusedXor && pl->op == AR_SUM && pl->s.r < pl->s.L;
+    const bool xor_long = pl->fused_kind == kFusedXor && pl->s.r < pl->s.L;
     pl->fused_flat =
         kind && op_ok &&
         (pl->rotate_mode == 1 ||
