@@ -232,6 +232,22 @@ def test_default_layout_of_max_plans(P, n, k, flat):
         assert st.fused_flat == flat, (P, n, k, dtype)
 
 
+@pytest.mark.parametrize("P,n,k,op,flat", [
+    (32, 1 << 24, 10, "sum", 1),    # Recursive Halving on long blocks: flat columns
+    (32, 1 << 24, 7, "sum", 1),     # hybrid
+    (32, 1 << 24, 7, "max", 1),
+    (128, 1 << 22, 14, "max", 1),
+    (32, 1 << 24, 5, "sum", 0),     # Recursive Doubling keeps block tiles
+    (32, 1 << 24, 5, "max", 0),
+    (8, 1 << 24, 6, "sum", 1),
+])
+def test_xor_plans_on_long_blocks_take_flat_columns(P, n, k, op, flat, monkeypatch):
+    st = ar.Plan(P, n, "float32", op, k, group="xor").stats()
+    assert st.fused_flat == flat
+    monkeypatch.setenv("AR_FUSED_ROTATE", "0")
+    assert ar.Plan(P, n, "float32", op, k, group="xor").stats().fused_flat == 0
+
+
 @pytest.mark.parametrize("P,k,group,schedule,flat", [
     (24, 10, "cyclic", "butterfly", 1), (127, 14, "cyclic", "butterfly", 1), (24, 46, "cyclic", "ring", 1),
     (24, 7, "cyclic", "butterfly", 1), (48, 8, "cyclic", "butterfly", 1),  # shifted max at P = 24-48: rank slots
