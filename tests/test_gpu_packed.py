@@ -231,6 +231,7 @@ def test_random_batches_with_the_split_forced_either_way(P, n, B, stride, k, gro
     (32, 200, 13, 10, "xor", "butterfly"), (32, 200, 13, 7, "xor", "butterfly"), (128, 2000, 5, 14, "xor", "butterfly"),
     (24, 100, 17, 10, "cyclic", "butterfly"), (24, 100, 17, 46, "cyclic", "ring"), (127, 1000, 9, 14, "cyclic", "butterfly"),
     (37, 300, 9, 8, "cyclic", "butterfly"), (48, 4000, 3, 9, "cyclic", "butterfly"),  # shifted max in rank slots
+    (32, 32 * 300 + 7, 2, 7, "xor", "butterfly"), (64, 64 * 500, 1, 12, "xor", "butterfly"),  # XOR, long blocks
 ])
 def test_max_of_signed_zeros_follows_the_schedules_operand_order(P, n, B, k, group, schedule, monkeypatch):
     """Inputs of +0.0 and -0.0 only: a max of two zeros returns the kept
