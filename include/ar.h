@@ -101,9 +101,9 @@ typedef enum { AR_SUM = 0, AR_MAX = 1 } ar_op;
  *   AR_FUSED_SPLIT = 0|1            single fused launch, or reduce plus
  *                                   broadcast where every rank receives the
  *                                   same result (default: split for
- *                                   P >= 64, for P >= 32 when n * e is at
- *                                   least 64 MiB, and for P >= 33 in the
- *                                   rank-slot kernel on short blocks);
+ *                                   P >= 64, for P >= 24 when n * e is at
+ *                                   least 32 MiB, and for P >= 33 in the
+ *                                   rank-slot kernel);
  *   AR_BCAST_NT = 0|1               nontemporal loads and stores in that
  *                                   broadcast (default, for launches of 128
  *                                   MiB and more: the tiled copy with
@@ -181,9 +181,9 @@ typedef struct {
   int32_t group, schedule;           /* ar_group and ar_schedule of the plan              */
   int32_t fused_launches;            /* FUSED path: 1, or 2 when split into a reducing
                                         launch and a broadcast (every rank receives the
-                                        same result and P >= 64; P >= 32 when n * e is
-                                        at least 64 MiB; P >= 33 for sums with short
-                                        blocks outside the XOR group)                    */
+                                        same result and P >= 64; P >= 24 when n * e is
+                                        at least 32 MiB; P >= 33 in the rank-slot
+                                        kernel)                                          */
   int32_t fused_flat;                /* FUSED path with short blocks (sums; max in the
                                         bandwidth-optimal, Ring and XOR plans), and on
                                         long blocks the AR_FUSED_ROTATE defaults: 1

@@ -31,13 +31,14 @@ constexpr int64_t kFusedNtThresholdBytes = int64_t(128) << 20;
 // many ranks up (broadcast.hip): measured faster at P = 64 and 127, slower
 // at P = 24 and 48 (with the tiled broadcast).  Block-tiled plans whose
 // instance spans kSplitMidMinBytes per rank split from kSplitMidMinP ranks:
-// with the destination-major broadcast the pair's launches summed to 5-11%
-// less time than the single launch at P = 32-56, n = 2^24 (the second launch
-// adds about 10 us per call); at n = 2^22 from 9% less to 5% more, and at
-// P = 24 the call took 2.5% longer.
+// with the current destination-major broadcast whole calls took 5-9% less
+// time than the single launch at P = 24 and 28 with 32-128 MB per rank (the
+// gradient-sync shape, P = 24 at 64 MB: 7%; its Ring: 6%), 1% less at P = 16
+// (64 MB); the pair's launches summed to 5-11% less at P = 32-56 with 64 MB,
+// and at 16 MB from 9% less to 5% more.
 constexpr int32_t kSplitMinP = 64;
-constexpr int32_t kSplitMidMinP = 32;
-constexpr int64_t kSplitMidMinBytes = int64_t(64) << 20;
+constexpr int32_t kSplitMidMinP = 24;
+constexpr int64_t kSplitMidMinBytes = int64_t(32) << 20;
 // Flat short-block sums in the rank-slot kernel (not the XOR group's) split
 // from this many ranks up: their single launch streams 5.0-5.6 TB/s there and
 // the pair up to 6.0 (P = 37: 7%, P = 48: 15% faster with caps 4 and 2 and a

@@ -198,13 +198,16 @@ def test_random_plans_reproduce_oracle(case):
     (127, 127 * 100, 14, "cyclic", "butterfly", 2, 1),
     (127, 127 * 100, 252, "cyclic", "ring", 2, 1),
     (4, 4 * 100, 4, "cyclic", "butterfly", 1, 0),       # unsplit, below 33 ranks: block tiles
-    (24, 1 << 24, 10, "cyclic", "butterfly", 1, 0),
-    (24, 1 << 24, 46, "cyclic", "ring", 1, 0),
-    (32, 1 << 24, 10, "cyclic", "butterfly", 2, 0),     # block tiles split from 32 ranks at 64 MiB
+    (24, 1 << 24, 10, "cyclic", "butterfly", 2, 0),     # block tiles split from 24 ranks at 32 MiB
+    (24, 1 << 24, 46, "cyclic", "ring", 2, 0),
+    (24, 1 << 23, 10, "cyclic", "butterfly", 2, 0),
+    (24, (1 << 23) - 1024, 10, "cyclic", "butterfly", 1, 0),
+    (23, 1 << 24, 10, "cyclic", "butterfly", 1, 0),
+    (32, 1 << 24, 10, "cyclic", "butterfly", 2, 0),
     (33, 1 << 24, 12, "cyclic", "butterfly", 2, 1),
     (127, 1 << 26, 14, "cyclic", "butterfly", 2, 0),    # 256 MiB per rank: block tiles, split
-    (37, 1 << 26, 12, "cyclic", "butterfly", 2, 0),     # block tiles split from 32 ranks at 64 MiB
-    (24, 1 << 26, 10, "cyclic", "butterfly", 1, 0),
+    (37, 1 << 26, 12, "cyclic", "butterfly", 2, 0),     # block tiles, 256 MiB
+    (24, 1 << 26, 10, "cyclic", "butterfly", 2, 0),
     (37, 1 << 22, 8, "cyclic", "butterfly", 1, 1),      # shifted sums at P = 24-48 up to 32 MiB: rank slots
     (37, 1 << 24, 8, "cyclic", "butterfly", 1, 0),
     (127, 1 << 26, 10, "cyclic", "butterfly", 1, 1),    # shifted sums at odd P >= 97: rank slots
